@@ -1,0 +1,153 @@
+/*
+ * lora_oracle.c -- fp64 CPU oracle for the LoRA-adapted linear layer.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path (the HIP library
+ * and its Python binding) may include, link or call this file; only the
+ * tests, the smoke check and the benchmark's CPU-baseline leg use it.  It
+ * shares no code, header, table or helper with the GPU implementation.
+ *
+ * What it computes (paper: "Background -- Parameter-Efficient Fine-Tuning"
+ * describes LoRA as a frozen base weight plus a trained pair of rank-r
+ * factors; the hyperparameter table fixes r and alpha; the algorithm
+ * "On-the-fly Dequantization" fixes the frozen base forward y = W x and
+ * backward dx = W^T dy, with no weight gradient):
+ *
+ *     U  = X A^T                       [T,r]      (saved LoRA activation)
+ *     Y  = X W^T + s U B^T             [T,N]      s = alpha / r
+ *     G  = dY B                        [T,r]
+ *     dU = s G                         [T,r]
+ *     dX = dY W + dU A                 [T,K]
+ *     dA = dU^T X                      [r,K]
+ *     dB = s dY^T U                    [N,r]
+ *
+ * Shapes: X [T,K], W [N,K], A [r,K], B [N,r], dY [T,N]; K = d_in, N = d_out.
+ * The paper writes the base linear with column vectors (y = W x); here tokens
+ * are rows, so y = x W^T and dx = dy W.  dW is never formed.
+ *
+ * Every value is fp64; the inputs are exact upcasts of the bf16 (or fp32)
+ * values the GPU consumes.  Every sum runs over ascending index with plain
+ * accumulation (no Kahan, no blocking, no BLAS).  OpenMP only splits
+ * independent output rows or columns across threads; it never changes the
+ * order of any single sum.
+ *
+ * Each function is one line of the definition above, written out.
+ */
+#include <stddef.h>
+#include <stdint.h>
+
+/* U[t][j] = sum_k X[t][k] * A[j][k]  (LoRA down-projection, saved for the
+ * backward pass). */
+void oracle_lora_u(const double *X, const double *A, int64_t T, int64_t K,
+                   int64_t r, double *U) {
+#pragma omp parallel for schedule(static)
+  for (int64_t t = 0; t < T; ++t) {
+    for (int64_t j = 0; j < r; ++j) {
+      double acc = 0.0;
+      for (int64_t k = 0; k < K; ++k) acc += X[t * K + k] * A[j * K + k];
+      U[t * r + j] = acc;
+    }
+  }
+}
+
+/* Y[t][n] = sum_k X[t][k] * W[n][k] + s * sum_j U[t][j] * B[n][j]
+ * (frozen base contraction plus the scaled LoRA up-projection).
+ * rows == NULL computes every row t = 0..T-1 into Y[t]; otherwise row
+ * rows[i] is computed into Y[i] (i = 0..nrows-1). */
+void oracle_lora_y_rows(const double *X, const double *W, const double *U,
+                        const double *B, int64_t T, int64_t K, int64_t N,
+                        int64_t r, double s, const int64_t *rows,
+                        int64_t nrows, double *Y) {
+  int64_t count = rows ? nrows : T;
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < count; ++i) {
+    int64_t t = rows ? rows[i] : i;
+    for (int64_t n = 0; n < N; ++n) {
+      double base = 0.0;
+      for (int64_t k = 0; k < K; ++k) base += X[t * K + k] * W[n * K + k];
+      double lora = 0.0;
+      for (int64_t j = 0; j < r; ++j) lora += U[t * r + j] * B[n * r + j];
+      Y[i * N + n] = base + s * lora;
+    }
+  }
+}
+
+/* G[t][j] = sum_n dY[t][n] * B[n][j];  dU[t][j] = s * G[t][j]
+ * (gradient reaching the LoRA activation U). */
+void oracle_lora_grad_u(const double *dY, const double *B, int64_t T,
+                        int64_t N, int64_t r, double s, double *G,
+                        double *dU) {
+#pragma omp parallel for schedule(static)
+  for (int64_t t = 0; t < T; ++t) {
+    for (int64_t j = 0; j < r; ++j) {
+      double acc = 0.0;
+      for (int64_t n = 0; n < N; ++n) acc += dY[t * N + n] * B[n * r + j];
+      G[t * r + j] = acc;
+      dU[t * r + j] = s * acc;
+    }
+  }
+}
+
+/* dX[t][k] = sum_n dY[t][n] * W[n][k] + sum_j dU[t][j] * A[j][k]
+ * (input gradient through the frozen W and through the LoRA branch).
+ * Row selection as in oracle_lora_y_rows.  The sum over n is accumulated in
+ * ascending n for every k (a row of dX is built up one n at a time, which
+ * keeps each element's summation order ascending). */
+void oracle_lora_dx_rows(const double *dY, const double *W, const double *dU,
+                         const double *A, int64_t T, int64_t K, int64_t N,
+                         int64_t r, const int64_t *rows, int64_t nrows,
+                         double *dX) {
+  int64_t count = rows ? nrows : T;
+  (void)T;
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < count; ++i) {
+    int64_t t = rows ? rows[i] : i;
+    double *out = dX + i * K;
+    for (int64_t k = 0; k < K; ++k) out[k] = 0.0;
+    for (int64_t n = 0; n < N; ++n) {
+      double g = dY[t * N + n];
+      const double *wrow = W + n * K;
+      for (int64_t k = 0; k < K; ++k) out[k] += g * wrow[k];
+    }
+    /* The LoRA term is its own sum, added once to the base sum. */
+    for (int64_t k = 0; k < K; ++k) {
+      double lora = 0.0;
+      for (int64_t j = 0; j < r; ++j) lora += dU[t * r + j] * A[j * K + k];
+      out[k] += lora;
+    }
+  }
+}
+
+/* dA[j][k] = sum_t dU[t][j] * X[t][k]  (gradient of the down factor A). */
+void oracle_lora_da(const double *dU, const double *X, int64_t T, int64_t K,
+                    int64_t r, double *dA) {
+#pragma omp parallel for schedule(static)
+  for (int64_t k = 0; k < K; ++k) {
+    for (int64_t j = 0; j < r; ++j) {
+      double acc = 0.0;
+      for (int64_t t = 0; t < T; ++t) acc += dU[t * r + j] * X[t * K + k];
+      dA[j * K + k] = acc;
+    }
+  }
+}
+
+/* dB[n][j] = s * sum_t dY[t][n] * U[t][j]  (gradient of the up factor B). */
+void oracle_lora_db(const double *dY, const double *U, int64_t T, int64_t N,
+                    int64_t r, double s, double *dB) {
+#pragma omp parallel for schedule(static)
+  for (int64_t n = 0; n < N; ++n) {
+    for (int64_t j = 0; j < r; ++j) {
+      double acc = 0.0;
+      for (int64_t t = 0; t < T; ++t) acc += dY[t * N + n] * U[t * r + j];
+      dB[n * r + j] = s * acc;
+    }
+  }
+}
+
+/* Number of OpenMP threads the oracle runs with (1 when built without
+ * OpenMP); reported next to its timings. */
+#ifdef _OPENMP
+#include <omp.h>
+int oracle_threads(void) { return omp_get_max_threads(); }
+#else
+int oracle_threads(void) { return 1; }
+#endif

@@ -1,0 +1,265 @@
+"""Pins for the fp64 oracle: checks against facts fixed by the mathematics,
+not against the oracle's own formulas.
+
+Each pin takes a loaded oracle (``oracle.Oracle``) and raises AssertionError on
+failure.  ``ALL_PINS`` is run by ``test_oracle.py`` on the real oracle and by
+``test_oracle_mutants.py`` on deliberately broken copies of it, where at least
+one pin must fail for every planted mistake.
+
+The definitions being pinned (LoRA: frozen W plus a scaled rank-r update, from
+the paper's background on parameter-efficient fine-tuning; frozen-base forward
+and input gradient with no weight gradient, from its "On-the-fly
+Dequantization" algorithm; tokens as rows):
+    Y = X W^T + s (X A^T) B^T,  dX = dY W + s (dY B) A,
+    dA = s (dY B)^T X,          dB = s dY^T (X A^T).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+TIGHT = 1e-12
+
+
+def _rng(seed):
+    return np.random.default_rng(seed)
+
+
+def _rand_case(T, K, N, r, seed=0):
+    g = _rng(seed)
+    return dict(X=g.standard_normal((T, K)), W=g.standard_normal((N, K)),
+                A=g.standard_normal((r, K)), B=g.standard_normal((N, r)),
+                dY=g.standard_normal((T, N)))
+
+
+def _relmax(got, ref):
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    assert got.shape == ref.shape, (got.shape, ref.shape)
+    den = np.max(np.abs(ref)) if ref.size else 0.0
+    num = np.max(np.abs(got - ref)) if ref.size else 0.0
+    return num / den if den > 0 else num
+
+
+def _full(o, c, s):
+    U, Y = o.forward(c["X"], c["W"], c["A"], c["B"], s)
+    bw = o.backward(c["X"], c["W"], c["A"], c["B"], c["dY"], s, U=U)
+    return U, Y, bw
+
+
+def pin_scalar_closed_form(o):
+    """1x1x1 rank-1 case worked by hand: x=2, W=3, A=5, B=7, s=0.5, dy=11."""
+    X, W, A, B, dY, s = [[2.0]], [[3.0]], [[5.0]], [[7.0]], [[11.0]], 0.5
+    U, Y = o.forward(np.array(X), np.array(W), np.array(A), np.array(B), s)
+    bw = o.backward(np.array(X), np.array(W), np.array(A), np.array(B), np.array(dY), s, U=U)
+    assert U[0, 0] == 2.0 * 5.0
+    assert Y[0, 0] == 2.0 * 3.0 + 0.5 * (2.0 * 5.0) * 7.0          # 41
+    assert bw["G"][0, 0] == 11.0 * 7.0                              # 77
+    assert bw["dU"][0, 0] == 0.5 * 11.0 * 7.0                       # 38.5
+    assert bw["dX"][0, 0] == 11.0 * 3.0 + (0.5 * 11.0 * 7.0) * 5.0  # 225.5
+    assert bw["dA"][0, 0] == (0.5 * 11.0 * 7.0) * 2.0               # 77
+    assert bw["dB"][0, 0] == 0.5 * 11.0 * (2.0 * 5.0)               # 55
+
+
+def pin_small_closed_form(o):
+    """Hand-worked 1x2 -> 3 example with distinct entries, so a transposed or
+    mis-indexed operand changes the answer (T=1, K=2, N=3, r=1, s=2)."""
+    X = np.array([[1.0, 2.0]])
+    W = np.array([[1.0, 2.0], [3.0, 4.0], [5.0, 6.0]])   # rows are output features
+    A = np.array([[1.0, -1.0]])                          # U = 1 - 2 = -1
+    B = np.array([[1.0], [0.0], [2.0]])
+    dY = np.array([[1.0, 10.0, 100.0]])
+    s = 2.0
+    U, Y = o.forward(X, W, A, B, s)
+    assert U.tolist() == [[-1.0]]
+    # base: [1+4, 3+8, 5+12] = [5, 11, 17]; lora: s*U*B^T = -2*[1, 0, 2]
+    assert Y.tolist() == [[3.0, 11.0, 13.0]]
+    bw = o.backward(X, W, A, B, dY, s, U=U)
+    assert bw["G"].tolist() == [[1.0 + 0.0 + 200.0]]       # dY B = 201
+    assert bw["dU"].tolist() == [[402.0]]
+    # dY W = [1+30+500, 2+40+600] = [531, 642]; dU A = 402*[1, -1]
+    assert bw["dX"].tolist() == [[933.0, 240.0]]
+    assert bw["dA"].tolist() == [[402.0, 804.0]]            # dU^T X
+    assert bw["dB"].tolist() == [[-2.0], [-20.0], [-200.0]]  # s dY^T U
+
+
+def pin_rank0_textbook_gemm(o):
+    """r = 0 reduces to the plain GEMMs Y = X W^T and dX = dY W (numpy matmul)."""
+    c = _rand_case(7, 5, 6, 0, seed=1)
+    U, Y = o.forward(c["X"], c["W"], c["A"], c["B"], 2.0)
+    assert U.shape == (7, 0)
+    assert _relmax(Y, c["X"] @ c["W"].T) <= TIGHT
+    dX = o.frozen_dx(c["dY"], c["W"])
+    assert _relmax(dX, c["dY"] @ c["W"]) <= TIGHT
+
+
+def pin_down_projection_gemm(o):
+    """U = X A^T is itself a plain GEMM (numpy matmul)."""
+    c = _rand_case(9, 11, 4, 3, seed=2)
+    assert _relmax(o.u(c["X"], c["A"]), c["X"] @ c["A"].T) <= TIGHT
+
+
+def pin_finite_differences(o):
+    """L = sum(Y * dY) is affine in each of X, A, B, W taken alone, so central
+    differences are exact up to rounding: they must reproduce dX, dA, dB."""
+    T, K, N, r, s = 3, 5, 4, 2, 1.7
+    c = _rand_case(T, K, N, r, seed=3)
+    U, Y, bw = _full(o, c, s)
+
+    def loss(X, W, A, B):
+        _, Yp = o.forward(X, W, A, B, s)
+        return float(np.sum(Yp * c["dY"]))
+
+    h = 0.5
+    for name, grad in (("X", bw["dX"]), ("A", bw["dA"]), ("B", bw["dB"])):
+        base = c[name]
+        fd = np.zeros_like(base)
+        for idx in np.ndindex(base.shape):
+            args = {k: c[k].copy() for k in ("X", "W", "A", "B")}
+            args[name][idx] += h
+            lp = loss(args["X"], args["W"], args["A"], args["B"])
+            args[name][idx] -= 2 * h
+            lm = loss(args["X"], args["W"], args["A"], args["B"])
+            fd[idx] = (lp - lm) / (2 * h)
+        assert _relmax(grad, fd) <= 1e-9, (name, _relmax(grad, fd))
+
+
+def pin_dense_identities(o):
+    """With W_eff = W + s B A (the merged LoRA weight):
+    Y = X W_eff^T, dX = dY W_eff, dA = s B^T (dY^T X), dB = s (dY^T X) A^T."""
+    T, K, N, r, s = 6, 8, 5, 3, 2.0
+    c = _rand_case(T, K, N, r, seed=4)
+    U, Y, bw = _full(o, c, s)
+    W_eff = c["W"] + s * (c["B"] @ c["A"])
+    G_xy = c["dY"].T @ c["X"]            # the dW that the method never forms, [N, K]
+    assert _relmax(Y, c["X"] @ W_eff.T) <= TIGHT
+    assert _relmax(bw["dX"], c["dY"] @ W_eff) <= TIGHT
+    assert _relmax(bw["dA"], s * (c["B"].T @ G_xy)) <= TIGHT
+    assert _relmax(bw["dB"], s * (G_xy @ c["A"].T)) <= TIGHT
+
+
+def pin_zero_B(o):
+    """B = 0: Y equals the rank-0 result bitwise, dA is exactly 0, dB = s dY^T U."""
+    c = _rand_case(5, 8, 6, 2, seed=5)
+    c["B"][:] = 0.0
+    s = 2.0
+    U, Y, bw = _full(o, c, s)
+    _, Y0 = o.forward(c["X"], c["W"], c["A"][:0], c["B"][:, :0], s)
+    assert np.array_equal(Y, Y0)
+    assert np.all(bw["dA"] == 0.0)
+    assert _relmax(bw["dB"], s * (c["dY"].T @ (c["X"] @ c["A"].T))) <= TIGHT
+    assert np.any(bw["dB"] != 0.0)
+
+
+def pin_zero_A(o):
+    """A = 0: U = 0, Y = X W^T, dB is exactly 0, dA = s (dY B)^T X."""
+    c = _rand_case(5, 8, 6, 2, seed=6)
+    c["A"][:] = 0.0
+    s = 2.0
+    U, Y, bw = _full(o, c, s)
+    assert np.all(U == 0.0)
+    assert _relmax(Y, c["X"] @ c["W"].T) <= TIGHT
+    assert np.all(bw["dB"] == 0.0)
+    assert _relmax(bw["dA"], s * ((c["dY"] @ c["B"]).T @ c["X"])) <= TIGHT
+
+
+def pin_zero_W(o):
+    """W = 0 isolates the LoRA branch: Y = s U B^T, dX = dU A."""
+    c = _rand_case(5, 8, 6, 3, seed=7)
+    c["W"][:] = 0.0
+    s = 3.0
+    U, Y, bw = _full(o, c, s)
+    assert _relmax(Y, s * (c["X"] @ c["A"].T) @ c["B"].T) <= TIGHT
+    assert _relmax(bw["dX"], (s * (c["dY"] @ c["B"])) @ c["A"]) <= TIGHT
+
+
+def pin_linear_in_scale(o):
+    """Y(s) - Y(0) is proportional to s; dA, dB and dU are proportional to s."""
+    c = _rand_case(4, 8, 5, 2, seed=8)
+    _, Y0, _ = _full(o, c, 0.0)
+    _, Y1, b1 = _full(o, c, 1.0)
+    _, Y3, b3 = _full(o, c, 3.0)
+    assert _relmax(Y3 - Y0, 3.0 * (Y1 - Y0)) <= 1e-11
+    for k in ("dA", "dB", "dU"):
+        assert _relmax(b3[k], 3.0 * b1[k]) <= TIGHT, k
+
+
+def pin_token_split_additivity(o):
+    """dA and dB are sums over tokens: the gradient over T equals the sum of the
+    gradients over a split T = T1 + T2 (the data-parallel decomposition)."""
+    c = _rand_case(9, 8, 6, 3, seed=9)
+    s = 2.0
+    _, _, full = _full(o, c, s)
+    parts = []
+    for sl in (slice(0, 4), slice(4, 9)):
+        cc = dict(c, X=c["X"][sl], dY=c["dY"][sl])
+        parts.append(_full(o, cc, s)[2])
+    for k in ("dA", "dB"):
+        assert _relmax(full[k], parts[0][k] + parts[1][k]) <= TIGHT, k
+    # per-token outputs are the concatenation of the parts
+    assert _relmax(full["dX"], np.concatenate([parts[0]["dX"], parts[1]["dX"]])) <= TIGHT
+
+
+def pin_row_permutation(o):
+    """Permuting token rows permutes Y, dX, U, G and leaves dA, dB unchanged."""
+    c = _rand_case(8, 8, 6, 2, seed=10)
+    s = 2.0
+    U, Y, bw = _full(o, c, s)
+    perm = _rng(11).permutation(8)
+    cp = dict(c, X=c["X"][perm], dY=c["dY"][perm])
+    Up, Yp, bwp = _full(o, cp, s)
+    assert _relmax(Yp, Y[perm]) <= TIGHT
+    assert _relmax(Up, U[perm]) <= TIGHT
+    assert _relmax(bwp["dX"], bw["dX"][perm]) <= TIGHT
+    assert _relmax(bwp["G"], bw["G"][perm]) <= TIGHT
+    for k in ("dA", "dB"):
+        assert _relmax(bwp[k], bw[k]) <= TIGHT, k
+
+
+def pin_row_sampling(o):
+    """Row-sampled Y and dX equal the corresponding rows of the full result."""
+    c = _rand_case(10, 8, 6, 2, seed=12)
+    s = 2.0
+    U, Y, bw = _full(o, c, s)
+    rows = [0, 3, 9]
+    _, Ys = o.forward(c["X"], c["W"], c["A"], c["B"], s, rows=rows)
+    assert np.array_equal(Ys, Y[rows])
+    dXs = o.dx(c["dY"], c["W"], bw["dU"], c["A"], rows=rows)
+    assert np.array_equal(dXs, bw["dX"][rows])
+
+
+def pin_torch_autograd(o):
+    """Independent library route: torch fp64 autograd of the LoRA forward."""
+    import torch
+
+    T, K, N, r, s = 6, 10, 7, 3, 2.0
+    c = _rand_case(T, K, N, r, seed=13)
+    t = {k: torch.tensor(v, dtype=torch.float64, requires_grad=(k in ("X", "A", "B")))
+         for k, v in c.items()}
+    Y_t = torch.nn.functional.linear(t["X"], t["W"]) + \
+        s * torch.nn.functional.linear(torch.nn.functional.linear(t["X"], t["A"]), t["B"])
+    Y_t.backward(t["dY"])
+    U, Y, bw = _full(o, c, s)
+    assert _relmax(Y, Y_t.detach().numpy()) <= TIGHT
+    assert _relmax(bw["dX"], t["X"].grad.numpy()) <= TIGHT
+    assert _relmax(bw["dA"], t["A"].grad.numpy()) <= TIGHT
+    assert _relmax(bw["dB"], t["B"].grad.numpy()) <= TIGHT
+
+
+ALL_PINS = [
+    pin_scalar_closed_form, pin_small_closed_form, pin_rank0_textbook_gemm,
+    pin_down_projection_gemm, pin_finite_differences, pin_dense_identities,
+    pin_zero_B, pin_zero_A, pin_zero_W, pin_linear_in_scale,
+    pin_token_split_additivity, pin_row_permutation, pin_row_sampling,
+    pin_torch_autograd,
+]
+
+
+def run_all(o) -> list:
+    """Run every pin; return the names of those that failed (or raised)."""
+    failed = []
+    for pin in ALL_PINS:
+        try:
+            pin(o)
+        except Exception:  # noqa: BLE001 -- any error means the pin caught something
+            failed.append(pin.__name__)
+    return failed

@@ -1,0 +1,67 @@
+"""Mutation check of the oracle's pins (CPU only).
+
+Each case plants one plausible mistake into a private copy of the oracle's C
+source (a dropped term, a wrong sign, a transposed operand, a wrong loop
+bound), compiles it into a temporary shared object and runs every pin against
+it in a child process.  The pins must reject every mutant; a mutant that
+crashes the child (an out-of-bounds index) counts as rejected too.
+"""
+import os
+import subprocess
+import sys
+import textwrap
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "lora_oracle.c")
+
+# (id, original text, mutated text) -- each original must occur exactly once.
+MUTANTS = [
+    ("u_transposed_A", "acc += X[t * K + k] * A[j * K + k];", "acc += X[t * K + k] * A[k * r + j];"),
+    ("u_short_loop", "for (int64_t k = 0; k < K; ++k) acc += X[t * K + k] * A[j * K + k];",
+     "for (int64_t k = 1; k < K; ++k) acc += X[t * K + k] * A[j * K + k];"),
+    ("y_transposed_W", "base += X[t * K + k] * W[n * K + k];", "base += X[t * K + k] * W[k * N + n];"),
+    ("y_short_loop", "for (int64_t k = 0; k < K; ++k) base +=", "for (int64_t k = 0; k + 1 < K; ++k) base +="),
+    ("y_dropped_scale", "Y[i * N + n] = base + s * lora;", "Y[i * N + n] = base + lora;"),
+    ("y_wrong_sign", "Y[i * N + n] = base + s * lora;", "Y[i * N + n] = base - s * lora;"),
+    ("y_dropped_lora", "Y[i * N + n] = base + s * lora;", "Y[i * N + n] = base;"),
+    ("y_transposed_B", "lora += U[t * r + j] * B[n * r + j];", "lora += U[t * r + j] * B[j * N + n];"),
+    ("grad_u_unscaled", "dU[t * r + j] = s * acc;", "dU[t * r + j] = acc;"),
+    ("grad_u_transposed_B", "acc += dY[t * N + n] * B[n * r + j];", "acc += dY[t * N + n] * B[j * N + n];"),
+    ("dx_dropped_lora", "out[k] += lora;", "out[k] += 0.0 * lora;"),
+    ("dx_wrong_row_of_W", "const double *wrow = W + n * K;", "const double *wrow = W + (N - 1 - n) * K;"),
+    ("dx_transposed_A", "lora += dU[t * r + j] * A[j * K + k];", "lora += dU[t * r + j] * A[k * r + j];"),
+    ("da_wrong_sign", "acc += dU[t * r + j] * X[t * K + k];", "acc -= dU[t * r + j] * X[t * K + k];"),
+    ("da_first_token_only", "for (int64_t t = 0; t < T; ++t) acc += dU[t * r + j] * X[t * K + k];",
+     "for (int64_t t = 0; t < 1; ++t) acc += dU[t * r + j] * X[t * K + k];"),
+    ("db_unscaled", "dB[n * r + j] = s * acc;", "dB[n * r + j] = acc;"),
+    ("db_transposed_U", "acc += dY[t * N + n] * U[t * r + j];", "acc += dY[t * N + n] * U[j * T + t];"),
+]
+
+CHILD = textwrap.dedent("""
+    import sys
+    sys.path[:0] = [{root!r}, {tests!r}]
+    import oracle, oracle_pins
+    o = oracle.load({lib!r})
+    failed = oracle_pins.run_all(o)
+    print("FAILED_PINS", ",".join(failed))
+    sys.exit(0 if failed else 3)
+""")
+
+
+@pytest.mark.parametrize("mid,orig,mut", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_pins_reject_mutant(tmp_path, mid, orig, mut):
+    src = open(SRC).read()
+    assert src.count(orig) == 1, f"mutation anchor for {mid} not unique/found"
+    msrc = tmp_path / "mutant.c"
+    msrc.write_text(src.replace(orig, mut))
+    lib = tmp_path / "libmutant.so"
+    subprocess.run(["gcc", "-O2", "-fPIC", "-shared", "-std=c11", "-o", str(lib), str(msrc)],
+                   check=True)
+    code = CHILD.format(root=ROOT, tests=os.path.join(ROOT, "tests"), lib=str(lib))
+    env = dict(os.environ, OMP_NUM_THREADS="1")
+    p = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, env=env,
+                       timeout=300)
+    # exit 0: at least one pin failed (mutant caught); a crash is also a catch.
+    assert p.returncode != 3, f"mutant {mid} passed every pin:\n{p.stdout}\n{p.stderr}"
