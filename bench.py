@@ -1,0 +1,225 @@
+"""Benchmark of the LoRA-linear hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+One step = the forward of every LoRA linear of the workload, then the
+backward of each in reverse order (u saved by the forward is reused), plus the
+frozen LM head's dx when the workload has one.  Inputs are synthetic (seeded
+Gaussian, bf16) and resident in HBM before timing starts.  Prints one JSON
+line: throughput in TFLOP/s of algorithmic work (4TKN + 6Tr(K+N) per LoRA
+linear, 2TKN per frozen dx), the dominant kernel's roofline position measured
+with HIP events around its launches, peak workspace bytes, and the fp64 CPU
+oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import paper_2606_19528_amd as lm  # noqa: E402
+from workloads import WORKLOADS, frozen_inputs, linear_seed, lora_inputs  # noqa: E402
+
+METRIC = "LoRA linear fwd+bwd TFLOP/s (% bf16 MFMA peak) + peak device workspace bytes"
+PEAK_BF16_TFLOPS = 2516.6   # 256 CU x 4096 dense bf16 flop/clk x 2.4 GHz
+PEAK_HBM_GBS = 8000.0
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+class Layer:
+    """Device buffers of one LoRA linear (inputs, outputs, workspace)."""
+
+    def __init__(self, lin, T, seed, dev):
+        self.lin = lin
+        K, N, r = lin.d_in, lin.d_out, lin.rank
+        inp = lora_inputs(T, K, N, r, seed=seed, device=dev)
+        self.x, self.W, self.A, self.B, self.dy = (inp[k] for k in ("x", "W", "A", "B", "dy"))
+        self.y = torch.empty(T, N, dtype=torch.bfloat16, device=dev)
+        self.u = torch.empty(T, r, dtype=torch.float32, device=dev)
+        self.dx = torch.empty(T, K, dtype=torch.bfloat16, device=dev)
+        self.dA = torch.empty(r, K, dtype=torch.float32, device=dev)
+        self.dB = torch.empty(N, r, dtype=torch.float32, device=dev)
+        self.T = T
+
+
+def build(workload, dev):
+    T = workload.tokens
+    layers = []
+    for layer in range(workload.layers):
+        for idx, lin in enumerate(workload.linears):
+            layers.append(Layer(lin, T, linear_seed(0, layer, idx), dev))
+    head = None
+    if workload.head is not None:
+        h = workload.head
+        hi = frozen_inputs(T, h.d_in, h.d_out, seed=10_000, device=dev)
+        head = (hi["dy"], hi["W"], torch.empty(T, h.d_in, dtype=torch.bfloat16, device=dev))
+    ws_bytes = 0
+    for L in layers:
+        K, N, r = L.lin.d_in, L.lin.d_out, L.lin.rank
+        ws_bytes = max(ws_bytes,
+                       lm.lora_linear_workspace_bytes(lm.LORA_OP_FWD, T, K, N, r, lm.LORA_BF16),
+                       lm.lora_linear_workspace_bytes(lm.LORA_OP_BWD, T, K, N, r, lm.LORA_BF16))
+    ws = torch.empty(max(ws_bytes, 256), dtype=torch.uint8, device=dev)
+    return layers, head, ws, ws_bytes
+
+
+def step(layers, head, ws):
+    for L in layers:
+        lm.lora_linear_fwd(L.x, L.W, L.A, L.B, L.y, L.u, L.lin.scale, ws=ws)
+    if head is not None:
+        lm.frozen_linear_bwd_dx(head[0], head[1], head[2])
+    for L in reversed(layers):
+        lm.lora_linear_bwd(L.x, L.W, L.A, L.B, L.u, L.dy, L.dx, L.dA, L.dB, L.lin.scale, ws=ws)
+
+
+def kernel_flops(workload):
+    """Algorithmic flops of one launch of each GEMM kernel, per linear shape."""
+    T = workload.tokens
+    per = {}
+    for lin in workload.linears:
+        K, N, r = lin.d_in, lin.d_out, lin.rank
+        per.setdefault("gemm_fwd", []).append(2.0 * T * N * (K + r))
+        per.setdefault("gemm_bwd_dx", []).append(2.0 * T * K * (N + r))
+    if workload.head is not None:
+        per["gemm_frozen_dx"] = [2.0 * T * workload.head.d_in * workload.head.d_out]
+    return per
+
+
+def cpu_baseline(workload, layers, target_s=12.0):
+    """The fp64 oracle (as it stands) timed on the host on a bounded sample:
+    the full fwd+bwd of the workload's first linear over its first Ts tokens,
+    Ts chosen so the run takes about `target_s` seconds."""
+    import oracle
+
+    orc = oracle.load()
+    L = layers[0]
+    K, N, r, s = L.lin.d_in, L.lin.d_out, L.lin.rank, L.lin.scale
+    cpu = {k: getattr(L, k).cpu() for k in ("x", "W", "A", "B", "dy")}
+
+    def run(Ts):
+        inp = {k: (v[:Ts] if k in ("x", "dy") else v) for k, v in cpu.items()}
+        t0 = time.perf_counter()
+        U = orc.u(inp["x"], inp["A"])
+        orc.y(inp["x"], inp["W"], U, inp["B"], s)
+        _, dU = orc.grad_u(inp["dy"], inp["B"], s)
+        orc.dx(inp["dy"], inp["W"], dU, inp["A"])
+        orc.da(dU, inp["x"])
+        orc.db(inp["dy"], U, s)
+        return time.perf_counter() - t0
+
+    def flops(Ts):
+        return 4.0 * Ts * K * N + 6.0 * Ts * r * (K + N)
+
+    Ts = 8
+    t = run(Ts)
+    Ts = int(max(8, min(L.T, Ts * target_s / max(t, 1e-3))))
+    t = run(Ts)
+    return {"value": flops(Ts) / t / 1e12, "unit": "TFLOP/s", "cores": orc.threads(),
+            "kind": "oracle",
+            "sample": f"full fwd+bwd of {L.lin.name} ({K}->{N}, r={r}) over the first {Ts} of "
+                      f"{L.T} tokens, {t:.1f} s, fp64 C loops (OpenMP)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="llama_q_proj", choices=sorted(WORKLOADS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}): the LoRA hot path is "
+              "measured on one MI355X; multi-GPU data parallelism is a design note, not a "
+              "measured configuration.", file=sys.stderr)
+        sys.exit(2)
+
+    w = WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    log(f"[bench] workload {w.key}: {w.description}")
+    layers, head, ws, ws_bytes = build(w, dev)
+    torch.cuda.synchronize()
+    base_mem = torch.cuda.memory_allocated()
+    torch.cuda.reset_peak_memory_stats()
+
+    for _ in range(args.warmup):
+        step(layers, head, ws)
+    torch.cuda.synchronize()
+    log(f"[bench] warmup {args.warmup} done")
+
+    # Timed region: plain steps.
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(args.steps):
+        step(layers, head, ws)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    log(f"[bench] {args.steps} steps: {ms:.4f} ms/step")
+    extra_peak = torch.cuda.max_memory_allocated() - base_mem
+
+    # Same steps again with the library's HIP-event hook around every kernel.
+    lm.profiler_reset()
+    lm.profiler_enable(True)
+    for _ in range(args.steps):
+        step(layers, head, ws)
+    torch.cuda.synchronize()
+    lm.profiler_enable(False)
+    per_kernel = {}
+    for name in lm.kernel_names():
+        tot, n = lm.profiler_read(name)
+        if n:
+            per_kernel[name] = (tot, n)
+    lm.profiler_reset()
+    dom = max(per_kernel, key=lambda k: per_kernel[k][0])
+    kf = kernel_flops(w)
+    launch_flops = sum(kf[dom]) / len(kf[dom]) if dom in kf else None
+    tot, n = per_kernel[dom]
+    avg_ms = tot / n
+    roofline = None
+    if launch_flops is not None:
+        achieved = launch_flops / (avg_ms * 1e-3) / 1e12
+        roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+                    "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                    "traffic": None, "kernel": dom, "avg_launch_us": round(avg_ms * 1e3, 3)}
+    log("[bench] per-kernel (ms total, launches): " +
+        ", ".join(f"{k}={v[0]:.3f}/{v[1]}" for k, v in per_kernel.items()))
+
+    flops = w.flops_per_step()
+    value = flops / (ms * 1e-3) / 1e12
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.key, "tokens": w.tokens,
+                   "linears": [[l.name, l.d_in, l.d_out, l.rank, l.alpha] for l in w.linears],
+                   "layers": w.layers,
+                   "head": None if w.head is None else [w.head.d_in, w.head.d_out],
+                   "parallelism": "single GPU"},
+        "frac_bf16_peak": round(value / PEAK_BF16_TFLOPS, 4),
+        "peak_workspace_bytes": int(ws_bytes),
+        "peak_extra_device_bytes_during_steps": int(extra_peak),
+        "frozen_weight_bytes": int(w.frozen_weight_bytes()),
+        "roofline": roofline,
+        "kernels_ms_per_step": {k: round(v[0] / args.steps, 5) for k, v in per_kernel.items()},
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] cpu baseline (oracle) ...")
+        out["cpu_baseline"] = cpu_baseline(w, layers)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,140 @@
+/*
+ * lora_mi355x.h -- C ABI of the MI355X (gfx950) LoRA-linear library.
+ *
+ * The operation (LoRA as described in the paper's background on
+ * parameter-efficient fine-tuning: a frozen base weight W plus a trained
+ * rank-r pair A, B; r and alpha from its hyperparameter table; the frozen-base
+ * forward y = W x and input gradient dx = W^T dy, with no weight gradient,
+ * from its algorithm "On-the-fly Dequantization"), with tokens as rows:
+ *
+ *   forward   u  = x A^T                      [T, r]   (fp32, kept for bwd)
+ *             y  = x W^T + s u B^T            [T, d_out]
+ *   backward  du = s dy B                     [T, r]
+ *             dx = dy W + du A                [T, d_in]
+ *             dA = du^T x                     [r, d_in]   (fp32)
+ *             dB = s dy^T u                   [d_out, r]  (fp32)
+ *   s = alpha / r.  W is frozen: dW = dy^T x is never formed or allocated.
+ *
+ * Layouts (all row-major, leading dimension = row length, no padding):
+ *   x [T, d_in], W [d_out, d_in], A [r, d_in], B [d_out, r], y/dy [T, d_out],
+ *   dx [T, d_in], u [T, r] fp32, dA [r, d_in] fp32, dB [d_out, r] fp32.
+ *
+ * Element types: x, W, A, B, dy, y, dx have the type `dt` (bf16 with fp32
+ * accumulation, or fp32 end to end as a check mode); u, dA, dB are fp32.
+ * In bf16 mode the products s*u and du are rounded to bf16 (round to nearest
+ * even) before they enter the matrix cores; y and dx are rounded once, from
+ * the fp32 accumulator.
+ *
+ * Ownership: every pointer is a device pointer owned by the caller.  The
+ * library never allocates device memory and keeps no pointer after a call
+ * returns.  Scratch space comes from the caller's workspace `ws` of
+ * `ws_bytes` bytes (size it with lora_linear_workspace_bytes); its contents
+ * on entry are ignored and on return are unspecified.
+ *
+ * Streams: all work is enqueued on `hip_stream` (a hipStream_t; NULL = the
+ * null stream) and the call returns without synchronising.  Two calls that
+ * share a workspace must be ordered on one stream.
+ *
+ * Errors: every entry point validates all arguments before enqueuing any
+ * work, so nothing is written when it returns an error.  It returns
+ *   LORA_EINVAL        a NULL required pointer, a pointer not 16-byte
+ *                      aligned, a size < 1, r outside [0,128], a non-finite
+ *                      scale, or an output overlapping an input or another
+ *                      output;
+ *   LORA_EUNSUPPORTED  d_in or d_out not a multiple of 8, or a matrix with
+ *                      2^31 or more elements;
+ *   LORA_EWORKSPACE    ws_bytes below the required size (or ws NULL when
+ *                      the required size is non-zero);
+ *   LORA_EHIP          a kernel launch failed (asynchronous device faults
+ *                      surface at the caller's next stream synchronisation).
+ * lora_last_error() returns a short text for the calling thread's last error.
+ * No entry point prints, aborts or throws.
+ *
+ * Determinism: no atomics on any path; reductions over tokens use fixed-order
+ * partial sums, so identical inputs give bitwise identical outputs.
+ */
+#ifndef LORA_MI355X_H
+#define LORA_MI355X_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  LORA_OK = 0,
+  LORA_EINVAL = 1,
+  LORA_EUNSUPPORTED = 2,
+  LORA_EWORKSPACE = 3,
+  LORA_EHIP = 4
+} lora_status_t;
+
+typedef enum { LORA_BF16 = 0, LORA_F32 = 1 } lora_dtype_t;
+
+typedef enum { LORA_OP_FWD = 0, LORA_OP_BWD = 1, LORA_OP_FROZEN_DX = 2 } lora_op_t;
+
+/* Workspace bytes sufficient for any call of `op` with these sizes, whether
+ * or not the optional u pointers are given.  Returns 0 when none is needed
+ * and (size_t)-1 for sizes the entry point would reject.  Pure host logic. */
+size_t lora_linear_workspace_bytes(lora_op_t op, int64_t T, int64_t d_in, int64_t d_out,
+                                   int64_t r, lora_dtype_t dt);
+
+/* LoRA forward (the definitions above): y = x W^T + s (x A^T) B^T.
+ *   u_save  optional [T, r] fp32 output receiving u = x A^T (unscaled) for the
+ *           backward pass; NULL keeps u in the workspace only.
+ *   r = 0   gives the plain frozen linear y = x W^T; A, B, u_save are ignored
+ *           and may be NULL.
+ *   scale   s = alpha / r, any finite value. */
+lora_status_t lora_linear_fwd(const void *x, const void *W, const void *A, const void *B,
+                              void *y, float *u_save, int64_t T, int64_t d_in, int64_t d_out,
+                              int64_t r, float scale, lora_dtype_t dt, void *ws,
+                              size_t ws_bytes, void *hip_stream);
+
+/* LoRA backward: dx = dy W + du A, dA = du^T x, dB = s dy^T u, du = s dy B.
+ *   u_saved  [T, r] fp32 from lora_linear_fwd, or NULL to recompute u = x A^T
+ *            (activation rematerialisation in place of storing it).
+ *   dx       may be NULL when the input gradient is not needed.
+ *   dA, dB   required when r > 0; ignored (may be NULL) when r = 0, in which
+ *            case the call computes dx = dy W only.
+ *   Outputs are overwritten, not accumulated. */
+lora_status_t lora_linear_bwd(const void *x, const void *W, const void *A, const void *B,
+                              const float *u_saved, const void *dy, void *dx, float *dA,
+                              float *dB, int64_t T, int64_t d_in, int64_t d_out, int64_t r,
+                              float scale, lora_dtype_t dt, void *ws, size_t ws_bytes,
+                              void *hip_stream);
+
+/* Rank-0 frozen linear input gradient, dx = dy W (the frozen LM head of the
+ * paper's checkpointing scheme, whose backward needs only dx):
+ *   dy [T, d_out], W [d_out, d_in], dx [T, d_in]. */
+lora_status_t frozen_linear_bwd_dx(const void *dy, const void *W, void *dx, int64_t T,
+                                   int64_t d_in, int64_t d_out, lora_dtype_t dt, void *ws,
+                                   size_t ws_bytes, void *hip_stream);
+
+/* Static text for a status code. */
+const char *lora_status_str(lora_status_t status);
+
+/* Text describing the calling thread's most recent error ("" if none). */
+const char *lora_last_error(void);
+
+/* Benchmark timing hook.  While enabled, every launch of a library kernel is
+ * bracketed by a pair of hipEvents recorded on the stream it runs on.
+ * lora_profiler_read() waits for the recorded events of kernel `kernel_id`
+ * (see lora_kernel_name) and returns their summed duration in milliseconds
+ * and the number of launches; lora_profiler_reset() drops all records.
+ * Returns LORA_EINVAL for an unknown id, LORA_EHIP on an event failure. */
+lora_status_t lora_profiler_enable(int on);
+lora_status_t lora_profiler_reset(void);
+lora_status_t lora_profiler_read(int kernel_id, double *total_ms, int64_t *launches);
+
+/* Name of library kernel `kernel_id` (0 .. lora_kernel_count()-1), NULL if
+ * out of range. */
+const char *lora_kernel_name(int kernel_id);
+int lora_kernel_count(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LORA_MI355X_H */

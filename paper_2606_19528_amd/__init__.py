@@ -1,0 +1,8 @@
+"""MI355X (gfx950) LoRA-linear hot path: HIP kernels behind a C ABI.
+
+The Python names mirror the C entry points of include/lora_mi355x.h.
+"""
+from .lora import (LORA_BF16, LORA_F32, LORA_OP_BWD, LORA_OP_FROZEN_DX, LORA_OP_FWD,  # noqa: F401
+                   LoraError, frozen_linear_bwd_dx, kernel_names, lib, lora_linear_bwd,
+                   lora_linear_fwd, lora_linear_workspace_bytes, profiler_enable,
+                   profiler_read, profiler_reset)

@@ -1,0 +1,401 @@
+// api.cpp -- the C ABI: argument validation, workspace layout and the launch
+// sequence of each entry point.  Every argument is checked before any work is
+// enqueued; the library allocates no device memory.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <vector>
+
+#include "../../include/lora_mi355x.h"
+#include "launch.hpp"
+
+using namespace lora;
+
+namespace {
+
+thread_local char g_err[256] = "";
+
+lora_status_t fail(lora_status_t s, const char *msg) {
+  std::snprintf(g_err, sizeof g_err, "%s", msg);
+  return s;
+}
+
+// ----- kernel timing hook ----------------------------------------------------
+enum KernelId {
+  K_GEMM_FWD = 0,     // y  = x W^T + (s u) B^T
+  K_GEMM_BWD_DX,      // dx = dy W + du A
+  K_GEMM_FROZEN_DX,   // dx = dy W (rank 0)
+  K_LORA_DOWN,        // u  = x A^T
+  K_LORA_DY_B,        // du = s dy B
+  K_DB_PARTS,         // dB partial sums over token chunks
+  K_DA_PARTS,         // dA partial sums over token chunks
+  K_REDUCE_PARTS,     // fixed-order sum of the partials
+  K_COUNT
+};
+const char *kKernelNames[K_COUNT] = {"gemm_fwd",   "gemm_bwd_dx", "gemm_frozen_dx",
+                                     "lora_down",  "lora_dy_b",   "db_parts",
+                                     "da_parts",   "reduce_parts"};
+
+struct EventPair {
+  hipEvent_t a, b;
+};
+std::mutex g_prof_mu;
+bool g_prof_on = false;
+std::vector<EventPair> g_prof[K_COUNT];
+
+struct Timed {
+  int id;
+  hipStream_t st;
+  EventPair ev{nullptr, nullptr};
+  bool on = false;
+  Timed(int id_, hipStream_t st_) : id(id_), st(st_) {
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    if (!g_prof_on) return;
+    if (hipEventCreate(&ev.a) != hipSuccess || hipEventCreate(&ev.b) != hipSuccess) return;
+    on = hipEventRecord(ev.a, st) == hipSuccess;
+  }
+  void done() {
+    if (!on) return;
+    if (hipEventRecord(ev.b, st) != hipSuccess) return;
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    g_prof[id].push_back(ev);
+    on = false;
+  }
+};
+
+// ----- validation helpers ------------------------------------------------------
+constexpr int64_t kMaxElems = (int64_t(1) << 31) - 1;
+constexpr int kMaxRank = 128;
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+struct Range {
+  uintptr_t lo, hi;  // [lo, hi)
+  bool set;
+};
+Range rng(const void *p, int64_t bytes) {
+  if (!p || bytes <= 0) return {0, 0, false};
+  uintptr_t lo = reinterpret_cast<uintptr_t>(p);
+  return {lo, lo + (uintptr_t)bytes, true};
+}
+bool overlap(const Range &a, const Range &b) {
+  return a.set && b.set && a.lo < b.hi && b.lo < a.hi;
+}
+bool any_overlap(const std::vector<Range> &outs, const std::vector<Range> &ins) {
+  for (size_t i = 0; i < outs.size(); ++i) {
+    for (const Range &x : ins)
+      if (overlap(outs[i], x)) return true;
+    for (size_t j = i + 1; j < outs.size(); ++j)
+      if (overlap(outs[i], outs[j])) return true;
+  }
+  return false;
+}
+
+size_t esize(lora_dtype_t dt) { return dt == LORA_BF16 ? 2 : 4; }
+size_t round256(size_t b) { return (b + 255) & ~size_t(255); }
+
+lora_status_t check_shapes(int64_t T, int64_t d_in, int64_t d_out, int64_t r, lora_dtype_t dt) {
+  if (dt != LORA_BF16 && dt != LORA_F32) return fail(LORA_EINVAL, "unknown dtype");
+  if (T < 1 || d_in < 1 || d_out < 1) return fail(LORA_EINVAL, "T, d_in and d_out must be >= 1");
+  if (r < 0 || r > kMaxRank) return fail(LORA_EINVAL, "rank r must be in [0, 128]");
+  if (d_in % 8 || d_out % 8) return fail(LORA_EUNSUPPORTED, "d_in and d_out must be multiples of 8");
+  if (T > kMaxElems / d_in || T > kMaxElems / d_out || d_in > kMaxElems / d_out)
+    return fail(LORA_EUNSUPPORTED, "a matrix has 2^31 or more elements");
+  return LORA_OK;
+}
+
+// Workspace layout of the backward pass (offsets in bytes, 256-byte aligned).
+struct BwdLayout {
+  size_t u, du, dbp, dap, total;
+  int nch_b, rpc_b, nch_a, rpc_a;
+};
+BwdLayout bwd_layout(int64_t T, int64_t K, int64_t N, int64_t r, lora_dtype_t dt) {
+  BwdLayout L{};
+  if (r == 0) return L;
+  const Dtype d = dt == LORA_BF16 ? DT_BF16 : DT_F32;
+  col_chunking((int)T, (int)N, (int)r, d, &L.nch_b, &L.rpc_b);
+  col_chunking((int)T, (int)K, (int)r, d, &L.nch_a, &L.rpc_a);
+  size_t off = 0;
+  L.u = off;
+  off += round256((size_t)T * r * 4);
+  L.du = off;
+  off += round256((size_t)T * r * 4);
+  L.dbp = off;
+  off += round256((size_t)L.nch_b * N * r * 4);
+  L.dap = off;
+  off += round256((size_t)L.nch_a * K * r * 4);
+  L.total = off;
+  return L;
+}
+
+lora_status_t check_ws(void *ws, size_t ws_bytes, size_t need) {
+  if (need == 0) return LORA_OK;
+  if (!ws) return fail(LORA_EWORKSPACE, "workspace required but ws is NULL");
+  if (ws_bytes < need) return fail(LORA_EWORKSPACE, "workspace too small");
+  if (!aligned16(ws)) return fail(LORA_EINVAL, "workspace not 16-byte aligned");
+  return LORA_OK;
+}
+
+lora_status_t hip_fail(hipError_t e, const char *what) {
+  std::snprintf(g_err, sizeof g_err, "%s: %s", what, hipGetErrorString(e));
+  return LORA_EHIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t lora_linear_workspace_bytes(lora_op_t op, int64_t T, int64_t d_in, int64_t d_out,
+                                   int64_t r, lora_dtype_t dt) {
+  if (check_shapes(T, d_in, d_out, op == LORA_OP_FROZEN_DX ? 0 : r, dt) != LORA_OK)
+    return (size_t)-1;
+  switch (op) {
+    case LORA_OP_FWD:
+      return r > 0 ? round256((size_t)T * r * 4) : 0;
+    case LORA_OP_BWD:
+      return bwd_layout(T, d_in, d_out, r, dt).total;
+    case LORA_OP_FROZEN_DX:
+      return 0;
+  }
+  return (size_t)-1;
+}
+
+lora_status_t lora_linear_fwd(const void *x, const void *W, const void *A, const void *B,
+                              void *y, float *u_save, int64_t T, int64_t d_in, int64_t d_out,
+                              int64_t r, float scale, lora_dtype_t dt, void *ws,
+                              size_t ws_bytes, void *hip_stream) {
+  lora_status_t s = check_shapes(T, d_in, d_out, r, dt);
+  if (s != LORA_OK) return s;
+  if (!x || !W || !y) return fail(LORA_EINVAL, "x, W and y are required");
+  if (r > 0 && (!A || !B)) return fail(LORA_EINVAL, "A and B are required when r > 0");
+  if (r > 0 && !std::isfinite(scale)) return fail(LORA_EINVAL, "scale must be finite");
+  const void *ptrs[] = {x, W, y, r > 0 ? A : nullptr, r > 0 ? B : nullptr,
+                        r > 0 ? (const void *)u_save : nullptr};
+  for (const void *p : ptrs)
+    if (p && !aligned16(p)) return fail(LORA_EINVAL, "pointers must be 16-byte aligned");
+  const size_t es = esize(dt);
+  const size_t need = lora_linear_workspace_bytes(LORA_OP_FWD, T, d_in, d_out, r, dt);
+  if ((s = check_ws(ws, ws_bytes, need)) != LORA_OK) return s;
+  std::vector<Range> ins = {rng(x, T * d_in * es), rng(W, d_out * d_in * es)};
+  std::vector<Range> outs = {rng(y, T * d_out * es)};
+  if (r > 0) {
+    ins.push_back(rng(A, r * d_in * es));
+    ins.push_back(rng(B, d_out * r * es));
+    if (u_save) outs.push_back(rng(u_save, T * r * 4));
+    if (need) outs.push_back(rng(ws, (int64_t)need));
+  }
+  if (any_overlap(outs, ins)) return fail(LORA_EINVAL, "an output overlaps an input or another output");
+
+  hipStream_t st = (hipStream_t)hip_stream;
+  const Dtype d = dt == LORA_BF16 ? DT_BF16 : DT_F32;
+  float *u = nullptr;
+  if (r > 0) {
+    u = u_save ? u_save : (float *)ws;
+    Timed t(K_LORA_DOWN, st);
+    hipError_t e = launch_row_skinny(x, d_in, (int)T, (int)d_in, A, d_in, false, (int)r, 1.0f, u, d, st);
+    t.done();
+    if (e != hipSuccess) return hip_fail(e, "lora_down launch");
+  }
+  GemmArgs g{};
+  g.A = x; g.lda = d_in;
+  g.B = W; g.ldb = d_in;
+  g.M = (int)T; g.N = (int)d_out; g.K = (int)d_in;
+  g.A2 = u; g.s2 = scale; g.B2 = B; g.ldb2 = r; g.r = (int)r;
+  g.C = y; g.ldc = d_out;
+  Timed t(K_GEMM_FWD, st);
+  hipError_t e = launch_gemm(g, d, false, st);
+  t.done();
+  if (e != hipSuccess) return hip_fail(e, "gemm_fwd launch");
+  return LORA_OK;
+}
+
+lora_status_t lora_linear_bwd(const void *x, const void *W, const void *A, const void *B,
+                              const float *u_saved, const void *dy, void *dx, float *dA,
+                              float *dB, int64_t T, int64_t d_in, int64_t d_out, int64_t r,
+                              float scale, lora_dtype_t dt, void *ws, size_t ws_bytes,
+                              void *hip_stream) {
+  lora_status_t s = check_shapes(T, d_in, d_out, r, dt);
+  if (s != LORA_OK) return s;
+  if (!dy || !W) return fail(LORA_EINVAL, "dy and W are required");
+  if (r > 0 && (!x || !A || !B || !dA || !dB))
+    return fail(LORA_EINVAL, "x, A, B, dA and dB are required when r > 0");
+  if (r == 0 && !dx) return fail(LORA_EINVAL, "nothing to compute: r = 0 and dx is NULL");
+  if (r > 0 && !std::isfinite(scale)) return fail(LORA_EINVAL, "scale must be finite");
+  const void *ptrs[] = {x, W, A, B, u_saved, dy, dx, dA, dB};
+  for (const void *p : ptrs)
+    if (p && !aligned16(p)) return fail(LORA_EINVAL, "pointers must be 16-byte aligned");
+  const size_t es = esize(dt);
+  const size_t need = lora_linear_workspace_bytes(LORA_OP_BWD, T, d_in, d_out, r, dt);
+  if ((s = check_ws(ws, ws_bytes, need)) != LORA_OK) return s;
+  std::vector<Range> ins = {rng(W, d_out * d_in * es), rng(dy, T * d_out * es)};
+  std::vector<Range> outs;
+  if (dx) outs.push_back(rng(dx, T * d_in * es));
+  if (r > 0) {
+    ins.push_back(rng(x, T * d_in * es));
+    ins.push_back(rng(A, r * d_in * es));
+    ins.push_back(rng(B, d_out * r * es));
+    if (u_saved) ins.push_back(rng(u_saved, T * r * 4));
+    outs.push_back(rng(dA, r * d_in * 4));
+    outs.push_back(rng(dB, d_out * r * 4));
+    if (need) outs.push_back(rng(ws, (int64_t)need));
+  }
+  if (any_overlap(outs, ins)) return fail(LORA_EINVAL, "an output overlaps an input or another output");
+
+  hipStream_t st = (hipStream_t)hip_stream;
+  const Dtype d = dt == LORA_BF16 ? DT_BF16 : DT_F32;
+  hipError_t e;
+  if (r == 0) {
+    GemmArgs g{};
+    g.A = dy; g.lda = d_out;
+    g.B = W; g.ldb = d_in;
+    g.M = (int)T; g.N = (int)d_in; g.K = (int)d_out;
+    g.C = dx; g.ldc = d_in;
+    Timed t(K_GEMM_BWD_DX, st);
+    e = launch_gemm(g, d, true, st);
+    t.done();
+    return e == hipSuccess ? LORA_OK : hip_fail(e, "gemm_bwd_dx launch");
+  }
+
+  const BwdLayout L = bwd_layout(T, d_in, d_out, r, dt);
+  char *wsb = (char *)ws;
+  const float *u = u_saved;
+  if (!u) {
+    float *ur = (float *)(wsb + L.u);
+    Timed t(K_LORA_DOWN, st);
+    e = launch_row_skinny(x, d_in, (int)T, (int)d_in, A, d_in, false, (int)r, 1.0f, ur, d, st);
+    t.done();
+    if (e != hipSuccess) return hip_fail(e, "lora_down launch");
+    u = ur;
+  }
+  float *du = (float *)(wsb + L.du);
+  float *dbp = (float *)(wsb + L.dbp);
+  float *dap = (float *)(wsb + L.dap);
+  {
+    Timed t(K_LORA_DY_B, st);
+    e = launch_row_skinny(dy, d_out, (int)T, (int)d_out, B, r, true, (int)r, scale, du, d, st);
+    t.done();
+    if (e != hipSuccess) return hip_fail(e, "lora_dy_b launch");
+  }
+  {
+    Timed t(K_DB_PARTS, st);
+    e = launch_col_skinny(dy, d_out, (int)T, (int)d_out, u, (int)r, L.nch_b, L.rpc_b, dbp, d, st);
+    t.done();
+    if (e != hipSuccess) return hip_fail(e, "db_parts launch");
+  }
+  if (dx) {
+    GemmArgs g{};
+    g.A = dy; g.lda = d_out;
+    g.B = W; g.ldb = d_in;
+    g.M = (int)T; g.N = (int)d_in; g.K = (int)d_out;
+    g.A2 = du; g.s2 = 1.0f; g.B2 = A; g.ldb2 = d_in; g.r = (int)r;
+    g.C = dx; g.ldc = d_in;
+    Timed t(K_GEMM_BWD_DX, st);
+    e = launch_gemm(g, d, true, st);
+    t.done();
+    if (e != hipSuccess) return hip_fail(e, "gemm_bwd_dx launch");
+  }
+  {
+    Timed t(K_DA_PARTS, st);
+    e = launch_col_skinny(x, d_in, (int)T, (int)d_in, du, (int)r, L.nch_a, L.rpc_a, dap, d, st);
+    t.done();
+    if (e != hipSuccess) return hip_fail(e, "da_parts launch");
+  }
+  {
+    Timed t(K_REDUCE_PARTS, st);
+    e = launch_reduce_parts(dbp, L.nch_b, (int)d_out, (int)r, scale, dB, false, st);
+    if (e == hipSuccess) e = launch_reduce_parts(dap, L.nch_a, (int)d_in, (int)r, 1.0f, dA, true, st);
+    t.done();
+    if (e != hipSuccess) return hip_fail(e, "reduce_parts launch");
+  }
+  return LORA_OK;
+}
+
+lora_status_t frozen_linear_bwd_dx(const void *dy, const void *W, void *dx, int64_t T,
+                                   int64_t d_in, int64_t d_out, lora_dtype_t dt, void *ws,
+                                   size_t ws_bytes, void *hip_stream) {
+  (void)ws;
+  (void)ws_bytes;
+  lora_status_t s = check_shapes(T, d_in, d_out, 0, dt);
+  if (s != LORA_OK) return s;
+  if (!dy || !W || !dx) return fail(LORA_EINVAL, "dy, W and dx are required");
+  if (!aligned16(dy) || !aligned16(W) || !aligned16(dx))
+    return fail(LORA_EINVAL, "pointers must be 16-byte aligned");
+  const size_t es = esize(dt);
+  std::vector<Range> ins = {rng(W, d_out * d_in * es), rng(dy, T * d_out * es)};
+  std::vector<Range> outs = {rng(dx, T * d_in * es)};
+  if (any_overlap(outs, ins)) return fail(LORA_EINVAL, "an output overlaps an input");
+  hipStream_t st = (hipStream_t)hip_stream;
+  GemmArgs g{};
+  g.A = dy; g.lda = d_out;
+  g.B = W; g.ldb = d_in;
+  g.M = (int)T; g.N = (int)d_in; g.K = (int)d_out;
+  g.C = dx; g.ldc = d_in;
+  Timed t(K_GEMM_FROZEN_DX, st);
+  hipError_t e = launch_gemm(g, dt == LORA_BF16 ? DT_BF16 : DT_F32, true, st);
+  t.done();
+  return e == hipSuccess ? LORA_OK : hip_fail(e, "gemm_frozen_dx launch");
+}
+
+const char *lora_status_str(lora_status_t status) {
+  switch (status) {
+    case LORA_OK: return "ok";
+    case LORA_EINVAL: return "invalid argument";
+    case LORA_EUNSUPPORTED: return "unsupported shape";
+    case LORA_EWORKSPACE: return "workspace missing or too small";
+    case LORA_EHIP: return "HIP launch error";
+  }
+  return "unknown status";
+}
+
+const char *lora_last_error(void) { return g_err; }
+
+lora_status_t lora_profiler_enable(int on) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_prof_on = on != 0;
+  return LORA_OK;
+}
+
+lora_status_t lora_profiler_reset(void) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  for (auto &v : g_prof) {
+    for (auto &p : v) {
+      (void)hipEventDestroy(p.a);
+      (void)hipEventDestroy(p.b);
+    }
+    v.clear();
+  }
+  return LORA_OK;
+}
+
+lora_status_t lora_profiler_read(int kernel_id, double *total_ms, int64_t *launches) {
+  if (kernel_id < 0 || kernel_id >= K_COUNT || !total_ms || !launches)
+    return fail(LORA_EINVAL, "bad kernel id or NULL output");
+  std::vector<EventPair> recs;
+  {
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    recs = g_prof[kernel_id];
+  }
+  double sum = 0.0;
+  for (auto &p : recs) {
+    hipError_t e = hipEventSynchronize(p.b);
+    if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+    float ms = 0.0f;
+    e = hipEventElapsedTime(&ms, p.a, p.b);
+    if (e != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
+    sum += ms;
+  }
+  *total_ms = sum;
+  *launches = (int64_t)recs.size();
+  return LORA_OK;
+}
+
+const char *lora_kernel_name(int kernel_id) {
+  return (kernel_id >= 0 && kernel_id < K_COUNT) ? kKernelNames[kernel_id] : nullptr;
+}
+
+int lora_kernel_count(void) { return K_COUNT; }
+
+}  // extern "C"

@@ -1,0 +1,175 @@
+"""Python binding of ``liblora_mi355x.so`` (the C ABI in include/lora_mi355x.h).
+
+Argument marshalling only: every step of the LoRA forward and backward runs in
+the library's HIP kernels on the caller's stream.  PyTorch provides device
+memory and the current HIP stream.  If the library has not been built the
+binding raises -- there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "liblora_mi355x.so")
+
+LORA_OK, LORA_EINVAL, LORA_EUNSUPPORTED, LORA_EWORKSPACE, LORA_EHIP = range(5)
+LORA_BF16, LORA_F32 = 0, 1
+LORA_OP_FWD, LORA_OP_BWD, LORA_OP_FROZEN_DX = 0, 1, 2
+
+_lib = None
+
+
+class LoraError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        super().__init__(f"{where}: status {status} ({detail})")
+        self.status = status
+
+
+def lib() -> ctypes.CDLL:
+    """Load the HIP library (once).  Raises if it is missing: build it with
+    ``python -m paper_2606_19528_amd.build``."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"HIP library not built: {LIB_PATH} is missing "
+                           "(run python -m paper_2606_19528_amd.build)")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i64, f32, sz, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t, ctypes.c_int
+    L.lora_linear_workspace_bytes.argtypes = [i32, i64, i64, i64, i64, i32]
+    L.lora_linear_workspace_bytes.restype = sz
+    L.lora_linear_fwd.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, i64, i64, f32, i32, vp, sz, vp]
+    L.lora_linear_fwd.restype = i32
+    L.lora_linear_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i64, i64, i64, i64, f32, i32,
+                                  vp, sz, vp]
+    L.lora_linear_bwd.restype = i32
+    L.frozen_linear_bwd_dx.argtypes = [vp, vp, vp, i64, i64, i64, i32, vp, sz, vp]
+    L.frozen_linear_bwd_dx.restype = i32
+    L.lora_status_str.argtypes = [i32]
+    L.lora_status_str.restype = ctypes.c_char_p
+    L.lora_last_error.argtypes = []
+    L.lora_last_error.restype = ctypes.c_char_p
+    L.lora_profiler_enable.argtypes = [i32]
+    L.lora_profiler_enable.restype = i32
+    L.lora_profiler_reset.argtypes = []
+    L.lora_profiler_reset.restype = i32
+    L.lora_profiler_read.argtypes = [i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64)]
+    L.lora_profiler_read.restype = i32
+    L.lora_kernel_name.argtypes = [i32]
+    L.lora_kernel_name.restype = ctypes.c_char_p
+    L.lora_kernel_count.argtypes = []
+    L.lora_kernel_count.restype = i32
+    _lib = L
+    return L
+
+
+def _check(status: int, where: str):
+    if status != LORA_OK:
+        detail = lib().lora_last_error().decode()
+        raise LoraError(status, where, detail)
+
+
+def _dtype_code(t) -> int:
+    import torch
+
+    if t.dtype == torch.bfloat16:
+        return LORA_BF16
+    if t.dtype == torch.float32:
+        return LORA_F32
+    raise TypeError(f"unsupported dtype {t.dtype} (bf16 or fp32)")
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("tensors must be contiguous (row-major, no padding)")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    import torch
+
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _ws(ws, nbytes: int, like):
+    import torch
+
+    if nbytes == 0:
+        return None, 0
+    if ws is None:
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=like.device)
+    return ws, ws.numel() * ws.element_size()
+
+
+def lora_linear_workspace_bytes(op: int, T: int, d_in: int, d_out: int, r: int, dt: int) -> int:
+    n = lib().lora_linear_workspace_bytes(op, T, d_in, d_out, r, dt)
+    if n == ctypes.c_size_t(-1).value:
+        raise LoraError(LORA_EINVAL, "lora_linear_workspace_bytes", lib().lora_last_error().decode())
+    return int(n)
+
+
+def lora_linear_fwd(x, W, A, B, y, u_save=None, scale: float = 1.0, ws=None, stream=None):
+    """y = x W^T + scale (x A^T) B^T; u_save (fp32 [T, r]) receives x A^T."""
+    T, d_in = x.shape
+    d_out = W.shape[0]
+    r = 0 if A is None else A.shape[0]
+    dt = _dtype_code(x)
+    ws, ws_bytes = _ws(ws, lora_linear_workspace_bytes(LORA_OP_FWD, T, d_in, d_out, r, dt), x)
+    st = lib().lora_linear_fwd(_ptr(x), _ptr(W), _ptr(A), _ptr(B), _ptr(y), _ptr(u_save), T, d_in,
+                               d_out, r, float(scale), dt, _ptr(ws), ws_bytes, _stream(stream))
+    _check(st, "lora_linear_fwd")
+    return y
+
+
+def lora_linear_bwd(x, W, A, B, u_saved, dy, dx, dA, dB, scale: float = 1.0, ws=None, stream=None):
+    """dx = dy W + du A, dA = du^T x, dB = scale dy^T u with du = scale dy B."""
+    T, d_out = dy.shape
+    d_in = W.shape[1]
+    r = 0 if A is None else A.shape[0]
+    dt = _dtype_code(dy)
+    ws, ws_bytes = _ws(ws, lora_linear_workspace_bytes(LORA_OP_BWD, T, d_in, d_out, r, dt), dy)
+    st = lib().lora_linear_bwd(_ptr(x), _ptr(W), _ptr(A), _ptr(B), _ptr(u_saved), _ptr(dy),
+                               _ptr(dx), _ptr(dA), _ptr(dB), T, d_in, d_out, r, float(scale), dt,
+                               _ptr(ws), ws_bytes, _stream(stream))
+    _check(st, "lora_linear_bwd")
+    return dx, dA, dB
+
+
+def frozen_linear_bwd_dx(dy, W, dx, ws=None, stream=None):
+    """Rank-0 frozen linear input gradient dx = dy W."""
+    T, d_out = dy.shape
+    d_in = W.shape[1]
+    dt = _dtype_code(dy)
+    st = lib().frozen_linear_bwd_dx(_ptr(dy), _ptr(W), _ptr(dx), T, d_in, d_out, dt, _ptr(ws),
+                                    0 if ws is None else ws.numel() * ws.element_size(),
+                                    _stream(stream))
+    _check(st, "frozen_linear_bwd_dx")
+    return dx
+
+
+# --- kernel timing hook (benchmarks) -----------------------------------------------
+def kernel_names() -> list:
+    L = lib()
+    return [L.lora_kernel_name(i).decode() for i in range(L.lora_kernel_count())]
+
+
+def profiler_enable(on: bool = True):
+    _check(lib().lora_profiler_enable(1 if on else 0), "lora_profiler_enable")
+
+
+def profiler_reset():
+    _check(lib().lora_profiler_reset(), "lora_profiler_reset")
+
+
+def profiler_read(name: str):
+    """(total milliseconds, launches) recorded for the kernel `name`."""
+    idx = kernel_names().index(name)
+    ms = ctypes.c_double(0.0)
+    n = ctypes.c_int64(0)
+    _check(lib().lora_profiler_read(idx, ctypes.byref(ms), ctypes.byref(n)), "lora_profiler_read")
+    return ms.value, n.value

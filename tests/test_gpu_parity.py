@@ -1,0 +1,190 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle.
+
+bf16 in / fp32 accumulate: max relative error <= 2e-2 per output tensor;
+fp32 check mode: <= 1e-5.  Small shapes are compared in full; the full-size
+workloads compare every element of u, dA and dB and a deterministic sample of
+rows of y and dx (including the first and the last, ragged-tail, row).
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from gpu_helpers import TOL, compare, gpu_lora, oracle_lora, relerr
+from workloads import WORKLOADS, frozen_inputs, linear_seed, lora_inputs, sample_rows
+
+pytestmark = pytest.mark.gpu
+
+import paper_2606_19528_amd as lm  # noqa: E402
+
+
+def _announce(msg):
+    print(f"[case] {msg}", file=sys.stderr, flush=True)
+
+
+def _case(orc, T, K, N, r, alpha, seed=0, dtype=torch.bfloat16, rows=None, recompute=False):
+    _announce(f"lora T={T} K={K} N={N} r={r} dtype={dtype} recompute={recompute}")
+    s = alpha / r if r else 0.0
+    inp = lora_inputs(T, K, N, r, seed=seed, dtype=dtype)
+    gpu = gpu_lora(inp, s, recompute_u=recompute)
+    ref = oracle_lora(orc, inp, s, rows=rows)
+    return compare(gpu, ref, dtype, rows=rows, label=f"T={T} K={K} N={N} r={r}")
+
+
+# --- small full-tensor cases --------------------------------------------------------
+def test_single_256_full(orc):
+    w = WORKLOADS["single_256"]
+    lin = w.linears[0]
+    _case(orc, w.tokens, lin.d_in, lin.d_out, lin.rank, lin.alpha)
+
+
+@pytest.mark.parametrize("T", [1, 3, 17, 129])
+@pytest.mark.parametrize("d", [8, 24, 136])
+@pytest.mark.parametrize("r", [0, 1, 8, 16, 32])
+def test_edge_shapes(orc, T, d, r):
+    _case(orc, T, d, d + 8 * (r % 3), r, 2.0 * r if r else 0.0, seed=T * 1000 + d + r)
+
+
+@pytest.mark.parametrize("shape", [(300, 520, 392, 16), (257, 392, 264, 8), (130, 1032, 136, 128),
+                                   (64, 128, 2056, 5), (515, 264, 1288, 32)])
+def test_multi_tile_ragged(orc, shape):
+    T, K, N, r = shape
+    _case(orc, T, K, N, r, 2.0 * r, seed=7)
+
+
+def test_recompute_u_matches(orc):
+    T, K, N, r = 200, 264, 136, 16
+    inp = lora_inputs(T, K, N, r, seed=5)
+    a = gpu_lora(inp, 2.0)
+    b = gpu_lora(inp, 2.0, recompute_u=True)
+    for k in ("y", "dx", "dA", "dB"):
+        assert torch.equal(a[k], b[k]), k
+
+
+def test_deterministic(orc):
+    inp = lora_inputs(333, 520, 264, 16, seed=9)
+    a = gpu_lora(inp, 2.0)
+    b = gpu_lora(inp, 2.0)
+    for k in ("y", "dx", "u", "dA", "dB"):
+        assert torch.equal(a[k], b[k]), k
+
+
+# --- isolating the LoRA branch (it is only ~10% of y and dx) -----------------------
+def test_zero_W_isolates_lora_branch(orc):
+    T, K, N, r = 256, 384, 264, 16
+    inp = lora_inputs(T, K, N, r, seed=11)
+    inp["W"].zero_()
+    ref = oracle_lora(orc, inp, 2.0)
+    gpu = gpu_lora(inp, 2.0)
+    compare(gpu, ref, torch.bfloat16, label="W=0")
+
+
+def test_zero_B_gives_plain_linear(orc):
+    T, K, N, r = 256, 384, 264, 16
+    inp = lora_inputs(T, K, N, r, seed=12)
+    inp["B"].zero_()
+    gpu = gpu_lora(inp, 2.0)
+    assert torch.all(gpu["dA"] == 0)
+    # y must equal the rank-0 forward bitwise (the LoRA tail adds exact zeros).
+    x, W = inp["x"].cuda(), inp["W"].cuda()
+    y0 = torch.empty(T, N, dtype=torch.bfloat16, device="cuda")
+    lm.lora_linear_fwd(x, W, None, None, y0, None, 0.0)
+    torch.cuda.synchronize()
+    assert torch.equal(gpu["y"], y0.cpu())
+    ref = oracle_lora(orc, inp, 2.0)
+    compare(gpu, ref, torch.bfloat16, label="B=0")
+
+
+# --- fp32 check mode -------------------------------------------------------------
+@pytest.mark.parametrize("shape", [(128, 256, 256, 8), (3, 8, 24, 1), (129, 136, 144, 32),
+                                   (300, 520, 392, 16), (65, 264, 128, 0)])
+def test_fp32_check_mode(orc, shape):
+    T, K, N, r = shape
+    _case(orc, T, K, N, r, 2.0 * r if r else 0.0, seed=21, dtype=torch.float32)
+
+
+# --- frozen rank-0 dx ----------------------------------------------------------------
+@pytest.mark.parametrize("shape", [(1, 8, 8), (129, 136, 392), (256, 512, 1032)])
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_frozen_dx_small(orc, shape, dtype):
+    T, K, N = shape
+    _announce(f"frozen T={T} K={K} N={N} {dtype}")
+    inp = frozen_inputs(T, K, N, seed=3, dtype=dtype)
+    dy, W = inp["dy"].cuda(), inp["W"].cuda()
+    dx = torch.empty(T, K, dtype=dtype, device="cuda")
+    lm.frozen_linear_bwd_dx(dy, W, dx)
+    torch.cuda.synchronize()
+    ref = orc.frozen_dx(inp["dy"], inp["W"])
+    assert relerr(dx.cpu().to(torch.float64).numpy(), ref) <= TOL[dtype]
+
+
+# --- full-size workloads (sampled rows of y and dx) --------------------------------
+def _full_size(orc, key, linears=None, layer=0, fp32=False):
+    w = WORKLOADS[key]
+    T = w.tokens
+    rows = sample_rows(T, 64)
+    for idx, lin in enumerate(w.linears):
+        if linears is not None and lin.name not in linears:
+            continue
+        dtype = torch.float32 if fp32 else torch.bfloat16
+        _case(orc, T, lin.d_in, lin.d_out, lin.rank, lin.alpha, seed=linear_seed(0, layer, idx),
+              dtype=dtype, rows=rows)
+
+
+def test_full_llama_q_proj(orc):
+    _full_size(orc, "llama_q_proj")
+
+
+def test_full_llama_q_proj_fp32(orc):
+    _full_size(orc, "llama_q_proj", fp32=True)
+
+
+def test_full_llama_mlp(orc):
+    _full_size(orc, "llama_mlp")
+
+
+def test_full_qwen_layer(orc):
+    _full_size(orc, "qwen_layer")
+
+
+def test_full_llama_stack_layer(orc):
+    # one decoder layer of the 28-layer stack (every layer has the same shapes)
+    _full_size(orc, "llama_stack", layer=27)
+
+
+def test_full_llama_lm_head_dx(orc):
+    w = WORKLOADS["llama_stack"]
+    head = w.head
+    T = w.tokens
+    _announce(f"lm head frozen dx T={T} K={head.d_in} N={head.d_out}")
+    inp = frozen_inputs(T, head.d_in, head.d_out, seed=10_000)
+    dy, W = inp["dy"].cuda(), inp["W"].cuda()
+    dx = torch.empty(T, head.d_in, dtype=torch.bfloat16, device="cuda")
+    lm.frozen_linear_bwd_dx(dy, W, dx)
+    torch.cuda.synchronize()
+    rows = sample_rows(T, 16)
+    ref = orc.frozen_dx(inp["dy"][rows], inp["W"])
+    assert relerr(dx.cpu()[rows].to(torch.float64).numpy(), ref) <= TOL[torch.bfloat16]
+
+
+def test_no_dw_sized_allocation():
+    """The backward never allocates anything of dW's size (d_out * d_in * 2 bytes)."""
+    T, K, N, r = 1024, 3072, 3072, 16
+    inp = {k: v.cuda() for k, v in lora_inputs(T, K, N, r, seed=0).items()}
+    ws_bytes = lm.lora_linear_workspace_bytes(lm.LORA_OP_BWD, T, K, N, r, lm.LORA_BF16)
+    assert ws_bytes < N * K * 2
+    u = torch.empty(T, r, device="cuda")
+    y = torch.empty(T, N, dtype=torch.bfloat16, device="cuda")
+    lm.lora_linear_fwd(inp["x"], inp["W"], inp["A"], inp["B"], y, u, 2.0)
+    dx = torch.empty(T, K, dtype=torch.bfloat16, device="cuda")
+    dA = torch.empty(r, K, device="cuda")
+    dB = torch.empty(N, r, device="cuda")
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+    torch.cuda.reset_peak_memory_stats()
+    base = torch.cuda.memory_allocated()
+    lm.lora_linear_bwd(inp["x"], inp["W"], inp["A"], inp["B"], u, inp["dy"], dx, dA, dB, 2.0, ws=ws)
+    torch.cuda.synchronize()
+    assert torch.cuda.max_memory_allocated() - base == 0
