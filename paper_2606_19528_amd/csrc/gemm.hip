@@ -1,170 +1,273 @@
 // gemm.hip -- LDS-tiled matrix-core GEMM for the two big contractions of the
 // LoRA linear, each with the rank-r LoRA term folded in as extra reduction
-// steps:
+// steps (so y and dx are rounded exactly once):
 //   forward   y  = [x | s*u] [W | B]^T          (NT: both operands k-contiguous)
 //   backward  dx = [dy | du] [W ; A]            (NN: W and A are k-major, i.e.
 //                                                 the reduction index is the row)
 //   frozen    dx = dy W                          (NN, no tail)
-// One workgroup computes a BM x BN output tile.  The reduction runs over
-// 128-byte k-stages staged through double-buffered LDS (one barrier per
-// stage); the next stage's global loads are issued before the current
-// stage's MFMAs.  k-major operands are transposed in registers (VEC x VEC
-// blocks) on their way into LDS, so the LDS layout -- rows of 128 bytes of k
-// plus 16 bytes of padding -- is the same for every operand.
+//
+// Structure of one workgroup (4 or 8 waves, one BM x BN output tile):
+//  * k advances in stages of BKB bytes per row.  Global loads go through
+//    buffer resources (hardware bounds checks instead of per-load branches)
+//    into one of two register sets, then into an LDS ring of NBUF buffers.
+//  * NBUF = 3: a stage is written to LDS two steps before it is consumed, so
+//    the first k-slice's MFMA fragments of the next stage can be read before
+//    the end-of-step barrier and the MFMAs of a step start without waiting on
+//    LDS.  NBUF = 2: classic double buffering.  One barrier per step.
+//  * The waves form a WM x WN x WK grid: WM x WN split the tile, WK splits
+//    each stage's 16-deep k-slices; with WK > 1 the partial accumulators are
+//    summed through LDS in a fixed order at the end.
+//  * k-major operands (W and A in the backward pass) keep their memory layout
+//    in LDS ([k][n]) and are read with ds_read_b64_tr_b16, which hands each
+//    lane four consecutive k of one column (bf16).  In the fp32 check mode
+//    they are transposed in registers on the way into LDS instead.
+//  * Workgroups are mapped to tiles XCD by XCD (the dispatcher deals workgroup
+//    ids round-robin over the 8 XCDs, each with its own L2), and each XCD's
+//    share of tiles is a compact block of GM tile rows.
 #include "kernels.hpp"
 #include "launch.hpp"
 
 namespace lora {
 
-template <class E, int BM, int BN, int WM, int WN, bool KMAJ>
-__global__ __launch_bounds__(WM * WN * 64) void gemm_kernel(GemmArgs g) {
-  typedef typename E::T T;
-  constexpr int NT = WM * WN * 64;
-  constexpr int VEC = E::VEC;
-  constexpr int BKB = 128;                  // k bytes per stage and row
-  constexpr int BKE = BKB / (int)sizeof(T); // k elements per stage
-  constexpr int ROWB = BKB + 16;            // padded LDS row
-  constexpr int WTM = BM / WM, WTN = BN / WN;
-  constexpr int FM = WTM / 32, FN = WTN / 32;
-  constexpr int CPR = BKB / 16;             // 16-byte chunks per row and stage
-  constexpr int A_CH = BM * CPR, A_PER = (A_CH + NT - 1) / NT;
-  constexpr int B_CH = BN * CPR, B_PER = (B_CH + NT - 1) / NT;
-  constexpr int NBV = BN / VEC;             // k-major: VEC x VEC blocks per k-row band
-  constexpr int KB_BLK = (BKE / VEC) * NBV, KB_PER = (KB_BLK + NT - 1) / NT;
-  constexpr int RB = KMAJ ? KB_PER * VEC : B_PER;
-  static_assert(BM % (WM * 32) == 0 && BN % (WN * 32) == 0, "tile shape");
+enum { B_ROW = 0, B_KMAJ_REG = 1, B_KMAJ_TR = 2 };
 
-  __shared__ __align__(16) char smem[2 * (BM + BN) * ROWB];
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+
+template <int V>
+struct IC {
+  static constexpr int value = V;
+};
+
+template <class E, int BM, int BN, int WM, int WN, int WK, int BMODE, int BKB, int NBUF>
+__global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int group_m) {
+  typedef typename E::T T;
+  constexpr int NT = 64 * WM * WN * WK;
+  constexpr int VEC = E::VEC;
+  constexpr int ES = (int)sizeof(T);
+  constexpr int BKE = BKB / ES;              // k elements per stage
+  constexpr int SLICES = BKB / 32;           // k-slices of 32 bytes per stage
+  constexpr int SPW = SLICES / WK;           // slices per wave
+  constexpr int ROWA = BKB + 16;             // padded LDS row of a k-contiguous operand
+  constexpr int ROWT = BN * 2 + 32;          // padded LDS row of a k-major bf16 operand
+  constexpr int WTM = BM / WM, WTN = BN / WN;
+  constexpr int FM = WTM / 32, FN = WTN / 32, NB = FM * FN;
+  constexpr int CPR = BKB / 16;              // 16-byte chunks per k-contiguous row
+  constexpr int A_CH = BM * CPR, A_PER = (A_CH + NT - 1) / NT;
+  constexpr int NBV = BN / VEC;
+  constexpr int B_CH = BMODE == B_KMAJ_TR ? BKE * NBV : BN * CPR;
+  constexpr int B_PER = (B_CH + NT - 1) / NT;
+  constexpr int KB_BLK = (BKE / VEC) * NBV, KB_PER = (KB_BLK + NT - 1) / NT;
+  constexpr int RB = BMODE == B_KMAJ_REG ? KB_PER * VEC : B_PER;
+  constexpr int A_BYTES = BM * ROWA;
+  constexpr int B_BYTES = BMODE == B_KMAJ_TR ? BKE * ROWT : BN * ROWA;
+  constexpr int STAGE = A_BYTES + B_BYTES;
+  constexpr int RED_BYTES = WK > 1 ? BM * BN * 4 : 0;
+  constexpr int LDS = NBUF * STAGE > RED_BYTES ? NBUF * STAGE : RED_BYTES;
+  constexpr uint32_t OOB = 0x80000000u;      // offset past every buffer: loads return 0
+  static_assert(WM * WN * WK == 4 || WM * WN * WK == 8, "four or eight waves");
+  static_assert(SLICES % WK == 0 && NB % WK == 0, "k split");
+  static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile");
+  static_assert(BMODE != B_KMAJ_TR || ES == 2, "transposed LDS reads are bf16");
+  static_assert(NBUF == 2 || NBUF == 3, "LDS ring depth");
+
+  __shared__ __align__(16) char smem[LDS];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
-  const int wm = wave / WN, wn = wave % WN;
+  const int wk = wave % WK;
+  const int wn = (wave / WK) % WN;
+  const int wm = wave / (WK * WN);
 
+  // ---- tile of this workgroup: XCD-contiguous, grouped by GM tile rows ----
   const int tiles_m = (g.M + BM - 1) / BM;
-  const int mt = blockIdx.x % tiles_m;
-  const int nt = blockIdx.x / tiles_m;
+  const int tiles_n = (g.N + BN - 1) / BN;
+  const int ntiles = tiles_m * tiles_n;
+  int t;
+  {
+    const int id = blockIdx.x;
+    const int xcd = id & 7, local = id >> 3;
+    const int base = ntiles >> 3, rem = ntiles & 7;
+    t = xcd * base + (xcd < rem ? xcd : rem) + local;
+  }
+  const int gsize = group_m * tiles_n;
+  const int first_m = (t / gsize) * group_m;
+  const int gm = min(tiles_m - first_m, group_m);
+  const int mt = first_m + (t % gsize) % gm;
+  const int nt = (t % gsize) / gm;
   const int m0 = mt * BM, n0 = nt * BN;
 
-  const char *Ab = (const char *)g.A;
-  const char *Bb = (const char *)g.B;
-  const int nk_main = (g.K + BKE - 1) / BKE;
+  const T *B2 = (const T *)g.B2;
+  const int nk = (g.K + BKE - 1) / BKE;
   const int nk_tail = g.r > 0 ? (g.r + BKE - 1) / BKE : 0;
-  const int nk = nk_main + nk_tail;
 
-  u32x4 ra[A_PER];
-  u32x4 rb[RB];
+  // Buffer resources.  The tile's rows past M (and, for row-major B, past N)
+  // lie beyond num_records; k past K is masked per stage by selecting OOB.
+  const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)((const char *)g.A + (int64_t)m0 * g.lda * ES), (short)0,
+      (int)(min(g.M - m0, BM) * g.lda * ES), 0x00020000);
+  __amdgpu_buffer_rsrc_t rsB;
+  if constexpr (BMODE == B_ROW)
+    rsB = __builtin_amdgcn_make_buffer_rsrc((void *)((const char *)g.B + (int64_t)n0 * g.ldb * ES),
+                                            (short)0, (int)(min(g.N - n0, BN) * g.ldb * ES),
+                                            0x00020000);
+  uint32_t va[A_PER], vb[BMODE == B_KMAJ_REG ? KB_PER : B_PER];
+  int kca[A_PER], kcb[B_PER];
+#pragma unroll
+  for (int i = 0; i < A_PER; ++i) {
+    const int c = tid + i * NT;
+    kca[i] = (c % CPR) * VEC;
+    va[i] = c < A_CH ? (uint32_t)((c / CPR) * g.lda * ES + (c % CPR) * 16) : OOB;
+  }
+  if constexpr (BMODE == B_ROW) {
+#pragma unroll
+    for (int i = 0; i < B_PER; ++i) {
+      const int c = tid + i * NT;
+      kcb[i] = (c % CPR) * VEC;
+      vb[i] = c < B_CH ? (uint32_t)((c / CPR) * g.ldb * ES + (c % CPR) * 16) : OOB;
+    }
+  } else if constexpr (BMODE == B_KMAJ_TR) {
+#pragma unroll
+    for (int i = 0; i < B_PER; ++i) {
+      const int c = tid + i * NT;
+      const int kr = c / NBV, nc = c % NBV;
+      vb[i] = (c < B_CH && n0 + nc * VEC < g.N) ? (uint32_t)(kr * g.ldb * ES + nc * 16) : OOB;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < KB_PER; ++i) {
+      const int b = tid + i * NT;
+      const int kb = b % (BKE / VEC), nb = b / (BKE / VEC);
+      vb[i] = (b < KB_BLK && n0 + nb * VEC < g.N) ? (uint32_t)(kb * VEC * g.ldb * ES + nb * 16)
+                                                   : OOB;
+    }
+  }
 
-  auto load_stage = [&](int kt) {
-    if (kt < nk_main) {
-      const int k0 = kt * BKE;
+  u32x4 ra[2][A_PER];
+  u32x4 rb[2][RB];
+
+  // ---- global -> register set S for main stage kt (zeros past the end) ------
+  auto load_stage = [&](auto SET, int kt) {
+    constexpr int S = decltype(SET)::value;
+    const int k0 = kt * BKE;
+    const int krem = g.K - k0;  // valid k remaining in this stage (uniform)
+    const int soff = k0 * ES;
 #pragma unroll
-      for (int i = 0; i < A_PER; ++i) {
-        const int c = tid + i * NT;
-        const int row = c / CPR, kc = c % CPR;
-        const int m = m0 + row, k = k0 + kc * VEC;
-        ra[i] = (c < A_CH && m < g.M && k < g.K)
-                    ? ld16(Ab + ((int64_t)m * g.lda + k) * (int64_t)sizeof(T))
-                    : zero16();
-      }
-      if constexpr (!KMAJ) {
+    for (int i = 0; i < A_PER; ++i)
+      ra[S][i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                               rsA, kca[i] < krem ? va[i] : OOB, soff, 0));
+    if constexpr (BMODE == B_ROW) {
 #pragma unroll
-        for (int i = 0; i < B_PER; ++i) {
-          const int c = tid + i * NT;
-          const int row = c / CPR, kc = c % CPR;
-          const int n = n0 + row, k = k0 + kc * VEC;
-          rb[i] = (c < B_CH && n < g.N && k < g.K)
-                      ? ld16(Bb + ((int64_t)n * g.ldb + k) * (int64_t)sizeof(T))
-                      : zero16();
-        }
-      } else {
-#pragma unroll
-        for (int i = 0; i < KB_PER; ++i) {
-          const int b = tid + i * NT;
-          const int kb = b / NBV, nb = b % NBV;
-          const int n = n0 + nb * VEC;
-#pragma unroll
-          for (int e = 0; e < VEC; ++e) {
-            const int k = k0 + kb * VEC + e;
-            rb[i * VEC + e] = (b < KB_BLK && n < g.N && k < g.K)
-                                  ? ld16(Bb + ((int64_t)k * g.ldb + n) * (int64_t)sizeof(T))
-                                  : zero16();
-          }
-        }
-      }
+      for (int i = 0; i < B_PER; ++i)
+        rb[S][i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                 rsB, kcb[i] < krem ? vb[i] : OOB, soff, 0));
     } else {
-      // LoRA tail stage: reduction index j in [j0, j0 + BKE), valid below r.
-      const int j0 = (kt - nk_main) * BKE;
+      // k-major: rebase on this stage's first k row; rows past K are out of range.
+      const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+          (void *)((const char *)g.B + ((int64_t)k0 * g.ldb + n0) * ES), (short)0,
+          (int)(krem > 0 ? min(krem, BKE) * g.ldb * ES : 0), 0x00020000);
+      if constexpr (BMODE == B_KMAJ_TR) {
 #pragma unroll
-      for (int i = 0; i < A_PER; ++i) {
-        const int c = tid + i * NT;
-        const int row = c / CPR, kc = c % CPR;
-        const int m = m0 + row;
-        float f[VEC];
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) {
-          const int j = j0 + kc * VEC + e;
-          f[e] = (c < A_CH && m < g.M && j < g.r) ? g.s2 * g.A2[(int64_t)m * g.r + j] : 0.0f;
-        }
-        ra[i] = pack_vec(E(), f);
-      }
-      const T *B2 = (const T *)g.B2;
-      if constexpr (!KMAJ) {
-#pragma unroll
-        for (int i = 0; i < B_PER; ++i) {
-          const int c = tid + i * NT;
-          const int row = c / CPR, kc = c % CPR;
-          const int n = n0 + row;
-          float f[VEC];
-#pragma unroll
-          for (int e = 0; e < VEC; ++e) {
-            const int j = j0 + kc * VEC + e;
-            f[e] = (c < B_CH && n < g.N && j < g.r) ? E::to_float(B2[(int64_t)n * g.r + j]) : 0.0f;
-          }
-          rb[i] = pack_vec(E(), f);
-        }
+        for (int i = 0; i < B_PER; ++i)
+          rb[S][i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, vb[i], 0, 0));
       } else {
 #pragma unroll
-        for (int i = 0; i < KB_PER; ++i) {
-          const int b = tid + i * NT;
-          const int kb = b / NBV, nb = b % NBV;
-          const int n = n0 + nb * VEC;
+        for (int i = 0; i < KB_PER; ++i)
 #pragma unroll
-          for (int e = 0; e < VEC; ++e) {
-            const int j = j0 + kb * VEC + e;
-            rb[i * VEC + e] = (b < KB_BLK && n < g.N && j < g.r)
-                                  ? ld16(B2 + (int64_t)j * g.ldb2 + n)
-                                  : zero16();
-          }
-        }
+          for (int e = 0; e < VEC; ++e)
+            rb[S][i * VEC + e] = __builtin_bit_cast(
+                u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                           rs, vb[i] == OOB ? OOB : vb[i] + (uint32_t)(e * g.ldb * ES), 0, 0));
       }
     }
   };
 
-  auto store_stage = [&](int buf) {
-    char *sA = smem + buf * (BM + BN) * ROWB;
-    char *sB = sA + BM * ROWB;
+  // ---- LoRA tail stage into set 0: reduction index j in [j0, j0 + BKE) ------
+  auto load_tail = [&](int j0) {
 #pragma unroll
     for (int i = 0; i < A_PER; ++i) {
       const int c = tid + i * NT;
-      if (c < A_CH) st16(sA + (c / CPR) * ROWB + (c % CPR) * 16, ra[i]);
+      const int row = c / CPR, kc = c % CPR;
+      const int m = m0 + row;
+      float f[VEC];
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        const int j = j0 + kc * VEC + e;
+        f[e] = (c < A_CH && m < g.M && j < g.r) ? g.s2 * g.A2[(int64_t)m * g.r + j] : 0.0f;
+      }
+      ra[0][i] = pack_vec(E(), f);
     }
-    if constexpr (!KMAJ) {
+    if constexpr (BMODE == B_ROW) {
 #pragma unroll
       for (int i = 0; i < B_PER; ++i) {
         const int c = tid + i * NT;
-        if (c < B_CH) st16(sB + (c / CPR) * ROWB + (c % CPR) * 16, rb[i]);
+        const int row = c / CPR, kc = c % CPR;
+        const int n = n0 + row;
+        float f[VEC];
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+          const int j = j0 + kc * VEC + e;
+          f[e] = (c < B_CH && n < g.N && j < g.r) ? E::to_float(B2[(int64_t)n * g.r + j]) : 0.0f;
+        }
+        rb[0][i] = pack_vec(E(), f);
+      }
+    } else if constexpr (BMODE == B_KMAJ_TR) {
+#pragma unroll
+      for (int i = 0; i < B_PER; ++i) {
+        const int c = tid + i * NT;
+        const int kr = c / NBV, nc = c % NBV;
+        const int j = j0 + kr, n = n0 + nc * VEC;
+        rb[0][i] = (c < B_CH && j < g.r && n < g.N) ? ld16(B2 + (int64_t)j * g.ldb2 + n) : zero16();
       }
     } else {
 #pragma unroll
       for (int i = 0; i < KB_PER; ++i) {
         const int b = tid + i * NT;
-        if (b < KB_BLK) {
-          const int kb = b / NBV, nb = b % NBV;
-          u32x4 t[VEC];
-          transpose_block(E(), &rb[i * VEC], t);
+        const int kb = b % (BKE / VEC), nb = b / (BKE / VEC);
+        const int n = n0 + nb * VEC;
 #pragma unroll
-          for (int c = 0; c < VEC; ++c) st16(sB + (nb * VEC + c) * ROWB + kb * 16, t[c]);
+        for (int e = 0; e < VEC; ++e) {
+          const int j = j0 + kb * VEC + e;
+          rb[0][i * VEC + e] = (b < KB_BLK && n < g.N && j < g.r) ? ld16(B2 + (int64_t)j * g.ldb2 + n)
+                                                                   : zero16();
+        }
+      }
+    }
+  };
+
+  // ---- register set S -> LDS buffer `buf` -----------------------------------
+  auto store_stage = [&](auto SET, int buf) {
+    constexpr int S = decltype(SET)::value;
+    char *sA = smem + buf * STAGE;
+    char *sB = sA + A_BYTES;
+#pragma unroll
+    for (int i = 0; i < A_PER; ++i) {
+      const int c = tid + i * NT;
+      if (A_CH % NT == 0 || c < A_CH) st16(sA + (c / CPR) * ROWA + (c % CPR) * 16, ra[S][i]);
+    }
+    if constexpr (BMODE == B_ROW) {
+#pragma unroll
+      for (int i = 0; i < B_PER; ++i) {
+        const int c = tid + i * NT;
+        if (B_CH % NT == 0 || c < B_CH) st16(sB + (c / CPR) * ROWA + (c % CPR) * 16, rb[S][i]);
+      }
+    } else if constexpr (BMODE == B_KMAJ_TR) {
+#pragma unroll
+      for (int i = 0; i < B_PER; ++i) {
+        const int c = tid + i * NT;
+        if (B_CH % NT == 0 || c < B_CH) st16(sB + (c / NBV) * ROWT + (c % NBV) * 16, rb[S][i]);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < KB_PER; ++i) {
+        const int b = tid + i * NT;
+        if (KB_BLK % NT == 0 || b < KB_BLK) {
+          const int kb = b % (BKE / VEC), nb = b / (BKE / VEC);
+          u32x4 tr[VEC];
+          transpose_block(E(), &rb[S][i * VEC], tr);
+#pragma unroll
+          for (int c = 0; c < VEC; ++c) st16(sB + (nb * VEC + c) * ROWA + kb * 16, tr[c]);
         }
       }
     }
@@ -178,77 +281,206 @@ __global__ __launch_bounds__(WM * WN * 64) void gemm_kernel(GemmArgs g) {
 #pragma unroll
       for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.0f;
 
-  load_stage(0);
-  store_stage(0);
-  __syncthreads();
-
+  // ---- MFMA fragments of one k-slice ------------------------------------------
+  struct Frag {
+    u32x4 a[FM], b[FN];
+  };
   const int lrow = lane & 31;
   const int lko = (lane >> 5) * 16;
-  for (int kt = 0; kt < nk; ++kt) {
-    if (kt + 1 < nk) load_stage(kt + 1);
-    const char *sA = smem + (kt & 1) * (BM + BN) * ROWB;
-    const char *sB = sA + BM * ROWB;
+  // transposed-read addressing: 16-lane group gq, lane iq within it
+  const int gq = lane >> 4, iq = lane & 15;
+  const int tr_k = 8 * (gq >> 1) + (iq >> 2);
+  const int tr_n = 16 * (gq & 1) + 4 * (iq & 3);
+
+  auto read_frags = [&](int buf, int s, Frag &f) {
+    const char *sA = smem + buf * STAGE;
+    const char *sB = sA + A_BYTES;
+    const int sl = wk * SPW + s;
 #pragma unroll
-    for (int s = 0; s < BKB / 32; ++s) {
-      u32x4 af[FM], bf[FN];
+    for (int i = 0; i < FM; ++i) f.a[i] = ld16(sA + (wm * WTM + i * 32 + lrow) * ROWA + sl * 32 + lko);
 #pragma unroll
-      for (int i = 0; i < FM; ++i) af[i] = ld16(sA + (wm * WTM + i * 32 + lrow) * ROWB + s * 32 + lko);
-#pragma unroll
-      for (int j = 0; j < FN; ++j) bf[j] = ld16(sB + (wn * WTN + j * 32 + lrow) * ROWB + s * 32 + lko);
-      // D = Bop * Aop^T: D rows are output columns n, D columns are rows m, so
-      // each lane ends up holding runs of 4 consecutive n of one output row.
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j) mma32(E(), acc[i][j], bf[j], af[i]);
+    for (int j = 0; j < FN; ++j) {
+      if constexpr (BMODE == B_KMAJ_TR) {
+        const char *p = sB + (sl * 16 + tr_k) * ROWT + (wn * WTN + j * 32 + tr_n) * 2;
+        i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)p);
+        i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(p + 4 * ROWT));
+        f.b[j] = u32x4{__builtin_bit_cast(uint2, lo).x, __builtin_bit_cast(uint2, lo).y,
+                       __builtin_bit_cast(uint2, hi).x, __builtin_bit_cast(uint2, hi).y};
+      } else {
+        f.b[j] = ld16(sB + (wn * WTN + j * 32 + lrow) * ROWA + sl * 32 + lko);
+      }
     }
-    if (kt + 1 < nk) store_stage((kt + 1) & 1);
+  };
+  // D = Bop * Aop^T: D rows are output columns n, D columns are rows m, so each
+  // lane ends up holding runs of 4 consecutive n of one output row.
+  auto mma_frags = [&](const Frag &f) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) mma32(E(), acc[i][j], f.b[j], f.a[i]);
+  };
+  // All slices of the stage in `buf`; slice 0's fragments arrive in f0.
+  auto compute = [&](int buf, const Frag &f0) {
+    Frag cur = f0;
+#pragma unroll
+    for (int s = 0; s < SPW; ++s) {
+      Frag nxt;
+      if (s + 1 < SPW) read_frags(buf, s + 1, nxt);
+      mma_frags(cur);
+      if (s + 1 < SPW) cur = nxt;
+    }
+  };
+
+  // ---- main loop, unrolled by two so the register sets are static ----------
+  // Each step is branch-free: loads of stages past the end select out-of-range
+  // offsets (zeros, no memory traffic) and stores of such stages land in an LDS
+  // buffer that is never read again.
+  Frag f0;
+  if constexpr (NBUF == 3) {
+    load_stage(IC<0>(), 0);
+    load_stage(IC<1>(), 1);
+    store_stage(IC<0>(), 0);
+    load_stage(IC<0>(), 2);
+    store_stage(IC<1>(), 1);
+    __syncthreads();
+    read_frags(0, 0, f0);
+    int cb = 0;  // LDS buffer of stage kt
+    auto step = [&](auto PAR, int kt) {
+      constexpr int P = decltype(PAR)::value;  // kt % 2
+      const int nb1 = cb == 2 ? 0 : cb + 1, nb2 = nb1 == 2 ? 0 : nb1 + 1;
+      load_stage(IC<1 - P>(), kt + 3);
+      // Keep the loads at the top of the step: left alone, the scheduler sinks
+      // them to the end of the step, exposing the full memory latency.
+      __builtin_amdgcn_sched_barrier(0);
+      store_stage(IC<P>(), nb2);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(cb, f0);
+      read_frags(nb1, 0, f0);
+      __syncthreads();
+      cb = nb1;
+    };
+    for (int kt = 0; kt < nk; kt += 2) {
+      step(IC<0>(), kt);
+      if (kt + 1 < nk) step(IC<1>(), kt + 1);
+    }
+  } else {
+    load_stage(IC<0>(), 0);
+    load_stage(IC<1>(), 1);
+    store_stage(IC<0>(), 0);
+    __syncthreads();
+    auto step = [&](auto PAR, int kt) {
+      constexpr int P = decltype(PAR)::value;  // kt % 2: LDS buffer and register set
+      load_stage(IC<P>(), kt + 2);
+      __builtin_amdgcn_sched_barrier(0);
+      store_stage(IC<1 - P>(), 1 - P);
+      __builtin_amdgcn_sched_barrier(0);
+      read_frags(P, 0, f0);
+      compute(P, f0);
+      __syncthreads();
+    };
+    for (int kt = 0; kt < nk; kt += 2) {
+      step(IC<0>(), kt);
+      if (kt + 1 < nk) step(IC<1>(), kt + 1);
+    }
+  }
+  // LoRA tail stages (r > 0): not pipelined, at most two.
+  for (int tt = 0; tt < nk_tail; ++tt) {
+    load_tail(tt * BKE);
+    store_stage(IC<0>(), 0);
+    __syncthreads();
+    read_frags(0, 0, f0);
+    compute(0, f0);
     __syncthreads();
   }
 
-  // Epilogue: lane holds D[n][m] at m = lane % 32, n = 8q + 4(lane / 32) + e
-  // for accumulator element 4q + e.
+  // ---- cross-wave reduction over the WK k-split (fixed order) ----------------
+  // Block b = i*FN + j of the wave tile is owned by wave wk == b % WK.  In phase
+  // r the wave hands block b to owner (wk + r) % WK through LDS.
+  if constexpr (WK > 1) {
+    constexpr int OWN = NB / WK;
+    char *slot_base = smem + (wm * WN + wn) * WK * OWN * 4096;
+#pragma unroll
+    for (int r = 1; r < WK; ++r) {
+      const int to = (wk + r) % WK;
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        if (b % WK == to) {
+          char *p = slot_base + (to * OWN + b / WK) * 4096 + lane * 16;
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            *(f32x4 *)(p + q * 1024) = f32x4{acc[b / FN][b % FN][4 * q + 0], acc[b / FN][b % FN][4 * q + 1],
+                                             acc[b / FN][b % FN][4 * q + 2], acc[b / FN][b % FN][4 * q + 3]};
+        }
+      }
+      __syncthreads();
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        if (b % WK == wk) {
+          const char *p = slot_base + (wk * OWN + b / WK) * 4096 + lane * 16;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const f32x4 v = *(const f32x4 *)(p + q * 1024);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc[b / FN][b % FN][4 * q + e] += v[e];
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+
+  // ---- epilogue: lane holds D[n][m] at m = lane % 32, n = 8q + 4(lane / 32) + e
   T *C = (T *)g.C;
 #pragma unroll
-  for (int i = 0; i < FM; ++i) {
+  for (int b = 0; b < NB; ++b) {
+    if (WK > 1 && b % WK != wk) continue;
+    const int i = b / FN, j = b % FN;
     const int m = m0 + wm * WTM + i * 32 + lrow;
 #pragma unroll
-    for (int j = 0; j < FN; ++j) {
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int n = n0 + wn * WTN + j * 32 + 8 * q + 4 * (lane >> 5);
-        if (m < g.M && n < g.N) {
-          T *dst = C + (int64_t)m * g.ldc + n;
-          if constexpr (sizeof(T) == 2) {
-            uint32_t lo = (uint32_t)E::from_float(acc[i][j][4 * q + 0]) |
-                          ((uint32_t)E::from_float(acc[i][j][4 * q + 1]) << 16);
-            uint32_t hi = (uint32_t)E::from_float(acc[i][j][4 * q + 2]) |
-                          ((uint32_t)E::from_float(acc[i][j][4 * q + 3]) << 16);
-            *(uint2 *)dst = make_uint2(lo, hi);
-          } else {
-            *(f32x4 *)dst = f32x4{acc[i][j][4 * q + 0], acc[i][j][4 * q + 1],
-                                  acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
-          }
+    for (int q = 0; q < 4; ++q) {
+      const int n = n0 + wn * WTN + j * 32 + 8 * q + 4 * (lane >> 5);
+      if (m < g.M && n < g.N) {
+        T *dst = C + (int64_t)m * g.ldc + n;
+        if constexpr (ES == 2) {
+          uint32_t lo = (uint32_t)E::from_float(acc[i][j][4 * q + 0]) |
+                        ((uint32_t)E::from_float(acc[i][j][4 * q + 1]) << 16);
+          uint32_t hi = (uint32_t)E::from_float(acc[i][j][4 * q + 2]) |
+                        ((uint32_t)E::from_float(acc[i][j][4 * q + 3]) << 16);
+          *(uint2 *)dst = make_uint2(lo, hi);
+        } else {
+          *(f32x4 *)dst = f32x4{acc[i][j][4 * q + 0], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                                acc[i][j][4 * q + 3]};
         }
       }
     }
   }
 }
 
-template <class E, int BM, int BN, int WM, int WN, bool KMAJ>
-static hipError_t launch_tile(const GemmArgs &g, hipStream_t st) {
-  const int tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_kernel<E, BM, BN, WM, WN, KMAJ>), dim3(tiles), dim3(WM * WN * 64), 0,
-                     st, g);
+// Tile rows per XCD group: each XCD's ~ntiles/8 consecutive tiles form a block
+// of about sqrt(c * BN / BM) tile rows, which minimises the A rows plus B
+// columns it streams.
+static int pick_group_m(int tiles_m, int tiles_n, int BM, int BN) {
+  const double c = (double)tiles_m * tiles_n / 8.0;
+  int gmv = (int)(__builtin_sqrt(c * BN / BM) + 0.5);
+  if (gmv < 1) gmv = 1;
+  if (gmv > tiles_m) gmv = tiles_m;
+  return gmv;
+}
+
+template <class E, int BM, int BN, int WM, int WN, int WK, int BMODE, int BKB, int NBUF>
+static hipError_t launch_cfg(const GemmArgs &g, hipStream_t st) {
+  const int tm = (g.M + BM - 1) / BM, tn = (g.N + BN - 1) / BN;
+  hipLaunchKernelGGL((gemm_kernel<E, BM, BN, WM, WN, WK, BMODE, BKB, NBUF>), dim3(tm * tn),
+                     dim3(64 * WM * WN * WK), 0, st, g, pick_group_m(tm, tn, BM, BN));
   return hipGetLastError();
 }
 
 hipError_t launch_gemm(const GemmArgs &g, Dtype dt, bool b_kmajor, hipStream_t st) {
   if (dt == DT_BF16)
-    return b_kmajor ? launch_tile<BF16, 128, 128, 2, 2, true>(g, st)
-                    : launch_tile<BF16, 128, 128, 2, 2, false>(g, st);
-  return b_kmajor ? launch_tile<F32, 128, 128, 2, 2, true>(g, st)
-                  : launch_tile<F32, 128, 128, 2, 2, false>(g, st);
+    return b_kmajor ? launch_cfg<BF16, 128, 128, 2, 2, 2, B_KMAJ_TR, 128, 3>(g, st)
+                    : launch_cfg<BF16, 128, 128, 2, 2, 2, B_ROW, 128, 3>(g, st);
+  return b_kmajor ? launch_cfg<F32, 128, 128, 2, 2, 1, B_KMAJ_REG, 128, 2>(g, st)
+                  : launch_cfg<F32, 128, 128, 2, 2, 1, B_ROW, 128, 2>(g, st);
 }
 
 }  // namespace lora
