@@ -26,18 +26,14 @@ lora_status_t fail(lora_status_t s, const char *msg) {
 // ----- kernel timing hook ----------------------------------------------------
 enum KernelId {
   K_GEMM_FWD = 0,     // y  = x W^T + (s u) B^T
-  K_GEMM_BWD_DX,      // dx = dy W + du A
+  K_GEMM_BWD_DX,      // dx = dy W + du A, with the dA / dB token reductions alongside
   K_GEMM_FROZEN_DX,   // dx = dy W (rank 0)
-  K_LORA_DOWN,        // u  = x A^T
-  K_LORA_DY_B,        // du = s dy B
-  K_DB_PARTS,         // dB partial sums over token chunks
-  K_DA_PARTS,         // dA partial sums over token chunks
-  K_REDUCE_PARTS,     // fixed-order sum of the partials
+  K_LORA_DOWN,        // u  = x A^T (+ LoRA-step operands)
+  K_LORA_DY_B,        // du = s dy B (+ LoRA-step operand)
   K_COUNT
 };
-const char *kKernelNames[K_COUNT] = {"gemm_fwd",   "gemm_bwd_dx", "gemm_frozen_dx",
-                                     "lora_down",  "lora_dy_b",   "db_parts",
-                                     "da_parts",   "reduce_parts"};
+const char *kKernelNames[K_COUNT] = {"gemm_fwd", "gemm_bwd_dx", "gemm_frozen_dx", "lora_down",
+                                     "lora_dy_b"};
 
 struct EventPair {
   hipEvent_t a, b;
@@ -69,6 +65,7 @@ struct Timed {
 // ----- validation helpers ------------------------------------------------------
 constexpr int64_t kMaxElems = (int64_t(1) << 31) - 1;
 constexpr int kMaxRank = 128;
+constexpr int64_t kMaxDim = int64_t(1) << 20;  // keeps every tile's byte offsets within 32 bits
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -104,29 +101,50 @@ lora_status_t check_shapes(int64_t T, int64_t d_in, int64_t d_out, int64_t r, lo
   if (d_in % 8 || d_out % 8) return fail(LORA_EUNSUPPORTED, "d_in and d_out must be multiples of 8");
   if (T > kMaxElems / d_in || T > kMaxElems / d_out || d_in > kMaxElems / d_out)
     return fail(LORA_EUNSUPPORTED, "a matrix has 2^31 or more elements");
+  if (d_in > kMaxDim || d_out > kMaxDim)
+    return fail(LORA_EUNSUPPORTED, "d_in and d_out must be at most 2^20");
   return LORA_OK;
 }
 
-// Workspace layout of the backward pass (offsets in bytes, 256-byte aligned).
+// Workspace layouts (offsets in bytes, 256-byte aligned).
+struct FwdLayout {
+  size_t u, utail, bpad, total;
+  int ldt;
+};
+FwdLayout fwd_layout(int64_t T, int64_t K, int64_t N, int64_t r, lora_dtype_t dt) {
+  FwdLayout L{};
+  if (r == 0) return L;
+  const Dtype d = dt == LORA_BF16 ? DT_BF16 : DT_F32;
+  L.ldt = tail_ld((int)r, d);
+  size_t off = 0;
+  L.u = off;
+  off += round256((size_t)T * r * 4);
+  L.utail = off;
+  off += round256((size_t)T * L.ldt * esize(dt));
+  L.bpad = off;
+  off += round256((size_t)N * L.ldt * esize(dt));
+  L.total = off;
+  return L;
+}
+
 struct BwdLayout {
-  size_t u, du, dbp, dap, total;
-  int nch_b, rpc_b, nch_a, rpc_a;
+  size_t u, du, dutail, total;
+  int ldt;
 };
 BwdLayout bwd_layout(int64_t T, int64_t K, int64_t N, int64_t r, lora_dtype_t dt) {
+  (void)K;
+  (void)N;
   BwdLayout L{};
   if (r == 0) return L;
   const Dtype d = dt == LORA_BF16 ? DT_BF16 : DT_F32;
-  col_chunking((int)T, (int)N, (int)r, d, &L.nch_b, &L.rpc_b);
-  col_chunking((int)T, (int)K, (int)r, d, &L.nch_a, &L.rpc_a);
+  L.ldt = tail_ld((int)r, d);
   size_t off = 0;
   L.u = off;
   off += round256((size_t)T * r * 4);
   L.du = off;
   off += round256((size_t)T * r * 4);
-  L.dbp = off;
-  off += round256((size_t)L.nch_b * N * r * 4);
-  L.dap = off;
-  off += round256((size_t)L.nch_a * K * r * 4);
+  L.dutail = off;
+  off += round256((size_t)T * L.ldt * esize(dt));
   L.total = off;
   return L;
 }
@@ -154,7 +172,7 @@ size_t lora_linear_workspace_bytes(lora_op_t op, int64_t T, int64_t d_in, int64_
     return (size_t)-1;
   switch (op) {
     case LORA_OP_FWD:
-      return r > 0 ? round256((size_t)T * r * 4) : 0;
+      return fwd_layout(T, d_in, d_out, r, dt).total;
     case LORA_OP_BWD:
       return bwd_layout(T, d_in, d_out, r, dt).total;
     case LORA_OP_FROZEN_DX:
@@ -191,22 +209,36 @@ lora_status_t lora_linear_fwd(const void *x, const void *W, const void *A, const
 
   hipStream_t st = (hipStream_t)hip_stream;
   const Dtype d = dt == LORA_BF16 ? DT_BF16 : DT_F32;
-  float *u = nullptr;
-  if (r > 0) {
-    u = u_save ? u_save : (float *)ws;
-    Timed t(K_LORA_DOWN, st);
-    hipError_t e = launch_row_skinny(x, d_in, (int)T, (int)d_in, A, d_in, false, (int)r, 1.0f, u, d, st);
-    t.done();
-    if (e != hipSuccess) return hip_fail(e, "lora_down launch");
-  }
   GemmArgs g{};
   g.A = x; g.lda = d_in;
   g.B = W; g.ldb = d_in;
   g.M = (int)T; g.N = (int)d_out; g.K = (int)d_in;
-  g.A2 = u; g.s2 = scale; g.B2 = B; g.ldb2 = r; g.r = (int)r;
   g.C = y; g.ldc = d_out;
+  if (r > 0) {
+    const FwdLayout L = fwd_layout(T, d_in, d_out, r, dt);
+    char *wsb = (char *)ws;
+    RowArgs ra{};
+    ra.X = x; ra.ldx = d_in; ra.M = (int)T; ra.L = (int)d_in;
+    ra.V = A; ra.ldv = d_in; ra.vmode = V_ROW; ra.r = (int)r;
+    ra.out_mult = 1.0f; ra.out = u_save ? u_save : (float *)(wsb + L.u);
+    ra.tail = wsb + L.utail; ra.ldt = L.ldt; ra.tail_mult = scale;
+    // B itself serves as the LoRA-step operand when its rows are whole 16-byte
+    // vectors; otherwise the kernel writes a zero-padded copy.
+    const bool pad_b = r % (16 / (int64_t)esize(dt)) != 0;
+    if (pad_b) {
+      ra.bcopy_src = B; ra.bcopy_dst = wsb + L.bpad; ra.bcopy_rows = (int)d_out;
+    }
+    Timed t(K_LORA_DOWN, st);
+    hipError_t e = launch_row_skinny(ra, d, st);
+    t.done();
+    if (e != hipSuccess) return hip_fail(e, "lora_down launch");
+    g.A2 = wsb + L.utail; g.lda2 = L.ldt;
+    g.B2 = pad_b ? (const void *)(wsb + L.bpad) : B;
+    g.ldb2 = pad_b ? L.ldt : r;
+    g.r = (int)r;
+  }
   Timed t(K_GEMM_FWD, st);
-  hipError_t e = launch_gemm(g, d, false, st);
+  hipError_t e = launch_gemm(g, d, false, nullptr, st);
   t.done();
   if (e != hipSuccess) return hip_fail(e, "gemm_fwd launch");
   return LORA_OK;
@@ -247,14 +279,14 @@ lora_status_t lora_linear_bwd(const void *x, const void *W, const void *A, const
   hipStream_t st = (hipStream_t)hip_stream;
   const Dtype d = dt == LORA_BF16 ? DT_BF16 : DT_F32;
   hipError_t e;
+  GemmArgs g{};
+  g.A = dy; g.lda = d_out;
+  g.B = W; g.ldb = d_in;
+  g.M = dx ? (int)T : 0; g.N = (int)d_in; g.K = (int)d_out;
+  g.C = dx; g.ldc = d_in;
   if (r == 0) {
-    GemmArgs g{};
-    g.A = dy; g.lda = d_out;
-    g.B = W; g.ldb = d_in;
-    g.M = (int)T; g.N = (int)d_in; g.K = (int)d_out;
-    g.C = dx; g.ldc = d_in;
     Timed t(K_GEMM_BWD_DX, st);
-    e = launch_gemm(g, d, true, st);
+    e = launch_gemm(g, d, true, nullptr, st);
     t.done();
     return e == hipSuccess ? LORA_OK : hip_fail(e, "gemm_bwd_dx launch");
   }
@@ -262,54 +294,40 @@ lora_status_t lora_linear_bwd(const void *x, const void *W, const void *A, const
   const BwdLayout L = bwd_layout(T, d_in, d_out, r, dt);
   char *wsb = (char *)ws;
   const float *u = u_saved;
-  if (!u) {
-    float *ur = (float *)(wsb + L.u);
+  if (!u) {  // rematerialise u = x A^T instead of having stored it
+    RowArgs ra{};
+    ra.X = x; ra.ldx = d_in; ra.M = (int)T; ra.L = (int)d_in;
+    ra.V = A; ra.ldv = d_in; ra.vmode = V_ROW; ra.r = (int)r;
+    ra.out_mult = 1.0f; ra.out = (float *)(wsb + L.u);
     Timed t(K_LORA_DOWN, st);
-    e = launch_row_skinny(x, d_in, (int)T, (int)d_in, A, d_in, false, (int)r, 1.0f, ur, d, st);
+    e = launch_row_skinny(ra, d, st);
     t.done();
     if (e != hipSuccess) return hip_fail(e, "lora_down launch");
-    u = ur;
+    u = (const float *)(wsb + L.u);
   }
   float *du = (float *)(wsb + L.du);
-  float *dbp = (float *)(wsb + L.dbp);
-  float *dap = (float *)(wsb + L.dap);
   {
+    RowArgs ra{};
+    ra.X = dy; ra.ldx = d_out; ra.M = (int)T; ra.L = (int)d_out;
+    ra.V = B; ra.ldv = r; ra.vmode = V_KMAJ_TR; ra.r = (int)r;
+    ra.out_mult = scale; ra.out = du;
+    ra.tail = wsb + L.dutail; ra.ldt = L.ldt; ra.tail_mult = scale;
     Timed t(K_LORA_DY_B, st);
-    e = launch_row_skinny(dy, d_out, (int)T, (int)d_out, B, r, true, (int)r, scale, du, d, st);
+    e = launch_row_skinny(ra, d, st);
     t.done();
     if (e != hipSuccess) return hip_fail(e, "lora_dy_b launch");
   }
-  {
-    Timed t(K_DB_PARTS, st);
-    e = launch_col_skinny(dy, d_out, (int)T, (int)d_out, u, (int)r, L.nch_b, L.rpc_b, dbp, d, st);
-    t.done();
-    if (e != hipSuccess) return hip_fail(e, "db_parts launch");
-  }
-  if (dx) {
-    GemmArgs g{};
-    g.A = dy; g.lda = d_out;
-    g.B = W; g.ldb = d_in;
-    g.M = (int)T; g.N = (int)d_in; g.K = (int)d_out;
-    g.A2 = du; g.s2 = 1.0f; g.B2 = A; g.ldb2 = d_in; g.r = (int)r;
-    g.C = dx; g.ldc = d_in;
-    Timed t(K_GEMM_BWD_DX, st);
-    e = launch_gemm(g, d, true, st);
-    t.done();
-    if (e != hipSuccess) return hip_fail(e, "gemm_bwd_dx launch");
-  }
-  {
-    Timed t(K_DA_PARTS, st);
-    e = launch_col_skinny(x, d_in, (int)T, (int)d_in, du, (int)r, L.nch_a, L.rpc_a, dap, d, st);
-    t.done();
-    if (e != hipSuccess) return hip_fail(e, "da_parts launch");
-  }
-  {
-    Timed t(K_REDUCE_PARTS, st);
-    e = launch_reduce_parts(dbp, L.nch_b, (int)d_out, (int)r, scale, dB, false, st);
-    if (e == hipSuccess) e = launch_reduce_parts(dap, L.nch_a, (int)d_in, (int)r, 1.0f, dA, true, st);
-    t.done();
-    if (e != hipSuccess) return hip_fail(e, "reduce_parts launch");
-  }
+  SideArgs sd{};
+  sd.T = (int)T; sd.r = (int)r; sd.njobs = 2;
+  sd.job[0] = ColJob{x, d_in, (int)d_in, du, dA, 1, 1.0f};
+  sd.job[1] = ColJob{dy, d_out, (int)d_out, u, dB, 0, scale};
+  g.A2 = wsb + L.dutail; g.lda2 = L.ldt;
+  g.B2 = A; g.ldb2 = d_in;
+  g.r = (int)r;
+  Timed t(K_GEMM_BWD_DX, st);
+  e = launch_gemm(g, d, true, &sd, st);
+  t.done();
+  if (e != hipSuccess) return hip_fail(e, "gemm_bwd_dx launch");
   return LORA_OK;
 }
 
@@ -334,7 +352,7 @@ lora_status_t frozen_linear_bwd_dx(const void *dy, const void *W, void *dx, int6
   g.M = (int)T; g.N = (int)d_in; g.K = (int)d_out;
   g.C = dx; g.ldc = d_in;
   Timed t(K_GEMM_FROZEN_DX, st);
-  hipError_t e = launch_gemm(g, dt == LORA_BF16 ? DT_BF16 : DT_F32, true, st);
+  hipError_t e = launch_gemm(g, dt == LORA_BF16 ? DT_BF16 : DT_F32, true, nullptr, st);
   t.done();
   return e == hipSuccess ? LORA_OK : hip_fail(e, "gemm_frozen_dx launch");
 }

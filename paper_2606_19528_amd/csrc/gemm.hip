@@ -24,6 +24,9 @@
 //  * Workgroups are mapped to tiles XCD by XCD (the dispatcher deals workgroup
 //    ids round-robin over the 8 XCDs, each with its own L2), and each XCD's
 //    share of tiles is a compact block of GM tile rows.
+#include <type_traits>
+
+#include "colred.hpp"
 #include "kernels.hpp"
 #include "launch.hpp"
 
@@ -40,7 +43,8 @@ struct IC {
 };
 
 template <class E, int BM, int BN, int WM, int WN, int WK, int BMODE, int BKB, int NBUF>
-__global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int group_m) {
+__global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int group_m,
+                                                                 SideArgs side, int nside) {
   typedef typename E::T T;
   constexpr int NT = 64 * WM * WN * WK;
   constexpr int VEC = E::VEC;
@@ -62,11 +66,14 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   constexpr int A_BYTES = BM * ROWA;
   constexpr int B_BYTES = BMODE == B_KMAJ_TR ? BKE * ROWT : BN * ROWA;
   constexpr int STAGE = A_BYTES + B_BYTES;
-  constexpr int RED_BYTES = WK > 1 ? BM * BN * 4 : 0;
-  constexpr int LDS = NBUF * STAGE > RED_BYTES ? NBUF * STAGE : RED_BYTES;
+  constexpr int OWN = (NB + WK - 1) / WK;    // accumulator blocks owned per wave (k-split)
+  constexpr int RED_BYTES = WK > 1 ? WM * WN * WK * OWN * 4096 : 0;
+  constexpr int LDS0 = NBUF * STAGE > RED_BYTES ? NBUF * STAGE : RED_BYTES;
+  constexpr int SIDE = side_lds_bytes<E, WM * WN * WK>();
+  constexpr int LDS = LDS0 > SIDE ? LDS0 : SIDE;
   constexpr uint32_t OOB = 0x80000000u;      // offset past every buffer: loads return 0
   static_assert(WM * WN * WK == 4 || WM * WN * WK == 8, "four or eight waves");
-  static_assert(SLICES % WK == 0 && NB % WK == 0, "k split");
+  static_assert(SLICES % WK == 0, "k split");
   static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile");
   static_assert(BMODE != B_KMAJ_TR || ES == 2, "transposed LDS reads are bf16");
   static_assert(NBUF == 2 || NBUF == 3, "LDS ring depth");
@@ -84,9 +91,16 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   const int tiles_m = (g.M + BM - 1) / BM;
   const int tiles_n = (g.N + BN - 1) / BN;
   const int ntiles = tiles_m * tiles_n;
+  // The first `nside` workgroups (a multiple of 8, so the XCD of a tile
+  // workgroup is unchanged) run the token-reduction side items; they start
+  // first and overlap with the tiles.
+  if ((int)blockIdx.x < nside) {
+    if ((int)blockIdx.x < side_items_total<E>(side)) side_item<E, WM * WN * WK>(side, blockIdx.x, smem);
+    return;
+  }
   int t;
   {
-    const int id = blockIdx.x;
+    const int id = (int)blockIdx.x - nside;
     const int xcd = id & 7, local = id >> 3;
     const int base = ntiles >> 3, rem = ntiles & 7;
     t = xcd * base + (xcd < rem ? xcd : rem) + local;
@@ -98,27 +112,36 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   const int nt = (t % gsize) / gm;
   const int m0 = mt * BM, n0 = nt * BN;
 
-  const T *B2 = (const T *)g.B2;
-  const int nk = (g.K + BKE - 1) / BKE;
-  const int nk_tail = g.r > 0 ? (g.r + BKE - 1) / BKE : 0;
+  const int nk_main = (g.K + BKE - 1) / BKE;
+  const int nk = nk_main + (g.r > 0 ? (g.r + BKE - 1) / BKE : 0);  // + LoRA steps
 
   // Buffer resources.  The tile's rows past M (and, for row-major B, past N)
-  // lie beyond num_records; k past K is masked per stage by selecting OOB.
+  // lie beyond num_records; k past K (or j past r) is masked per stage by
+  // selecting OOB.  The LoRA step reads A2 / B2 through resources of its own.
+  const int mrows = min(g.M - m0, BM);
   const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc(
-      (void *)((const char *)g.A + (int64_t)m0 * g.lda * ES), (short)0,
-      (int)(min(g.M - m0, BM) * g.lda * ES), 0x00020000);
-  __amdgpu_buffer_rsrc_t rsB;
-  if constexpr (BMODE == B_ROW)
+      (void *)((const char *)g.A + (int64_t)m0 * g.lda * ES), (short)0, (int)(mrows * g.lda * ES),
+      0x00020000);
+  const __amdgpu_buffer_rsrc_t rsA2 = __builtin_amdgcn_make_buffer_rsrc(
+      (void *)((const char *)g.A2 + (int64_t)m0 * g.lda2 * ES), (short)0,
+      g.r > 0 ? (int)(mrows * g.lda2 * ES) : 0, 0x00020000);
+  __amdgpu_buffer_rsrc_t rsB, rsB2;
+  if constexpr (BMODE == B_ROW) {
+    const int nrows = min(g.N - n0, BN);
     rsB = __builtin_amdgcn_make_buffer_rsrc((void *)((const char *)g.B + (int64_t)n0 * g.ldb * ES),
-                                            (short)0, (int)(min(g.N - n0, BN) * g.ldb * ES),
-                                            0x00020000);
-  uint32_t va[A_PER], vb[BMODE == B_KMAJ_REG ? KB_PER : B_PER];
+                                            (short)0, (int)(nrows * g.ldb * ES), 0x00020000);
+    rsB2 = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)((const char *)g.B2 + (int64_t)n0 * g.ldb2 * ES), (short)0,
+        g.r > 0 ? (int)(nrows * g.ldb2 * ES) : 0, 0x00020000);
+  }
+  uint32_t va[A_PER], va2[A_PER], vb[BMODE == B_KMAJ_REG ? KB_PER : B_PER], vb2[B_PER];
   int kca[A_PER], kcb[B_PER];
 #pragma unroll
   for (int i = 0; i < A_PER; ++i) {
     const int c = tid + i * NT;
     kca[i] = (c % CPR) * VEC;
     va[i] = c < A_CH ? (uint32_t)((c / CPR) * g.lda * ES + (c % CPR) * 16) : OOB;
+    va2[i] = c < A_CH ? (uint32_t)((c / CPR) * g.lda2 * ES + (c % CPR) * 16) : OOB;
   }
   if constexpr (BMODE == B_ROW) {
 #pragma unroll
@@ -126,6 +149,7 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
       const int c = tid + i * NT;
       kcb[i] = (c % CPR) * VEC;
       vb[i] = c < B_CH ? (uint32_t)((c / CPR) * g.ldb * ES + (c % CPR) * 16) : OOB;
+      vb2[i] = c < B_CH ? (uint32_t)((c / CPR) * g.ldb2 * ES + (c % CPR) * 16) : OOB;
     }
   } else if constexpr (BMODE == B_KMAJ_TR) {
 #pragma unroll
@@ -133,6 +157,7 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
       const int c = tid + i * NT;
       const int kr = c / NBV, nc = c % NBV;
       vb[i] = (c < B_CH && n0 + nc * VEC < g.N) ? (uint32_t)(kr * g.ldb * ES + nc * 16) : OOB;
+      vb2[i] = (c < B_CH && n0 + nc * VEC < g.N) ? (uint32_t)(kr * g.ldb2 * ES + nc * 16) : OOB;
     }
   } else {
 #pragma unroll
@@ -147,91 +172,51 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   u32x4 ra[2][A_PER];
   u32x4 rb[2][RB];
 
-  // ---- global -> register set S for main stage kt (zeros past the end) ------
+  // ---- global -> register set S for stage kt (zeros past the end) ----------
+  // Stages kt < nk_main stream x/dy and W; the following ones stream the LoRA
+  // operands (j = (kt - nk_main) * BKE ...).  The choice is a uniform select
+  // of resources and offsets, so the step stays branch-free.
   auto load_stage = [&](auto SET, int kt) {
     constexpr int S = decltype(SET)::value;
-    const int k0 = kt * BKE;
-    const int krem = g.K - k0;  // valid k remaining in this stage (uniform)
+    const bool lora = kt >= nk_main;
+    const int k0 = (lora ? kt - nk_main : kt) * BKE;
+    const int krem = (lora ? g.r : g.K) - k0;  // valid k remaining (uniform)
     const int soff = k0 * ES;
+    const __amdgpu_buffer_rsrc_t ra_rs = lora ? rsA2 : rsA;
 #pragma unroll
     for (int i = 0; i < A_PER; ++i)
-      ra[S][i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                               rsA, kca[i] < krem ? va[i] : OOB, soff, 0));
+      ra[S][i] = __builtin_bit_cast(
+          u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                     ra_rs, kca[i] < krem ? (lora ? va2[i] : va[i]) : OOB, soff, 0));
     if constexpr (BMODE == B_ROW) {
+      const __amdgpu_buffer_rsrc_t rb_rs = lora ? rsB2 : rsB;
 #pragma unroll
       for (int i = 0; i < B_PER; ++i)
-        rb[S][i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                                 rsB, kcb[i] < krem ? vb[i] : OOB, soff, 0));
+        rb[S][i] = __builtin_bit_cast(
+            u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                       rb_rs, kcb[i] < krem ? (lora ? vb2[i] : vb[i]) : OOB, soff, 0));
     } else {
-      // k-major: rebase on this stage's first k row; rows past K are out of range.
+      // k-major: rebase on this stage's first k row; rows past K (r) are out of range.
+      const char *base = lora ? (const char *)g.B2 + ((int64_t)k0 * g.ldb2 + n0) * ES
+                              : (const char *)g.B + ((int64_t)k0 * g.ldb + n0) * ES;
+      const int64_t ld = lora ? g.ldb2 : g.ldb;
       const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-          (void *)((const char *)g.B + ((int64_t)k0 * g.ldb + n0) * ES), (short)0,
-          (int)(krem > 0 ? min(krem, BKE) * g.ldb * ES : 0), 0x00020000);
+          (void *)base, (short)0, (int)(krem > 0 ? min(krem, BKE) * ld * ES : 0), 0x00020000);
       if constexpr (BMODE == B_KMAJ_TR) {
 #pragma unroll
         for (int i = 0; i < B_PER; ++i)
-          rb[S][i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, vb[i], 0, 0));
+          rb[S][i] = __builtin_bit_cast(
+              u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, lora ? vb2[i] : vb[i], 0, 0));
       } else {
+        // fp32 check mode: W and A have the same row length (d_in), so one
+        // set of offsets serves both.
 #pragma unroll
         for (int i = 0; i < KB_PER; ++i)
 #pragma unroll
           for (int e = 0; e < VEC; ++e)
             rb[S][i * VEC + e] = __builtin_bit_cast(
                 u32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                           rs, vb[i] == OOB ? OOB : vb[i] + (uint32_t)(e * g.ldb * ES), 0, 0));
-      }
-    }
-  };
-
-  // ---- LoRA tail stage into set 0: reduction index j in [j0, j0 + BKE) ------
-  auto load_tail = [&](int j0) {
-#pragma unroll
-    for (int i = 0; i < A_PER; ++i) {
-      const int c = tid + i * NT;
-      const int row = c / CPR, kc = c % CPR;
-      const int m = m0 + row;
-      float f[VEC];
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) {
-        const int j = j0 + kc * VEC + e;
-        f[e] = (c < A_CH && m < g.M && j < g.r) ? g.s2 * g.A2[(int64_t)m * g.r + j] : 0.0f;
-      }
-      ra[0][i] = pack_vec(E(), f);
-    }
-    if constexpr (BMODE == B_ROW) {
-#pragma unroll
-      for (int i = 0; i < B_PER; ++i) {
-        const int c = tid + i * NT;
-        const int row = c / CPR, kc = c % CPR;
-        const int n = n0 + row;
-        float f[VEC];
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) {
-          const int j = j0 + kc * VEC + e;
-          f[e] = (c < B_CH && n < g.N && j < g.r) ? E::to_float(B2[(int64_t)n * g.r + j]) : 0.0f;
-        }
-        rb[0][i] = pack_vec(E(), f);
-      }
-    } else if constexpr (BMODE == B_KMAJ_TR) {
-#pragma unroll
-      for (int i = 0; i < B_PER; ++i) {
-        const int c = tid + i * NT;
-        const int kr = c / NBV, nc = c % NBV;
-        const int j = j0 + kr, n = n0 + nc * VEC;
-        rb[0][i] = (c < B_CH && j < g.r && n < g.N) ? ld16(B2 + (int64_t)j * g.ldb2 + n) : zero16();
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < KB_PER; ++i) {
-        const int b = tid + i * NT;
-        const int kb = b % (BKE / VEC), nb = b / (BKE / VEC);
-        const int n = n0 + nb * VEC;
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) {
-          const int j = j0 + kb * VEC + e;
-          rb[0][i * VEC + e] = (b < KB_BLK && n < g.N && j < g.r) ? ld16(B2 + (int64_t)j * g.ldb2 + n)
-                                                                   : zero16();
-        }
+                           rs, vb[i] == OOB ? OOB : vb[i] + (uint32_t)(e * ld * ES), 0, 0));
       }
     }
   };
@@ -383,21 +368,10 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
       if (kt + 1 < nk) step(IC<1>(), kt + 1);
     }
   }
-  // LoRA tail stages (r > 0): not pipelined, at most two.
-  for (int tt = 0; tt < nk_tail; ++tt) {
-    load_tail(tt * BKE);
-    store_stage(IC<0>(), 0);
-    __syncthreads();
-    read_frags(0, 0, f0);
-    compute(0, f0);
-    __syncthreads();
-  }
-
   // ---- cross-wave reduction over the WK k-split (fixed order) ----------------
   // Block b = i*FN + j of the wave tile is owned by wave wk == b % WK.  In phase
   // r the wave hands block b to owner (wk + r) % WK through LDS.
   if constexpr (WK > 1) {
-    constexpr int OWN = NB / WK;
     char *slot_base = smem + (wm * WN + wn) * WK * OWN * 4096;
 #pragma unroll
     for (int r = 1; r < WK; ++r) {
@@ -468,19 +442,59 @@ static int pick_group_m(int tiles_m, int tiles_n, int BM, int BN) {
 }
 
 template <class E, int BM, int BN, int WM, int WN, int WK, int BMODE, int BKB, int NBUF>
-static hipError_t launch_cfg(const GemmArgs &g, hipStream_t st) {
-  const int tm = (g.M + BM - 1) / BM, tn = (g.N + BN - 1) / BN;
-  hipLaunchKernelGGL((gemm_kernel<E, BM, BN, WM, WN, WK, BMODE, BKB, NBUF>), dim3(tm * tn),
-                     dim3(64 * WM * WN * WK), 0, st, g, pick_group_m(tm, tn, BM, BN));
+static hipError_t launch_cfg(const GemmArgs &g, const SideArgs *side, hipStream_t st) {
+  const int tm = g.M > 0 ? (g.M + BM - 1) / BM : 0, tn = (g.N + BN - 1) / BN;
+  SideArgs sa{};
+  int nside = 0;
+  if (side) {
+    sa = *side;
+    nside = side_workgroups(sa, std::is_same<E, BF16>::value ? DT_BF16 : DT_F32);
+  }
+  const int grid = tm * tn + nside;
+  if (grid == 0) return hipSuccess;
+  hipLaunchKernelGGL((gemm_kernel<E, BM, BN, WM, WN, WK, BMODE, BKB, NBUF>), dim3(grid),
+                     dim3(64 * WM * WN * WK), 0, st, g, tm > 0 ? pick_group_m(tm, tn, BM, BN) : 1,
+                     sa, nside);
   return hipGetLastError();
 }
 
-hipError_t launch_gemm(const GemmArgs &g, Dtype dt, bool b_kmajor, hipStream_t st) {
-  if (dt == DT_BF16)
-    return b_kmajor ? launch_cfg<BF16, 128, 128, 2, 2, 2, B_KMAJ_TR, 128, 3>(g, st)
-                    : launch_cfg<BF16, 128, 128, 2, 2, 2, B_ROW, 128, 3>(g, st);
-  return b_kmajor ? launch_cfg<F32, 128, 128, 2, 2, 1, B_KMAJ_REG, 128, 2>(g, st)
-                  : launch_cfg<F32, 128, 128, 2, 2, 1, B_ROW, 128, 2>(g, st);
+int side_workgroups(const SideArgs &s, Dtype dt) {
+  const int cols = dt == DT_BF16 ? SideShape<BF16>::COLS : SideShape<F32>::COLS;
+  int n = 0;
+  for (int i = 0; i < s.njobs; ++i) n += (s.job[i].L + cols - 1) / cols * ((s.r + 31) / 32);
+  return (n + 7) / 8 * 8;
+}
+
+// Tile shape per problem: an estimate of the time of each candidate -- full
+// waves of tiles over the 256 CUs times the per-tile cost (relative per-CU
+// throughput measured on MI355X: 128x128 0.69, 256x128 0.87, 256x256 1.0).
+static int pick_shape(int M, int N) {
+  auto cost = [&](int bm, int bn, double eff) {
+    const long tiles = (long)((M + bm - 1) / bm) * ((N + bn - 1) / bn);
+    return (double)((tiles + 255) / 256) * bm * bn / eff;
+  };
+  const double c0 = cost(128, 128, 0.69), c1 = cost(256, 128, 0.87), c2 = cost(256, 256, 1.0);
+  if (c2 <= c1 && c2 <= c0) return 2;
+  return c1 < c0 ? 1 : 0;
+}
+
+hipError_t launch_gemm(const GemmArgs &g, Dtype dt, bool b_kmajor, const SideArgs *side,
+                       hipStream_t st) {
+  if (dt == DT_BF16) {
+    switch (pick_shape(g.M, g.N)) {
+      case 2:
+        return b_kmajor ? launch_cfg<BF16, 256, 256, 4, 2, 1, B_KMAJ_TR, 128, 2>(g, side, st)
+                        : launch_cfg<BF16, 256, 256, 4, 2, 1, B_ROW, 128, 2>(g, side, st);
+      case 1:
+        return b_kmajor ? launch_cfg<BF16, 256, 128, 4, 2, 1, B_KMAJ_TR, 128, 2>(g, side, st)
+                        : launch_cfg<BF16, 256, 128, 4, 2, 1, B_ROW, 128, 2>(g, side, st);
+      default:
+        return b_kmajor ? launch_cfg<BF16, 128, 128, 2, 2, 2, B_KMAJ_TR, 128, 3>(g, side, st)
+                        : launch_cfg<BF16, 128, 128, 2, 2, 2, B_ROW, 128, 3>(g, side, st);
+    }
+  }
+  return b_kmajor ? launch_cfg<F32, 128, 128, 2, 4, 1, B_KMAJ_REG, 128, 2>(g, side, st)
+                  : launch_cfg<F32, 128, 128, 2, 4, 1, B_ROW, 128, 2>(g, side, st);
 }
 
 }  // namespace lora

@@ -9,22 +9,42 @@ namespace lora {
 
 enum Dtype { DT_BF16 = 0, DT_F32 = 1 };
 
-// C[M, N] = sum_k Aop[m][k] Bop[n][k]  (+ LoRA tail), rounded to the element type.
+// Side work run by extra workgroups of the backward GEMM launch (they
+// overlap with the dx tiles): token-reduced products
+//   dA = du^T x   out [r, L] (transposed store), scale 1
+//   dB = s dy^T u out [L, r],                    scale s
+// out[l][j] = scale * sum_t X[t*ldx + l] * V[t*r + j], t < T.
+struct ColJob {
+  const void *X;
+  int64_t ldx;
+  int L;
+  const float *V;
+  float *out;
+  int transpose_out;
+  float scale;
+};
+struct SideArgs {
+  ColJob job[2];
+  int njobs;
+  int T, r;
+};
+
+// C[M, N] = sum_k Aop[m][k] Bop[n][k]  (+ LoRA step), rounded to the element type.
 //   Aop[m][k] = A[m*lda + k]                         m < M, k < K
 //   Bop[n][k] = B[n*ldb + k]   (b_kmajor = false)    n < N
 //             = B[k*ldb + n]   (b_kmajor = true)
-// Tail (r > 0), an extra reduction over j < r appended to k:
-//   Aop2[m][j] = s2 * A2[m*r + j]  (fp32 in memory, rounded to the element type)
-//   Bop2[n][j] = B2[n*r + j]       (b_kmajor = false)
-//              = B2[j*ldb2 + n]    (b_kmajor = true)
+// LoRA step (r > 0), extra reduction over j < r appended to k, both operands
+// already in the element type:
+//   Aop2[m][j] = A2[m*lda2 + j]
+//   Bop2[n][j] = B2[n*ldb2 + j] (b_kmajor = false)  or  B2[j*ldb2 + n] (true)
 struct GemmArgs {
   const void *A;
   int64_t lda;
   const void *B;
   int64_t ldb;
   int M, N, K;
-  const float *A2;
-  float s2;
+  const void *A2;
+  int64_t lda2;
   const void *B2;
   int64_t ldb2;
   int r;
@@ -32,28 +52,41 @@ struct GemmArgs {
   int64_t ldc;
 };
 
-hipError_t launch_gemm(const GemmArgs &g, Dtype dt, bool b_kmajor, hipStream_t st);
+// GEMM launch; `side` (may be NULL) adds the token-reduction workgroups.
+hipError_t launch_gemm(const GemmArgs &g, Dtype dt, bool b_kmajor, const SideArgs *side,
+                       hipStream_t st);
 
-// out[m][j] = scale * sum_k X[m*ldx + k] * V(j, k),  m < M, j < r, k < L,
-//   V(j, k) = V[j*ldv + k] (v_kmajor = false) or V[k*ldv + j] (v_kmajor = true).
-hipError_t launch_row_skinny(const void *X, int64_t ldx, int M, int L, const void *V,
-                             int64_t ldv, bool v_kmajor, int r, float scale, float *out,
-                             Dtype dt, hipStream_t st);
+// Number of side workgroups needed for `side` (a multiple of 8).
+int side_workgroups(const SideArgs &s, Dtype dt);
 
-// Partial sums over token chunks:
-//   part[c][l][j] = sum_{t in chunk c} X[t*ldx + l] * V[t*r + j],  l < L, j < r
-// with chunk c = [c*rows_per_chunk, min(T, (c+1)*rows_per_chunk)).
-hipError_t launch_col_skinny(const void *X, int64_t ldx, int T, int L, const float *V, int r,
-                             int nchunks, int rows_per_chunk, float *part, Dtype dt,
-                             hipStream_t st);
+enum { V_ROW = 0, V_KMAJ_TR = 1, V_KMAJ_GATHER = 2 };
+// Row-skinny product out[m][j] = out_mult * sum_k X[m*ldx + k] * V(j, k),
+// V(j, k) = V[j*ldv + k] (V_ROW) or V[k*ldv + j] (k-major, ldv = r).
+// Optional: tail[m][j] = E(tail_mult * sum) for j < r, 0 up to ldt;
+// bcopy_dst[n][j] = bcopy_src[n*r + j] zero-padded to ldt, n < bcopy_rows.
+struct RowArgs {
+  const void *X;
+  int64_t ldx;
+  int M, L;
+  const void *V;
+  int64_t ldv;
+  int vmode;
+  int r;
+  float out_mult;
+  float *out;
+  void *tail;
+  int ldt;
+  float tail_mult;
+  const void *bcopy_src;
+  void *bcopy_dst;
+  int bcopy_rows;
+};
+hipError_t launch_row_skinny(const RowArgs &a, Dtype dt, hipStream_t st);
 
-// out = scale * sum_c part[c]  (fixed order c = 0, 1, ...), part [nchunks][L][r];
-// out layout [L][r], or [r][L] when transpose_out.
-hipError_t launch_reduce_parts(const float *part, int nchunks, int L, int r, float scale,
-                               float *out, bool transpose_out, hipStream_t st);
-
-// Token chunking of the column-skinny partial sums (a pure function of the
-// shapes, shared by the workspace query and the launches).
-void col_chunking(int T, int L, int r, Dtype dt, int *nchunks, int *rows_per_chunk);
+// Padded row length of the LoRA-step operands (a multiple of the GEMM stage).
+inline int tail_ld(int r, Dtype dt) {
+  const int s = dt == DT_BF16 ? 64 : 32;
+  return (r + s - 1) / s * s;
+}
 
 }  // namespace lora

@@ -188,3 +188,51 @@ def test_no_dw_sized_allocation():
     lm.lora_linear_bwd(inp["x"], inp["W"], inp["A"], inp["B"], u, inp["dy"], dx, dA, dB, 2.0, ws=ws)
     torch.cuda.synchronize()
     assert torch.cuda.max_memory_allocated() - base == 0
+
+
+def test_bwd_without_dx_matches(orc):
+    """dx = NULL runs only the dA / dB reductions; they must equal the full call's."""
+    T, K, N, r = 300, 264, 392, 16
+    inp = {k: v.cuda() for k, v in lora_inputs(T, K, N, r, seed=31).items()}
+    u = torch.empty(T, r, device="cuda")
+    y = torch.empty(T, N, dtype=torch.bfloat16, device="cuda")
+    lm.lora_linear_fwd(inp["x"], inp["W"], inp["A"], inp["B"], y, u, 2.0)
+    outs = []
+    for with_dx in (True, False):
+        dx = torch.empty(T, K, dtype=torch.bfloat16, device="cuda") if with_dx else None
+        dA = torch.full((r, K), float("nan"), device="cuda")
+        dB = torch.full((N, r), float("nan"), device="cuda")
+        lm.lora_linear_bwd(inp["x"], inp["W"], inp["A"], inp["B"], u, inp["dy"], dx, dA, dB, 2.0)
+        torch.cuda.synchronize()
+        outs.append((dA.cpu(), dB.cpu()))
+    assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1])
+
+
+def test_repeated_calls_reuse_workspace(orc):
+    """The side reductions' counters are left zeroed: back-to-back calls sharing one
+    workspace (and calls with a smaller shape in between) give identical results."""
+    T, K, N, r = 256, 392, 264, 32
+    inp = {k: v.cuda() for k, v in lora_inputs(T, K, N, r, seed=33).items()}
+    nbytes = lm.lora_linear_workspace_bytes(lm.LORA_OP_BWD, T, K, N, r, lm.LORA_BF16)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    u = torch.empty(T, r, device="cuda")
+    y = torch.empty(T, N, dtype=torch.bfloat16, device="cuda")
+    lm.lora_linear_fwd(inp["x"], inp["W"], inp["A"], inp["B"], y, u, 2.0)
+    res = []
+    for i in range(3):
+        if i == 1:  # a different, smaller problem through the same workspace
+            small = {k: v.cuda() for k, v in lora_inputs(40, 64, 72, 8, seed=34).items()}
+            lm.lora_linear_bwd(small["x"], small["W"], small["A"], small["B"], None, small["dy"],
+                               torch.empty(40, 64, dtype=torch.bfloat16, device="cuda"),
+                               torch.empty(8, 64, device="cuda"), torch.empty(72, 8, device="cuda"),
+                               2.0, ws=ws)
+        dx = torch.empty(T, K, dtype=torch.bfloat16, device="cuda")
+        dA = torch.empty(r, K, device="cuda")
+        dB = torch.empty(N, r, device="cuda")
+        lm.lora_linear_bwd(inp["x"], inp["W"], inp["A"], inp["B"], u, inp["dy"], dx, dA, dB, 2.0, ws=ws)
+        torch.cuda.synchronize()
+        res.append((dx.cpu(), dA.cpu(), dB.cpu()))
+    for a, b in zip(res[0], res[2]):
+        assert torch.equal(a, b)
+    ref = oracle_lora(orc, {k: v.cpu() for k, v in inp.items()}, 2.0)
+    compare({"dx": res[1][0], "dA": res[1][1], "dB": res[1][2]}, ref, torch.bfloat16, label="reuse")
