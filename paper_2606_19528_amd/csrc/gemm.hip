@@ -9,7 +9,9 @@
 // Structure of one workgroup (4 or 8 waves, one BM x BN output tile):
 //  * k advances in stages of BKB bytes per row.  Global loads go through
 //    buffer resources (hardware bounds checks instead of per-load branches)
-//    into one of two register sets, then into an LDS ring of NBUF buffers.
+//    into a ring of RD register sets, then into an LDS ring of NBUF buffers;
+//    a stage's loads are issued RD - 1 steps before its LDS write, which
+//    covers the latency of reads that miss L2.
 //  * NBUF = 3: a stage is written to LDS two steps before it is consumed, so
 //    the first k-slice's MFMA fragments of the next stage can be read before
 //    the end-of-step barrier and the MFMAs of a step start without waiting on
@@ -42,7 +44,16 @@ struct IC {
   static constexpr int value = V;
 };
 
-template <class E, int BM, int BN, int WM, int WN, int WK, int BMODE, int BKB, int NBUF>
+// Calls f(IC<I>()) for I = B .. E-1.
+template <int B, int E, class F>
+__device__ __forceinline__ void static_for(F &&f) {
+  if constexpr (B < E) {
+    f(IC<B>());
+    static_for<B + 1, E>(f);
+  }
+}
+
+template <class E, int BM, int BN, int WM, int WN, int WK, int BMODE, int BKB, int NBUF, int RD, int FS>
 __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int group_m,
                                                                  SideArgs side, int nside) {
   typedef typename E::T T;
@@ -77,6 +88,8 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile");
   static_assert(BMODE != B_KMAJ_TR || ES == 2, "transposed LDS reads are bf16");
   static_assert(NBUF == 2 || NBUF == 3, "LDS ring depth");
+  static_assert(RD >= 2 && RD <= 4, "register ring depth");
+  static_assert(!FS || NBUF == 2, "staged fragments use two LDS buffers");
 
   __shared__ __align__(16) char smem[LDS];
 
@@ -169,8 +182,8 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
     }
   }
 
-  u32x4 ra[2][A_PER];
-  u32x4 rb[2][RB];
+  u32x4 ra[RD][A_PER];
+  u32x4 rb[RD][RB];
 
   // ---- global -> register set S for stage kt (zeros past the end) ----------
   // Stages kt < nk_main stream x/dy and W; the following ones stream the LoRA
@@ -316,57 +329,144 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
     }
   };
 
-  // ---- main loop, unrolled by two so the register sets are static ----------
-  // Each step is branch-free: loads of stages past the end select out-of-range
-  // offsets (zeros, no memory traffic) and stores of such stages land in an LDS
-  // buffer that is never read again.
-  Frag f0;
-  if constexpr (NBUF == 3) {
-    load_stage(IC<0>(), 0);
-    load_stage(IC<1>(), 1);
-    store_stage(IC<0>(), 0);
-    load_stage(IC<0>(), 2);
-    store_stage(IC<1>(), 1);
+  // ---- main loop -------------------------------------------------------------
+  // Step kt: issue the global loads of stage kt + D into register set
+  // (kt + D) % RD, write register set (kt + E) % RD (loaded RD - 1 steps
+  // earlier, so the loads have RD - 1 steps to land) into LDS buffer
+  // (kt + E) % NBUF, then run the MFMAs of stage kt.  With NBUF = 3, E = 2 and
+  // the first fragments of stage kt + 1 are read before the barrier; with
+  // NBUF = 2, E = 1.  Unrolled by RD so the register sets are static; the LDS
+  // buffer index is a run-time value.  Each step is branch-free: loads of
+  // stages past the end select out-of-range offsets (zeros, no memory traffic)
+  // and stores of such stages land in an LDS buffer that is never read again.
+  if constexpr (FS) {
+    // Staged fragments: every MFMA fragment of a stage is read from LDS one
+    // step ahead into the second of two register sets, so the MFMAs of a
+    // step never wait on LDS and the reads of the next stage overlap them.
+    // A stage's LDS buffer is free once its fragments are in registers, so
+    // two buffers suffice: step kt writes stage kt + 2 over stage kt.
+    constexpr int E_ST = 2;
+    constexpr int D_LD = E_ST + RD - 1;
+    constexpr int UN = RD % 2 == 0 ? RD : 2 * RD;  // unroll: register sets and fragment sets static
+    Frag F[2][SPW];
+    auto read_stage = [&](int buf, Frag(&f)[SPW]) {
+#pragma unroll
+      for (int s2 = 0; s2 < SPW; ++s2) read_frags(buf, s2, f[s2]);
+    };
+    auto mma_stage = [&](const Frag(&f)[SPW]) {
+#pragma unroll
+      for (int s2 = 0; s2 < SPW; ++s2) mma_frags(f[s2]);
+    };
+    static_for<0, RD>([&](auto SI) {
+      constexpr int st = decltype(SI)::value;
+      load_stage(IC<st>(), st);
+    });
+    static_for<0, E_ST>([&](auto SI) {
+      constexpr int st = decltype(SI)::value;
+      store_stage(IC<st % RD>(), st);
+      if constexpr (st + RD < D_LD) load_stage(IC<(st + RD) % RD>(), st + RD);
+    });
     __syncthreads();
-    read_frags(0, 0, f0);
+    read_stage(0, F[0]);
+    __syncthreads();
+    auto step = [&](auto PH, int kt) {
+      constexpr int P = decltype(PH)::value;  // kt % UN
+      const int cb = P % 2;                    // LDS buffer of stage kt (and kt + 2)
+      if constexpr (FS == 2) {
+        // Interleaved: the step's memory instructions are spread between its
+        // MFMAs (which depend only on registers read in the previous step), so
+        // the load, LDS and matrix pipes work side by side instead of in turn.
+        load_stage(IC<(P + D_LD) % RD>(), kt + D_LD);
+        store_stage(IC<(P + E_ST) % RD>(), cb);
+        read_stage(1 - cb, F[(P + 1) % 2]);
+        mma_stage(F[P % 2]);
+        constexpr int NM = SPW * FM * FN;
+        constexpr int NV = A_PER + (BMODE == B_KMAJ_REG ? KB_PER * VEC : B_PER);
+        constexpr int NW = A_PER + (BMODE == B_KMAJ_REG ? KB_PER * VEC : B_PER);
+        constexpr int NR = SPW * (FM + FN * (BMODE == B_KMAJ_TR ? 2 : 1));
+        static_for<0, NM>([&](auto MI) {
+          constexpr int m = decltype(MI)::value;
+          constexpr int v = (m + 1) * NV / NM - m * NV / NM;
+          constexpr int w = (m + 1) * NW / NM - m * NW / NM;
+          constexpr int r = (m + 1) * NR / NM - m * NR / NM;
+          if constexpr (v > 0) __builtin_amdgcn_sched_group_barrier(0x020, v, 0);  // VMEM read
+          if constexpr (w > 0) __builtin_amdgcn_sched_group_barrier(0x200, w, 0);  // DS write
+          if constexpr (r > 0) __builtin_amdgcn_sched_group_barrier(0x100, r, 0);  // DS read
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                       // MFMA
+        });
+      } else {
+        load_stage(IC<(P + D_LD) % RD>(), kt + D_LD);
+        __builtin_amdgcn_sched_barrier(0);
+        store_stage(IC<(P + E_ST) % RD>(), cb);
+        __builtin_amdgcn_sched_barrier(0);
+        read_stage(1 - cb, F[(P + 1) % 2]);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_stage(F[P % 2]);
+      }
+      // Keep the MFMAs ahead of the barrier: the scheduler would otherwise
+      // hoist the barrier (and its wait for every outstanding LDS read) above
+      // them, so they would stall on the reads of the next stage.
+      __builtin_amdgcn_sched_barrier(0);
+      __syncthreads();
+    };
+    // Whole groups of UN steps without branches (a step skipped on some path
+    // would make the compiler wait for every load in flight where the paths
+    // merge), then the remaining steps.
+    int kt = 0;
+    for (; kt + UN <= nk; kt += UN) static_for<0, UN>([&](auto PH) { step(PH, kt + decltype(PH)::value); });
+    static_for<0, UN - 1>([&](auto PH) {
+      constexpr int P = decltype(PH)::value;
+      if (kt + P < nk) step(PH, kt + P);
+    });
+  } else {
+    constexpr int E_ST = NBUF == 3 ? 2 : 1;
+    constexpr int D_LD = E_ST + RD - 1;
+    Frag f0;
+    {
+      // prologue: stages 0 .. D_LD - 1 loaded, 0 .. E_ST - 1 stored
+      static_for<0, RD>([&](auto SI) {
+        constexpr int st = decltype(SI)::value;
+        load_stage(IC<st>(), st);
+      });
+      static_for<0, E_ST>([&](auto SI) {
+        constexpr int st = decltype(SI)::value;
+        store_stage(IC<st % RD>(), st);
+        if constexpr (st + RD < D_LD) load_stage(IC<(st + RD) % RD>(), st + RD);
+      });
+      __syncthreads();
+      if constexpr (NBUF == 3) read_frags(0, 0, f0);
+    }
     int cb = 0;  // LDS buffer of stage kt
-    auto step = [&](auto PAR, int kt) {
-      constexpr int P = decltype(PAR)::value;  // kt % 2
-      const int nb1 = cb == 2 ? 0 : cb + 1, nb2 = nb1 == 2 ? 0 : nb1 + 1;
-      load_stage(IC<1 - P>(), kt + 3);
+    auto step = [&](auto PH, int kt) {
+      constexpr int P = decltype(PH)::value;  // kt % RD
+      const int nb1 = cb + 1 == NBUF ? 0 : cb + 1;
+      const int nbe = NBUF == 3 ? (nb1 + 1 == NBUF ? 0 : nb1 + 1) : nb1;
+      load_stage(IC<(P + D_LD) % RD>(), kt + D_LD);
       // Keep the loads at the top of the step: left alone, the scheduler sinks
       // them to the end of the step, exposing the full memory latency.
       __builtin_amdgcn_sched_barrier(0);
-      store_stage(IC<P>(), nb2);
+      store_stage(IC<(P + E_ST) % RD>(), nbe);
       __builtin_amdgcn_sched_barrier(0);
-      compute(cb, f0);
-      read_frags(nb1, 0, f0);
+      if constexpr (NBUF == 3) {
+        compute(cb, f0);
+        read_frags(nb1, 0, f0);
+      } else {
+        read_frags(cb, 0, f0);
+        compute(cb, f0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
       __syncthreads();
       cb = nb1;
     };
-    for (int kt = 0; kt < nk; kt += 2) {
-      step(IC<0>(), kt);
-      if (kt + 1 < nk) step(IC<1>(), kt + 1);
-    }
-  } else {
-    load_stage(IC<0>(), 0);
-    load_stage(IC<1>(), 1);
-    store_stage(IC<0>(), 0);
-    __syncthreads();
-    auto step = [&](auto PAR, int kt) {
-      constexpr int P = decltype(PAR)::value;  // kt % 2: LDS buffer and register set
-      load_stage(IC<P>(), kt + 2);
-      __builtin_amdgcn_sched_barrier(0);
-      store_stage(IC<1 - P>(), 1 - P);
-      __builtin_amdgcn_sched_barrier(0);
-      read_frags(P, 0, f0);
-      compute(P, f0);
-      __syncthreads();
-    };
-    for (int kt = 0; kt < nk; kt += 2) {
-      step(IC<0>(), kt);
-      if (kt + 1 < nk) step(IC<1>(), kt + 1);
-    }
+    // Whole groups of RD steps without branches (a step skipped on some path
+    // would make the compiler wait for every load in flight where the paths
+    // merge), then the remaining steps.
+    int kt = 0;
+    for (; kt + RD <= nk; kt += RD) static_for<0, RD>([&](auto PH) { step(PH, kt + decltype(PH)::value); });
+    static_for<0, RD - 1>([&](auto PH) {
+      constexpr int P = decltype(PH)::value;
+      if (kt + P < nk) step(PH, kt + P);
+    });
   }
   // ---- cross-wave reduction over the WK k-split (fixed order) ----------------
   // Block b = i*FN + j of the wave tile is owned by wave wk == b % WK.  In phase
@@ -441,7 +541,7 @@ static int pick_group_m(int tiles_m, int tiles_n, int BM, int BN) {
   return gmv;
 }
 
-template <class E, int BM, int BN, int WM, int WN, int WK, int BMODE, int BKB, int NBUF>
+template <class E, int BM, int BN, int WM, int WN, int WK, int BMODE, int BKB, int NBUF, int RD, int FS>
 static hipError_t launch_cfg(const GemmArgs &g, const SideArgs *side, hipStream_t st) {
   const int tm = g.M > 0 ? (g.M + BM - 1) / BM : 0, tn = (g.N + BN - 1) / BN;
   SideArgs sa{};
@@ -452,7 +552,7 @@ static hipError_t launch_cfg(const GemmArgs &g, const SideArgs *side, hipStream_
   }
   const int grid = tm * tn + nside;
   if (grid == 0) return hipSuccess;
-  hipLaunchKernelGGL((gemm_kernel<E, BM, BN, WM, WN, WK, BMODE, BKB, NBUF>), dim3(grid),
+  hipLaunchKernelGGL((gemm_kernel<E, BM, BN, WM, WN, WK, BMODE, BKB, NBUF, RD, FS>), dim3(grid),
                      dim3(64 * WM * WN * WK), 0, st, g, tm > 0 ? pick_group_m(tm, tn, BM, BN) : 1,
                      sa, nside);
   return hipGetLastError();
@@ -467,13 +567,13 @@ int side_workgroups(const SideArgs &s, Dtype dt) {
 
 // Tile shape per problem: an estimate of the time of each candidate -- full
 // waves of tiles over the 256 CUs times the per-tile cost (relative per-CU
-// throughput measured on MI355X: 128x128 0.69, 256x128 0.87, 256x256 1.0).
+// throughput measured on MI355X: 128x128 0.80, 256x128 0.87, 256x256 1.0).
 static int pick_shape(int M, int N) {
   auto cost = [&](int bm, int bn, double eff) {
     const long tiles = (long)((M + bm - 1) / bm) * ((N + bn - 1) / bn);
     return (double)((tiles + 255) / 256) * bm * bn / eff;
   };
-  const double c0 = cost(128, 128, 0.69), c1 = cost(256, 128, 0.87), c2 = cost(256, 256, 1.0);
+  const double c0 = cost(128, 128, 0.80), c1 = cost(256, 128, 0.87), c2 = cost(256, 256, 1.0);
   if (c2 <= c1 && c2 <= c0) return 2;
   return c1 < c0 ? 1 : 0;
 }
@@ -483,18 +583,18 @@ hipError_t launch_gemm(const GemmArgs &g, Dtype dt, bool b_kmajor, const SideArg
   if (dt == DT_BF16) {
     switch (pick_shape(g.M, g.N)) {
       case 2:
-        return b_kmajor ? launch_cfg<BF16, 256, 256, 4, 2, 1, B_KMAJ_TR, 128, 2>(g, side, st)
-                        : launch_cfg<BF16, 256, 256, 4, 2, 1, B_ROW, 128, 2>(g, side, st);
+        return b_kmajor ? launch_cfg<BF16, 256, 256, 4, 2, 1, B_KMAJ_TR, 128, 2, 2, 0>(g, side, st)
+                        : launch_cfg<BF16, 256, 256, 4, 2, 1, B_ROW, 128, 2, 2, 0>(g, side, st);
       case 1:
-        return b_kmajor ? launch_cfg<BF16, 256, 128, 4, 2, 1, B_KMAJ_TR, 128, 2>(g, side, st)
-                        : launch_cfg<BF16, 256, 128, 4, 2, 1, B_ROW, 128, 2>(g, side, st);
+        return b_kmajor ? launch_cfg<BF16, 256, 128, 4, 2, 1, B_KMAJ_TR, 128, 2, 2, 0>(g, side, st)
+                        : launch_cfg<BF16, 256, 128, 4, 2, 1, B_ROW, 128, 2, 2, 0>(g, side, st);
       default:
-        return b_kmajor ? launch_cfg<BF16, 128, 128, 2, 2, 2, B_KMAJ_TR, 128, 3>(g, side, st)
-                        : launch_cfg<BF16, 128, 128, 2, 2, 2, B_ROW, 128, 3>(g, side, st);
+        return b_kmajor ? launch_cfg<BF16, 128, 128, 2, 2, 2, B_KMAJ_TR, 128, 2, 3, 2>(g, side, st)
+                        : launch_cfg<BF16, 128, 128, 2, 2, 2, B_ROW, 128, 2, 3, 2>(g, side, st);
     }
   }
-  return b_kmajor ? launch_cfg<F32, 128, 128, 2, 4, 1, B_KMAJ_REG, 128, 2>(g, side, st)
-                  : launch_cfg<F32, 128, 128, 2, 4, 1, B_ROW, 128, 2>(g, side, st);
+  return b_kmajor ? launch_cfg<F32, 128, 128, 2, 4, 1, B_KMAJ_REG, 128, 2, 2, 0>(g, side, st)
+                  : launch_cfg<F32, 128, 128, 2, 4, 1, B_ROW, 128, 2, 2, 0>(g, side, st);
 }
 
 }  // namespace lora
