@@ -106,45 +106,52 @@ lora_status_t check_shapes(int64_t T, int64_t d_in, int64_t d_out, int64_t r, lo
   return LORA_OK;
 }
 
-// Workspace layouts (offsets in bytes, 256-byte aligned).
+// Workspace layouts (offsets in bytes, 256-byte aligned).  The rank-r row
+// products are computed as `nsplit` partial sums over their reduction axis
+// (row_split); the LoRA-step operands hold one column block per partial.
 struct FwdLayout {
   size_t u, utail, bpad, total;
   int ldt;
+  RowSplit sp;
 };
 FwdLayout fwd_layout(int64_t T, int64_t K, int64_t N, int64_t r, lora_dtype_t dt) {
   FwdLayout L{};
   if (r == 0) return L;
   const Dtype d = dt == LORA_BF16 ? DT_BF16 : DT_F32;
   L.ldt = tail_ld((int)r, d);
+  L.sp = row_split(T, K, (int)r, d);
   size_t off = 0;
-  L.u = off;
-  off += round256((size_t)T * r * 4);
-  L.utail = off;
+  L.u = off;  // partial sums of u = x A^T, [nsplit][T][r] fp32
+  off += round256((size_t)L.sp.nsplit * T * r * 4);
+  L.utail = off;  // [T][ldt]: E(s * partial p) in columns p*r ..
   off += round256((size_t)T * L.ldt * esize(dt));
-  L.bpad = off;
+  L.bpad = off;  // [N][ldt]: B repeated once per partial, zero-padded
   off += round256((size_t)N * L.ldt * esize(dt));
   L.total = off;
   return L;
 }
 
 struct BwdLayout {
-  size_t u, du, dutail, total;
+  size_t u, du, dutail, acat, total;
   int ldt;
+  RowSplit sp_u, sp_du;
 };
 BwdLayout bwd_layout(int64_t T, int64_t K, int64_t N, int64_t r, lora_dtype_t dt) {
-  (void)K;
-  (void)N;
   BwdLayout L{};
   if (r == 0) return L;
   const Dtype d = dt == LORA_BF16 ? DT_BF16 : DT_F32;
   L.ldt = tail_ld((int)r, d);
+  L.sp_u = row_split(T, K, (int)r, d);
+  L.sp_du = row_split(T, N, (int)r, d);
   size_t off = 0;
-  L.u = off;
-  off += round256((size_t)T * r * 4);
-  L.du = off;
-  off += round256((size_t)T * r * 4);
-  L.dutail = off;
+  L.u = off;  // partial sums of u (when it is recomputed)
+  off += round256((size_t)L.sp_u.nsplit * T * r * 4);
+  L.du = off;  // partial sums of du = s dy B
+  off += round256((size_t)L.sp_du.nsplit * T * r * 4);
+  L.dutail = off;  // [T][ldt]: E(partial p of du) in columns p*r ..
   off += round256((size_t)T * L.ldt * esize(dt));
+  L.acat = off;  // [nsplit * r][K]: A repeated once per partial
+  off += L.sp_du.nsplit > 1 ? round256((size_t)L.sp_du.nsplit * r * K * esize(dt)) : 0;
   L.total = off;
   return L;
 }
@@ -216,17 +223,22 @@ lora_status_t lora_linear_fwd(const void *x, const void *W, const void *A, const
   g.C = y; g.ldc = d_out;
   if (r > 0) {
     const FwdLayout L = fwd_layout(T, d_in, d_out, r, dt);
+    const int ns = L.sp.nsplit;
     char *wsb = (char *)ws;
+    float *upart = (float *)(wsb + L.u);
     RowArgs ra{};
     ra.X = x; ra.ldx = d_in; ra.M = (int)T; ra.L = (int)d_in;
     ra.V = A; ra.ldv = d_in; ra.vmode = V_ROW; ra.r = (int)r;
-    ra.out_mult = 1.0f; ra.out = u_save ? u_save : (float *)(wsb + L.u);
+    ra.nsplit = ns; ra.seg = L.sp.seg;
+    ra.out_mult = 1.0f; ra.out = (ns == 1 && u_save) ? u_save : upart; ra.out_stride = T * r;
     ra.tail = wsb + L.utail; ra.ldt = L.ldt; ra.tail_mult = scale;
-    // B itself serves as the LoRA-step operand when its rows are whole 16-byte
-    // vectors; otherwise the kernel writes a zero-padded copy.
-    const bool pad_b = r % (16 / (int64_t)esize(dt)) != 0;
+    // B itself serves as the LoRA-step operand when there is one partial and
+    // its rows are whole 16-byte vectors; otherwise the kernel writes B
+    // repeated once per partial, zero-padded.
+    const bool pad_b = ns > 1 || r % (16 / (int64_t)esize(dt)) != 0;
     if (pad_b) {
-      ra.bcopy_src = B; ra.bcopy_dst = wsb + L.bpad; ra.bcopy_rows = (int)d_out;
+      ra.bcopy_mode = BCOPY_COLS; ra.bcopy_src = B; ra.bcopy_dst = wsb + L.bpad;
+      ra.bcopy_rows = (int)d_out;
     }
     Timed t(K_LORA_DOWN, st);
     hipError_t e = launch_row_skinny(ra, d, st);
@@ -235,7 +247,10 @@ lora_status_t lora_linear_fwd(const void *x, const void *W, const void *A, const
     g.A2 = wsb + L.utail; g.lda2 = L.ldt;
     g.B2 = pad_b ? (const void *)(wsb + L.bpad) : B;
     g.ldb2 = pad_b ? L.ldt : r;
-    g.r = (int)r;
+    g.r = (int)(ns * r);
+    if (ns > 1 && u_save) {
+      g.usum_src = upart; g.usum_out = u_save; g.usum_parts = ns; g.usum_r = (int)r;
+    }
   }
   Timed t(K_GEMM_FWD, st);
   hipError_t e = launch_gemm(g, d, false, nullptr, st);
@@ -294,24 +309,33 @@ lora_status_t lora_linear_bwd(const void *x, const void *W, const void *A, const
   const BwdLayout L = bwd_layout(T, d_in, d_out, r, dt);
   char *wsb = (char *)ws;
   const float *u = u_saved;
+  int u_parts = 1;
   if (!u) {  // rematerialise u = x A^T instead of having stored it
     RowArgs ra{};
     ra.X = x; ra.ldx = d_in; ra.M = (int)T; ra.L = (int)d_in;
     ra.V = A; ra.ldv = d_in; ra.vmode = V_ROW; ra.r = (int)r;
-    ra.out_mult = 1.0f; ra.out = (float *)(wsb + L.u);
+    ra.nsplit = L.sp_u.nsplit; ra.seg = L.sp_u.seg;
+    ra.out_mult = 1.0f; ra.out = (float *)(wsb + L.u); ra.out_stride = T * r;
     Timed t(K_LORA_DOWN, st);
     e = launch_row_skinny(ra, d, st);
     t.done();
     if (e != hipSuccess) return hip_fail(e, "lora_down launch");
     u = (const float *)(wsb + L.u);
+    u_parts = L.sp_u.nsplit;
   }
+  const int ns = L.sp_du.nsplit;
   float *du = (float *)(wsb + L.du);
   {
     RowArgs ra{};
     ra.X = dy; ra.ldx = d_out; ra.M = (int)T; ra.L = (int)d_out;
     ra.V = B; ra.ldv = r; ra.vmode = V_KMAJ_TR; ra.r = (int)r;
-    ra.out_mult = scale; ra.out = du;
+    ra.nsplit = ns; ra.seg = L.sp_du.seg;
+    ra.out_mult = scale; ra.out = du; ra.out_stride = T * r;
     ra.tail = wsb + L.dutail; ra.ldt = L.ldt; ra.tail_mult = scale;
+    if (ns > 1) {  // A repeated once per partial of du
+      ra.bcopy_mode = BCOPY_FLAT; ra.bcopy_src = A; ra.bcopy_dst = wsb + L.acat;
+      ra.bcopy_period = r * d_in; ra.bcopy_elems = ns * r * d_in;
+    }
     Timed t(K_LORA_DY_B, st);
     e = launch_row_skinny(ra, d, st);
     t.done();
@@ -319,11 +343,11 @@ lora_status_t lora_linear_bwd(const void *x, const void *W, const void *A, const
   }
   SideArgs sd{};
   sd.T = (int)T; sd.r = (int)r; sd.njobs = 2;
-  sd.job[0] = ColJob{x, d_in, (int)d_in, du, dA, 1, 1.0f};
-  sd.job[1] = ColJob{dy, d_out, (int)d_out, u, dB, 0, scale};
+  sd.job[0] = ColJob{x, d_in, (int)d_in, du, dA, 1, 1.0f, ns, T * r};
+  sd.job[1] = ColJob{dy, d_out, (int)d_out, u, dB, 0, scale, u_parts, T * r};
   g.A2 = wsb + L.dutail; g.lda2 = L.ldt;
-  g.B2 = A; g.ldb2 = d_in;
-  g.r = (int)r;
+  g.B2 = ns > 1 ? (const void *)(wsb + L.acat) : A; g.ldb2 = d_in;
+  g.r = (int)(ns * r);
   Timed t(K_GEMM_BWD_DX, st);
   e = launch_gemm(g, d, true, &sd, st);
   t.done();

@@ -2,7 +2,8 @@
 // backward GEMM launch (they overlap with the dx tiles):
 //   dA = du^T x   and   dB = s dy^T u,
 // both of the form out[l][j] = scale * sum_t X[t][l] V[t][j] with X a bf16 (or
-// fp32) activation [T, L] and V an fp32 [T, r] matrix.
+// fp32) activation [T, L] and V an fp32 [T, r] matrix, possibly given as
+// partial sums over a split reduction (added in ascending order on load).
 //
 // One work item = (column block of 16*VEC columns, group of 32 rank indices)
 // over all T tokens, so no partial sums leave the workgroup (cross-workgroup
@@ -100,7 +101,16 @@ __device__ void side_item(const SideArgs &s, int item, char *smem) {
 #pragma unroll
       for (int e = 0; e < VEC; ++e) {
         const int t = tb + g * VEC + e;
-        f[e] = (t < t_end && j < r) ? job.V[(int64_t)t * r + j] : 0.0f;
+        float part[MAX_SPLIT];  // all loads issued before the first add
+        const bool ok = t < t_end && j < r;
+        const float *src = job.V + (int64_t)t * r + j;
+#pragma unroll
+        for (int q = 0; q < MAX_SPLIT; ++q) part[q] = (ok && q < job.vparts) ? src[q * job.vstride] : 0.0f;
+        float v = part[0];
+#pragma unroll
+        for (int q = 1; q < MAX_SPLIT; ++q)
+          if (q < job.vparts) v += part[q];
+        f[e] = v;
       }
       vf[jb] = pack_vec(E(), f);
     }

@@ -125,6 +125,33 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   const int nt = (t % gsize) / gm;
   const int m0 = mt * BM, n0 = nt * BN;
 
+  // Optional sum of partial rank-r products for the rows of this tile row:
+  // its BM x r elements are shared out over the tile row's workgroups, one
+  // per thread; the loads are issued here and the sum stored after the main
+  // loop, so their latency is hidden.
+  // (Tiles larger than 128 x 128 have no registers to spare across the loop:
+  // they issue the loads after it.)
+  constexpr bool US_EARLY = BM * BN <= 128 * 128;
+  float us_part[MAX_SPLIT];
+  int64_t us_idx = -1;
+  int us_first = 0, us_last = 0;
+  auto us_load = [&]() {
+    const int64_t plane = (int64_t)g.M * g.usum_r;
+#pragma unroll
+    for (int q = 0; q < MAX_SPLIT; ++q) us_part[q] = q < g.usum_parts ? g.usum_src[q * plane + us_idx] : 0.0f;
+  };
+  // Only the forward GEMM (row-major B) carries this job.
+  if (BMODE == B_ROW && g.usum_out) {
+    const int total = min(BM, g.M - m0) * g.usum_r;
+    const int chunk = (total + tiles_n - 1) / tiles_n;
+    us_first = nt * chunk + tid;
+    us_last = min(total, (nt + 1) * chunk);
+    if (us_first < us_last) {
+      us_idx = (int64_t)(m0 + us_first / g.usum_r) * g.usum_r + us_first % g.usum_r;
+      if constexpr (US_EARLY) us_load();
+    }
+  }
+
   const int nk_main = (g.K + BKE - 1) / BKE;
   const int nk = nk_main + (g.r > 0 ? (g.r + BKE - 1) / BKE : 0);  // + LoRA steps
 
@@ -500,6 +527,25 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
         }
       }
       __syncthreads();
+    }
+  }
+
+  // ---- sum of partial rank-r products: store (loads issued before the loop) --
+  if (BMODE == B_ROW && g.usum_out) {
+    if (us_idx >= 0) {
+      if constexpr (!US_EARLY) us_load();
+      float v = us_part[0];
+#pragma unroll
+      for (int q = 1; q < MAX_SPLIT; ++q)
+        if (q < g.usum_parts) v += us_part[q];
+      g.usum_out[us_idx] = v;
+    }
+    // elements beyond one per thread (large r with few tile columns)
+    for (int e = us_first + NT; e < us_last; e += NT) {
+      const int64_t o = (int64_t)(m0 + e / g.usum_r) * g.usum_r + e % g.usum_r;
+      float v = g.usum_src[o];
+      for (int q = 1; q < g.usum_parts; ++q) v += g.usum_src[q * (int64_t)g.M * g.usum_r + o];
+      g.usum_out[o] = v;
     }
   }
 

@@ -2,20 +2,27 @@
 // activation [T, L] against a small [r, L] factor, reduced over the long axis L.
 //   forward   u  = x A^T                    (A row-major [r, d_in])
 //   backward  du = s dy B                   (B k-major   [d_out, r])
-// Each workgroup owns 16 rows; its eight waves take interleaved 128-byte
-// chunks of those rows (up to four chunks in flight per wave, enough loads
-// outstanding to stream at HBM speed with only T/16 workgroups), accumulate
-// 16 x r tiles on 16x16 matrix cores, and the eight partial tiles are summed
-// in LDS in a fixed order.  At r >= 16 vector FMAs would not keep up with HBM.
+// Each workgroup owns 16 rows and one segment of the reduction axis (the axis
+// is split so that the T/16 row blocks times the segments give about one
+// workgroup per CU); its eight waves take interleaved 128-byte chunks of the
+// segment (up to four chunks in flight per wave), accumulate 16 x r tiles on
+// 16x16 matrix cores, and the eight partial tiles are summed in LDS in a fixed
+// order.  Each segment's sum is written separately: the GEMM that consumes the
+// LoRA-step operand adds the segments as extra reduction columns, and the
+// other consumers add them in ascending order when they load them.  At
+// r >= 16 vector FMAs would not keep up with HBM.
 //
 // k-major B: each wave copies the B rows of its chunk into a private LDS
 // region and reads them back with ds_read_b64_tr_b16, which returns four
 // consecutive k of one column per lane -- exactly the matrix-core operand --
 // instead of gathering 2-byte elements from global memory.
 //
-// Besides the fp32 result the kernel writes the operand of the big GEMM's
-// LoRA step: tail = E(tail_mult * sum), zero-padded to `ldt` columns, and
-// (forward) a zero-padded copy of B.
+// Besides the fp32 partial sums the kernel writes the operand of the big
+// GEMM's LoRA step: tail[m][p*r + j] = E(tail_mult * sum_p), zero-padded to
+// `ldt` columns, and a copy of the other LoRA factor repeated once per
+// segment (B column-wise in the forward pass, A row-wise in the backward).
+#include <algorithm>
+
 #include "kernels.hpp"
 #include "launch.hpp"
 
@@ -41,21 +48,30 @@ __global__ __launch_bounds__(64 * ROW_NW) void row_skinny_kernel(RowArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int m0 = blockIdx.x * 16;
+  const int p = blockIdx.y;  // segment of the reduction axis
   const int row = m0 + (lane & 15);
   const int g = lane >> 4;
-  const int M = a.M, L = a.L, r = a.r;
+  const int M = a.M, r = a.r;
+  const int k_lo = p * a.seg, k_hi = min(a.L, k_lo + a.seg);
   const T *Xp = (const T *)a.X;
   const T *Vp = (const T *)a.V;
 
-  // Optional side job: copy B zero-padded (the forward LoRA-step operand).
-  if (a.bcopy_src) {
+  // Optional copy job (LoRA-step operands repeated once per segment).
+  if (a.bcopy_mode != BCOPY_NONE) {
     const T *src = (const T *)a.bcopy_src;
     T *dst = (T *)a.bcopy_dst;
-    const int64_t total = (int64_t)a.bcopy_rows * a.ldt;
-    for (int64_t i = (int64_t)blockIdx.x * NT + tid; i < total; i += (int64_t)gridDim.x * NT) {
-      const int64_t n = i / a.ldt;
-      const int j = (int)(i % a.ldt);
-      dst[i] = j < r ? src[n * r + j] : (T)0;
+    const int64_t wg = (int64_t)blockIdx.y * gridDim.x + blockIdx.x;
+    const int64_t stride = (int64_t)gridDim.x * gridDim.y * NT;
+    if (a.bcopy_mode == BCOPY_COLS) {
+      const int rep = a.nsplit * r;
+      const int64_t total = (int64_t)a.bcopy_rows * a.ldt;
+      for (int64_t i = wg * NT + tid; i < total; i += stride) {
+        const int64_t n = i / a.ldt;
+        const int c = (int)(i % a.ldt);
+        dst[i] = c < rep ? src[n * r + c % r] : (T)0;
+      }
+    } else {
+      for (int64_t i = wg * NT + tid; i < a.bcopy_elems; i += stride) dst[i] = src[i % a.bcopy_period];
     }
   }
 
@@ -64,7 +80,7 @@ __global__ __launch_bounds__(64 * ROW_NW) void row_skinny_kernel(RowArgs a) {
   for (int jb = 0; jb < JB; ++jb) acc[jb] = f32x4{0.f, 0.f, 0.f, 0.f};
   char *region = smem + wave * REGION;
 
-  for (int kc0 = wave * CE; kc0 < L; kc0 += NW * CE * U) {
+  for (int kc0 = k_lo + wave * CE; kc0 < k_hi; kc0 += NW * CE * U) {
     u32x4 xf[U][2];
     u32x4 vf[U][2][JB];
     // issue every global load of the U chunks first
@@ -74,12 +90,12 @@ __global__ __launch_bounds__(64 * ROW_NW) void row_skinny_kernel(RowArgs a) {
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const int k = kc + h * 4 * VEC + g * VEC;
-        xf[u][h] = (row < M && k < L) ? ld16(Xp + (int64_t)row * a.ldx + k) : zero16();
+        xf[u][h] = (row < M && k < k_hi) ? ld16(Xp + (int64_t)row * a.ldx + k) : zero16();
         if constexpr (VMODE == V_ROW) {
 #pragma unroll
           for (int jb = 0; jb < JB; ++jb) {
             const int j = jb * 16 + (lane & 15);
-            vf[u][h][jb] = (j < r && k < L) ? ld16(Vp + (int64_t)j * a.ldv + k) : zero16();
+            vf[u][h][jb] = (j < r && k < k_hi) ? ld16(Vp + (int64_t)j * a.ldv + k) : zero16();
           }
         } else if constexpr (VMODE == V_KMAJ_GATHER) {
 #pragma unroll
@@ -88,7 +104,7 @@ __global__ __launch_bounds__(64 * ROW_NW) void row_skinny_kernel(RowArgs a) {
             float f[VEC];
 #pragma unroll
             for (int e = 0; e < VEC; ++e)
-              f[e] = (j < r && k + e < L) ? E::to_float(Vp[(int64_t)(k + e) * a.ldv + j]) : 0.0f;
+              f[e] = (j < r && k + e < k_hi) ? E::to_float(Vp[(int64_t)(k + e) * a.ldv + j]) : 0.0f;
             vf[u][h][jb] = pack_vec(E(), f);
           }
         }
@@ -104,7 +120,7 @@ __global__ __launch_bounds__(64 * ROW_NW) void row_skinny_kernel(RowArgs a) {
         for (int c = lane; c < CE * cpr; c += 64) {
           const int br = c / cpr, bc = c % cpr;
           const int n = kc + br;
-          const u32x4 v = n < L ? ld16(Vp + (int64_t)n * r + bc * 8) : zero16();
+          const u32x4 v = n < k_hi ? ld16(Vp + (int64_t)n * r + bc * 8) : zero16();
           st16(region + (u * CE + br) * RSB + bc * 16, v);
         }
       }
@@ -142,25 +158,30 @@ __global__ __launch_bounds__(64 * ROW_NW) void row_skinny_kernel(RowArgs a) {
     for (int i = 0; i < 4; ++i)
       red[(wave * 16 + g * 4 + i) * (R16 + 1) + jb * 16 + (lane & 15)] = acc[jb][i];
   __syncthreads();
+  // Segment p owns columns p*r .. p*r + r-1 of the tail; the last segment
+  // also writes its zero padding.
   T *tail = (T *)a.tail;
-  const int ncol = a.tail ? a.ldt : r;
+  float *out = a.out + (int64_t)p * a.out_stride;
+  const int pad_lo = a.nsplit * r;
+  const int ncol = (tail && p == a.nsplit - 1) ? r + (a.ldt - pad_lo) : r;
   for (int idx = tid; idx < 16 * ncol; idx += NT) {
-    const int mm = idx / ncol, j = idx % ncol;
+    const int mm = idx / ncol, c = idx % ncol;
     if (m0 + mm >= M) continue;
-    float s = 0.0f;
-    if (j < r) {
-      s = red[(0 * 16 + mm) * (R16 + 1) + j];
+    if (c < r) {
+      float s = red[(0 * 16 + mm) * (R16 + 1) + c];
 #pragma unroll
-      for (int w = 1; w < NW; ++w) s += red[(w * 16 + mm) * (R16 + 1) + j];
-      a.out[(int64_t)(m0 + mm) * r + j] = a.out_mult * s;
+      for (int w = 1; w < NW; ++w) s += red[(w * 16 + mm) * (R16 + 1) + c];
+      out[(int64_t)(m0 + mm) * r + c] = a.out_mult * s;
+      if (tail) tail[(int64_t)(m0 + mm) * a.ldt + p * r + c] = E::from_float(a.tail_mult * s);
+    } else {
+      tail[(int64_t)(m0 + mm) * a.ldt + pad_lo + (c - r)] = (T)0;
     }
-    if (tail) tail[(int64_t)(m0 + mm) * a.ldt + j] = E::from_float(a.tail_mult * s);
   }
 }
 
 template <class E, int VMODE>
 static hipError_t row_dispatch(const RowArgs &a, hipStream_t st) {
-  dim3 grid((a.M + 15) / 16), block(64 * ROW_NW);
+  dim3 grid((a.M + 15) / 16, a.nsplit), block(64 * ROW_NW);
   const int jb = (a.r + 15) / 16;
 #define ROWSK(J)                                                                                  \
   case J:                                                                                         \
@@ -176,7 +197,9 @@ static hipError_t row_dispatch(const RowArgs &a, hipStream_t st) {
 }
 
 hipError_t launch_row_skinny(const RowArgs &a, Dtype dt, hipStream_t st) {
-  if (a.r < 1 || a.r > 128) return hipErrorInvalidValue;
+  if (a.r < 1 || a.r > 128 || a.nsplit < 1 || a.nsplit > MAX_SPLIT || a.seg < 1) return hipErrorInvalidValue;
+  if ((int64_t)(a.nsplit - 1) * a.seg >= a.L || (int64_t)a.nsplit * a.seg < a.L) return hipErrorInvalidValue;
+  if (a.tail && a.nsplit * a.r > a.ldt) return hipErrorInvalidValue;
   if (dt == DT_BF16) {
     if (a.vmode == V_ROW) return row_dispatch<BF16, V_ROW>(a, st);
     if (a.r % 8 == 0) return row_dispatch<BF16, V_KMAJ_TR>(a, st);
@@ -184,6 +207,18 @@ hipError_t launch_row_skinny(const RowArgs &a, Dtype dt, hipStream_t st) {
   }
   if (a.vmode == V_ROW) return row_dispatch<F32, V_ROW>(a, st);
   return row_dispatch<F32, V_KMAJ_GATHER>(a, st);
+}
+
+RowSplit row_split(int64_t T, int64_t L, int r, Dtype dt) {
+  const int64_t blocks = (T + 15) / 16;
+  const int ce = dt == DT_BF16 ? 64 : 32;  // elements per 128-byte chunk
+  int64_t s = (256 + blocks - 1) / blocks;
+  s = std::min<int64_t>(s, std::max(1, tail_ld(r, dt) / r));
+  s = std::min<int64_t>(s, MAX_SPLIT);
+  s = std::min<int64_t>(s, (L + (int64_t)ROW_NW * ce - 1) / ((int64_t)ROW_NW * ce));
+  s = std::max<int64_t>(s, 1);
+  const int64_t seg = ((L + s - 1) / s + ce - 1) / ce * ce;
+  return RowSplit{(int)((L + seg - 1) / seg), (int)seg};
 }
 
 }  // namespace lora

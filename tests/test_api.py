@@ -53,17 +53,23 @@ BAD = ctypes.c_size_t(-1).value
 def test_workspace_query():
     assert ws(L.LORA_OP_FROZEN_DX, 4096, 3072, 128256, 0) == 0
     assert ws(L.LORA_OP_FWD, 128, 256, 256, 0) == 0
-    # forward: u, the bf16 LoRA-step operand (padded to 64) and a padded copy of B
-    assert 128 * 8 * 4 <= ws(L.LORA_OP_FWD, 128, 256, 256, 8) <= 128 * 8 * 4 + (128 + 256) * 64 * 2 + 512
+    # forward: partial sums of u (at most ldt / r of them over the split
+    # reduction axis), the bf16 LoRA-step operand (ldt = 64 columns) and B
+    # repeated once per partial; backward: partial sums of u and du, the
+    # LoRA-step operand and A repeated once per partial -- all far below the
+    # fp32 dW the method never forms.
     assert ws(L.LORA_OP_BWD, 128, 256, 256, 0) == 0
-    # backward: u + du + LoRA-step operand + bounded partial sums; below a fp32 dW
-    for T, K, N, r in [(1024, 3072, 3072, 16), (2048, 3072, 8192, 16), (4096, 8192, 3072, 32),
-                       (2048, 2048, 256, 8)]:
+    for T, K, N, r in [(128, 256, 256, 8), (1024, 3072, 3072, 16), (2048, 3072, 8192, 16),
+                       (4096, 8192, 3072, 32), (2048, 2048, 256, 8), (16, 4096, 4096, 128)]:
+        ldt = (r + 63) // 64 * 64
+        S = ldt // r
+        f = ws(L.LORA_OP_FWD, T, K, N, r)
+        assert T * r * 4 <= f <= S * T * r * 4 + (T + N) * ldt * 2 + 3 * 256, (T, K, N, r, f)
         b = ws(L.LORA_OP_BWD, T, K, N, r)
-        assert 8 * T * r <= b < N * K * 4, (T, K, N, r, b)
-    # grows with T and r
-    assert ws(L.LORA_OP_BWD, 2048, 3072, 3072, 16) >= ws(L.LORA_OP_BWD, 1024, 3072, 3072, 16)
-    assert ws(L.LORA_OP_BWD, 1024, 3072, 3072, 32) >= ws(L.LORA_OP_BWD, 1024, 3072, 3072, 16)
+        assert 8 * T * r <= b <= 2 * S * T * r * 4 + T * ldt * 2 + S * r * K * 2 + 4 * 256, (T, K, N, r, b)
+        assert b < N * K * 4, (T, K, N, r, b)
+    # fp32 check mode pads the LoRA step to 32 columns
+    assert 64 * 16 * 4 <= ws(L.LORA_OP_FWD, 64, 256, 256, 16, dt=L.LORA_F32) <= 2 * 64 * 16 * 4 + (64 + 256) * 32 * 4 + 768
     # rejected shapes
     assert ws(L.LORA_OP_BWD, 0, 256, 256, 8) == BAD
     assert ws(L.LORA_OP_BWD, 16, 250, 256, 8) == BAD

@@ -54,6 +54,38 @@ def test_multi_tile_ragged(orc, shape):
     _case(orc, T, K, N, r, 2.0 * r, seed=7)
 
 
+# Shapes where the rank-r row products are split over their reduction axis
+# into several partial sums (ragged last segment, up to 8 segments, odd rank,
+# u rematerialised in the backward pass).
+@pytest.mark.parametrize("shape,recompute,dtype", [
+    ((256, 1800, 1032, 16), False, torch.bfloat16),
+    ((256, 1800, 1032, 16), True, torch.bfloat16),
+    ((96, 2048, 4104, 8), True, torch.bfloat16),
+    ((40, 1024, 2048, 3), False, torch.bfloat16),
+    ((40, 1024, 2048, 3), True, torch.bfloat16),
+    ((256, 1800, 1032, 16), True, torch.float32),
+])
+def test_split_reduction(orc, shape, recompute, dtype):
+    T, K, N, r = shape
+    _case(orc, T, K, N, r, 2.0 * r, seed=41, dtype=dtype, recompute=recompute)
+
+
+def test_split_forward_without_u_save(orc):
+    # the partial sums of u stay in the workspace; y must not depend on u_save
+    T, K, N, r = 256, 1800, 1032, 16
+    _announce(f"fwd without u_save T={T} K={K} N={N} r={r}")
+    inp = {k: v.cuda() for k, v in lora_inputs(T, K, N, r, seed=43).items()}
+    y0 = torch.empty(T, N, dtype=torch.bfloat16, device="cuda")
+    y1 = torch.empty_like(y0)
+    u = torch.empty(T, r, dtype=torch.float32, device="cuda")
+    lm.lora_linear_fwd(inp["x"], inp["W"], inp["A"], inp["B"], y0, u, 2.0)
+    lm.lora_linear_fwd(inp["x"], inp["W"], inp["A"], inp["B"], y1, None, 2.0)
+    torch.cuda.synchronize()
+    assert torch.equal(y0, y1)
+    ref = orc.u(inp["x"].cpu(), inp["A"].cpu())
+    assert relerr(u.cpu().double().numpy(), ref) <= TOL[torch.bfloat16]
+
+
 def test_recompute_u_matches(orc):
     T, K, N, r = 200, 264, 136, 16
     inp = lora_inputs(T, K, N, r, seed=5)
