@@ -41,8 +41,8 @@
  *                      aligned, a size < 1, r outside [0,128], a non-finite
  *                      scale, or an output overlapping an input or another
  *                      output;
- *   LORA_EUNSUPPORTED  d_in or d_out not a multiple of 8, or a matrix with
- *                      2^31 or more elements;
+ *   LORA_EUNSUPPORTED  d_in or d_out not a multiple of 8 or above 2^20, or a
+ *                      matrix with 2^31 or more elements;
  *   LORA_EWORKSPACE    ws_bytes below the required size (or ws NULL when
  *                      the required size is non-zero);
  *   LORA_EHIP          a kernel launch failed (asynchronous device faults
@@ -50,8 +50,9 @@
  * lora_last_error() returns a short text for the calling thread's last error.
  * No entry point prints, aborts or throws.
  *
- * Determinism: no atomics on any path; reductions over tokens use fixed-order
- * partial sums, so identical inputs give bitwise identical outputs.
+ * Determinism: no atomics on any path; every reduction (over tokens, over the
+ * split feature axis of the rank-r products, across waves) adds its parts in
+ * a fixed order, so identical inputs give bitwise identical outputs.
  */
 #ifndef LORA_MI355X_H
 #define LORA_MI355X_H
