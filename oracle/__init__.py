@@ -12,6 +12,7 @@ per-definition functions into the forward and backward passes:
     forward:   U = X A^T ;  Y = X W^T + s U B^T
     backward:  G = dY B ; dU = s G ; dX = dY W + dU A ; dA = dU^T X ;
                dB = s dY^T U
+    quantized base:  W = S * W_q + Bo per group (dequant), then as above
 
 (LoRA as described in the paper's background on parameter-efficient
 fine-tuning, with r and alpha from its hyperparameter table; frozen-base
@@ -56,8 +57,10 @@ def _declare(lib: ctypes.CDLL) -> ctypes.CDLL:
                                         _lp, _i64, _dp]
     lib.oracle_lora_da.argtypes = [_dp, _dp, _i64, _i64, _i64, _dp]
     lib.oracle_lora_db.argtypes = [_dp, _dp, _i64, _i64, _i64, ctypes.c_double, _dp]
+    lib.oracle_dequant.argtypes = [ctypes.POINTER(ctypes.c_uint8), _dp, _dp, _i64, _i64,
+                                   ctypes.c_int, _i64, _dp]
     for name in ("oracle_lora_u", "oracle_lora_y_rows", "oracle_lora_grad_u",
-                 "oracle_lora_dx_rows", "oracle_lora_da", "oracle_lora_db"):
+                 "oracle_lora_dx_rows", "oracle_lora_da", "oracle_lora_db", "oracle_dequant"):
         getattr(lib, name).restype = None
     lib.oracle_threads.argtypes = []
     lib.oracle_threads.restype = ctypes.c_int
@@ -180,6 +183,21 @@ class Oracle:
         if want_dx:
             out["dX"] = self.dx(dY, W, dU, A, rows=dx_rows)
         return out
+
+    def dequant(self, Wq, S, Bo, bits, G):
+        """W = S * q + Bo per group of G inputs (fp64 [N, K]) from the codes in
+        Wq ([N, K*bits/8] uint8) and the per-group scales S / offsets Bo."""
+        if hasattr(Wq, "detach"):
+            Wq = Wq.detach().to("cpu").numpy()
+        Wq = np.ascontiguousarray(Wq, dtype=np.uint8)
+        S, Bo = _f64(S), _f64(Bo)
+        N = Wq.shape[0]
+        K = Wq.shape[1] * 8 // bits
+        assert bits in (4, 8) and K % G == 0 and S.shape == (N, K // G) == Bo.shape
+        W = np.empty((N, K), dtype=np.float64)
+        self.lib.oracle_dequant(Wq.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8)), _ptr(S),
+                                _ptr(Bo), N, K, bits, G, _ptr(W))
+        return W
 
     def frozen_dx(self, dY, W, rows=None):
         """Rank-0 frozen linear input gradient dX = dY W."""

@@ -31,6 +31,9 @@
  * order of any single sum.
  *
  * Each function is one line of the definition above, written out.
+ *
+ * For a quantized frozen base the weight W is first reconstructed in fp64 by
+ * oracle_dequant (below) and then used exactly as above.
  */
 #include <stddef.h>
 #include <stdint.h>
@@ -139,6 +142,33 @@ void oracle_lora_db(const double *dY, const double *U, int64_t T, int64_t N,
       double acc = 0.0;
       for (int64_t t = 0; t < T; ++t) acc += dY[t * N + n] * U[t * r + j];
       dB[n * r + j] = s * acc;
+    }
+  }
+}
+
+/* W[n][k] = S[n][g] * q(n, k) + Bo[n][g],  g = k / G
+ * (the dequantization step of the algorithm "On-the-fly Dequantization",
+ * W = s * W_q + b, with one scale s and offset b per group of G consecutive
+ * inputs of an output row).  The codes q are unsigned integers read from Wq
+ * [N, K * bits / 8] bytes: bits = 8 stores one code per byte; bits = 4 two per
+ * byte, the code of even k in the low nibble and of odd k in the high one.
+ * S and Bo are [N, K / G]. */
+void oracle_dequant(const uint8_t *Wq, const double *S, const double *Bo,
+                    int64_t N, int64_t K, int bits, int64_t G, double *W) {
+  const int64_t row_bytes = K * bits / 8;
+  const int64_t ngroups = K / G;
+#pragma omp parallel for schedule(static)
+  for (int64_t n = 0; n < N; ++n) {
+    for (int64_t k = 0; k < K; ++k) {
+      int q;
+      if (bits == 8) {
+        q = Wq[n * row_bytes + k];
+      } else {
+        const uint8_t byte = Wq[n * row_bytes + k / 2];
+        q = (k % 2 == 0) ? (byte & 0x0F) : (byte >> 4);
+      }
+      const int64_t g = k / G;
+      W[n * K + k] = S[n * ngroups + g] * (double)q + Bo[n * ngroups + g];
     }
   }
 }

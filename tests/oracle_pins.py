@@ -12,6 +12,8 @@ and input gradient with no weight gradient, from its "On-the-fly
 Dequantization" algorithm; tokens as rows):
     Y = X W^T + s (X A^T) B^T,  dX = dY W + s (dY B) A,
     dA = s (dY B)^T X,          dB = s dY^T (X A^T).
+A quantized frozen base is dequantized first, as in that algorithm:
+    W = s W_q + b, one scale s and offset b per group of G inputs of a row.
 """
 from __future__ import annotations
 
@@ -245,12 +247,59 @@ def pin_torch_autograd(o):
     assert _relmax(bw["dB"], t["B"].grad.numpy()) <= TIGHT
 
 
+# --- dequantization of a quantized frozen base (W = s W_q + b per group) --------
+def pin_dequant_worked_example(o):
+    """Codes and parameters worked by hand.  4-bit, one row, K = 32, G = 16:
+    byte 0 = 0x5A holds k=0 -> 0xA = 10 (low nibble) and k=1 -> 5; byte 1 = 0x01
+    holds k=2 -> 1 and k=3 -> 0; byte 8 = 0xF3 (first byte of group 1) holds
+    k=16 -> 3 and k=17 -> 15.  Group 0 has s=0.5, b=-1; group 1 s=2, b=3."""
+    Wq = np.zeros((1, 16), np.uint8)
+    Wq[0, 0], Wq[0, 1], Wq[0, 8] = 0x5A, 0x01, 0xF3
+    W = o.dequant(Wq, np.array([[0.5, 2.0]]), np.array([[-1.0, 3.0]]), 4, 16)
+    assert W.shape == (1, 32)
+    assert list(W[0, :4]) == [4.0, 1.5, -0.5, -1.0]
+    assert W[0, 15] == -1.0                      # code 0 in group 0: the offset
+    assert list(W[0, 16:19]) == [9.0, 33.0, 3.0]
+    # 8-bit: one code per byte, K = 4, G = 2
+    W8 = o.dequant(np.array([[200, 7, 255, 0]], np.uint8), np.array([[0.25, -1.0]]),
+                   np.array([[1.0, 0.5]]), 8, 2)
+    assert list(W8[0]) == [51.0, 2.75, -254.5, 0.5]
+
+
+def pin_dequant_unit_scale_is_the_codes(o):
+    """With s = 1 and b = 0 the weight is the integer codes themselves, read out
+    of the bytes with numpy's own bit operations (low nibble = even k)."""
+    g = _rng(40)
+    Wq = g.integers(0, 256, size=(5, 48), dtype=np.uint8)
+    W8 = o.dequant(Wq, np.ones((5, 3)), np.zeros((5, 3)), 8, 16)
+    assert np.array_equal(W8, Wq.astype(np.float64))
+    W4 = o.dequant(Wq, np.ones((5, 6)), np.zeros((5, 6)), 4, 16)
+    assert np.array_equal(W4[:, 0::2], (Wq & 0x0F).astype(np.float64))
+    assert np.array_equal(W4[:, 1::2], (Wq >> 4).astype(np.float64))
+
+
+def pin_dequant_groups(o):
+    """Groups are G consecutive inputs of one row: with every code 1 and b = 0
+    the weight is each group's scale repeated G times (numpy repeat); with
+    s = 0 it is each group's offset repeated."""
+    g = _rng(41)
+    N, K, G = 4, 96, 32
+    S, Bo = g.standard_normal((N, K // G)), g.standard_normal((N, K // G))
+    ones4 = np.full((N, K // 2), 0x11, np.uint8)
+    assert np.array_equal(o.dequant(ones4, S, np.zeros_like(Bo), 4, G), np.repeat(S, G, axis=1))
+    codes = g.integers(0, 256, size=(N, K // 2), dtype=np.uint8)
+    assert np.array_equal(o.dequant(codes, np.zeros_like(S), Bo, 4, G), np.repeat(Bo, G, axis=1))
+    ones8 = np.ones((N, K), np.uint8)
+    assert np.array_equal(o.dequant(ones8, S, np.zeros_like(Bo), 8, G), np.repeat(S, G, axis=1))
+
+
 ALL_PINS = [
     pin_scalar_closed_form, pin_small_closed_form, pin_rank0_textbook_gemm,
     pin_down_projection_gemm, pin_finite_differences, pin_dense_identities,
     pin_zero_B, pin_zero_A, pin_zero_W, pin_linear_in_scale,
     pin_token_split_additivity, pin_row_permutation, pin_row_sampling,
-    pin_torch_autograd,
+    pin_torch_autograd, pin_dequant_worked_example, pin_dequant_unit_scale_is_the_codes,
+    pin_dequant_groups,
 ]
 
 

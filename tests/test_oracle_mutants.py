@@ -37,6 +37,16 @@ MUTANTS = [
      "for (int64_t t = 0; t < 1; ++t) acc += dU[t * r + j] * X[t * K + k];"),
     ("db_unscaled", "dB[n * r + j] = s * acc;", "dB[n * r + j] = acc;"),
     ("db_transposed_U", "acc += dY[t * N + n] * U[t * r + j];", "acc += dY[t * N + n] * U[j * T + t];"),
+    ("dq_nibbles_swapped", "q = (k % 2 == 0) ? (byte & 0x0F) : (byte >> 4);",
+     "q = (k % 2 == 0) ? (byte >> 4) : (byte & 0x0F);"),
+    ("dq_wrong_group", "const int64_t g = k / G;", "const int64_t g = k / (2 * G);"),
+    ("dq_scale_offset_swapped", "W[n * K + k] = S[n * ngroups + g] * (double)q + Bo[n * ngroups + g];",
+     "W[n * K + k] = Bo[n * ngroups + g] * (double)q + S[n * ngroups + g];"),
+    ("dq_dropped_offset", "W[n * K + k] = S[n * ngroups + g] * (double)q + Bo[n * ngroups + g];",
+     "W[n * K + k] = S[n * ngroups + g] * (double)q;"),
+    ("dq_8bit_as_nibble", "q = Wq[n * row_bytes + k];", "q = Wq[n * row_bytes + k] & 0x0F;"),
+    ("dq_wrong_byte", "const uint8_t byte = Wq[n * row_bytes + k / 2];",
+     "const uint8_t byte = Wq[n * row_bytes + k / 2 + (k / 2 + 1 < row_bytes)];"),
 ]
 
 CHILD = textwrap.dedent("""
