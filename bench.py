@@ -25,7 +25,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 import paper_2606_19528_amd as lm  # noqa: E402
-from workloads import WORKLOADS, frozen_inputs, linear_seed, lora_inputs  # noqa: E402
+from workloads import WORKLOADS, frozen_inputs, linear_seed, lora_inputs, quant_weight  # noqa: E402
 
 METRIC = "LoRA linear fwd+bwd TFLOP/s (% bf16 MFMA peak) + peak device workspace bytes"
 PEAK_BF16_TFLOPS = 2516.6   # 256 CU x 4096 dense bf16 flop/clk x 2.4 GHz
@@ -118,6 +118,56 @@ def step(layers, head, ws):
         lm.lora_linear_bwd(L.x, L.W, L.A, L.B, L.u, L.dy, L.dx, L.dA, L.dB, L.lin.scale, ws=ws)
 
 
+def build_quant(layers, head, workload, dev):
+    """INT4 codes (groups of 128 inputs) for every LoRA linear's frozen W and
+    INT8 codes for the frozen head, the paper's mixed-precision setting."""
+    qs = [quant_weight(L.lin.d_out, L.lin.d_in, 4, 128, seed=1000 + i, device=dev)
+          for i, L in enumerate(layers)]
+    qh = None
+    if head is not None:
+        h = workload.head
+        qh = quant_weight(h.d_out, h.d_in, 8, 128, seed=20_000, device=dev)
+    return qs, qh
+
+
+def step_quant(layers, head, ws, qs, qh):
+    for L, q in zip(layers, qs):
+        lm.lora_linear_fwd_q(L.x, q, L.A, L.B, L.y, L.u, L.lin.scale, ws=ws)
+    if head is not None:
+        lm.frozen_linear_bwd_dx_q(head[0], qh, head[2])
+    for L, q in zip(reversed(layers), reversed(qs)):
+        lm.lora_linear_bwd_q(L.x, q, L.A, L.B, L.u, L.dy, L.dx, L.dA, L.dB, L.lin.scale, ws=ws)
+
+
+def time_steps(fn, steps, warmup):
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
+def per_kernel_ms(fn, steps):
+    lm.profiler_reset()
+    lm.profiler_enable(True)
+    for _ in range(steps):
+        fn()
+    torch.cuda.synchronize()
+    lm.profiler_enable(False)
+    out = {}
+    for name in lm.kernel_names():
+        tot, n = lm.profiler_read(name)
+        if n:
+            out[name] = (tot, n)
+    lm.profiler_reset()
+    return out
+
+
 def kernel_flops(workload):
     """Algorithmic flops of one launch of each GEMM kernel, per linear shape."""
     T = workload.tokens
@@ -179,6 +229,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="llama_q_proj", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-quant", action="store_true",
+                    help="skip the secondary measurement with the quantized frozen base")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after the steps, copy a buffer of this many MiB (device to device) so a "
                          "counter run can calibrate FETCH_SIZE / WRITE_SIZE against known bytes")
@@ -261,6 +313,23 @@ def main():
         "roofline": roofline,
         "kernels_ms_per_step": {k: round(v[0] / args.steps, 5) for k, v in per_kernel.items()},
     }
+    if not args.no_quant:
+        # Quantized frozen base (INT4 linears, INT8 head) dequantized inside the
+        # GEMMs: same workload, same flop count, weights read as codes.
+        qs, qh = build_quant(layers, head, w, dev)
+        fq = lambda: step_quant(layers, head, ws, qs, qh)  # noqa: E731
+        msq = time_steps(fq, args.steps, args.warmup)
+        pk = per_kernel_ms(fq, args.steps)
+        wbytes = sum(q["codes"].numel() + 2 * q["scale"].numel() * 4 for q in qs)
+        if qh is not None:
+            wbytes += qh["codes"].numel() + 2 * qh["scale"].numel() * 4
+        out["quantized_base"] = {
+            "weights": "INT4 codes, groups of 128, fp32 scale and offset"
+                       + ("; head INT8" if qh is not None else ""),
+            "ms_per_step": round(msq, 5), "value": round(flops / (msq * 1e-3) / 1e12, 2),
+            "unit": "TFLOP/s", "frozen_weight_bytes": int(wbytes),
+            "kernels_ms_per_step": {k: round(v[0] / args.steps, 5) for k, v in pk.items()}}
+        log(f"[bench] quantized base: {msq:.4f} ms/step")
     if args.calib_copy_mib:
         n = args.calib_copy_mib * (1 << 20) // 4
         src = torch.ones(n, dtype=torch.float32, device=dev)

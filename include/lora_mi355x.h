@@ -113,6 +113,41 @@ lora_status_t frozen_linear_bwd_dx(const void *dy, const void *W, void *dx, int6
                                    int64_t d_in, int64_t d_out, lora_dtype_t dt, void *ws,
                                    size_t ws_bytes, void *hip_stream);
 
+/* ---- Quantized frozen base ------------------------------------------------
+ * The same three operations with W stored quantized and dequantized on the
+ * fly (the paper's algorithm "On-the-fly Dequantization": W = s * W_q + b,
+ * rematerialised for the forward and again for the backward; its mixed
+ * precision quantization keeps linear layers in INT4 and the output head in
+ * INT8).  Here the dequantized W never exists in memory: each GEMM workgroup
+ * expands the codes of its tile into bf16 in on-chip memory.
+ *
+ *   W_codes   [d_out][d_in * bits / 8] bytes of unsigned codes; bits = 8:
+ *             one code per byte; bits = 4: two per byte, the code of the even
+ *             input k in the low nibble, of k + 1 in the high nibble.
+ *   W_scale,  [d_out][d_in / group] fp32: the weight of code q in row n,
+ *   W_offset  input k is  W_scale[n][k / group] * q + W_offset[n][k / group].
+ *   group     a power of two >= 16 that divides d_in.
+ * Everything else is as for the bf16 entry points, with dt = LORA_BF16
+ * (x, A, B, y, dy, dx bf16) and rank r <= 64.  Errors as above, plus
+ * LORA_EINVAL for bits not 4 or 8 or a NULL codes / scale / offset pointer,
+ * and LORA_EUNSUPPORTED for a bad group or r > 64.  The workspace sizes are
+ * those of the bf16 operations. */
+lora_status_t lora_linear_fwd_q(const void *x, const void *W_codes, const float *W_scale,
+                                const float *W_offset, int bits, int64_t group, const void *A,
+                                const void *B, void *y, float *u_save, int64_t T, int64_t d_in,
+                                int64_t d_out, int64_t r, float scale, void *ws, size_t ws_bytes,
+                                void *hip_stream);
+lora_status_t lora_linear_bwd_q(const void *x, const void *W_codes, const float *W_scale,
+                                const float *W_offset, int bits, int64_t group, const void *A,
+                                const void *B, const float *u_saved, const void *dy, void *dx,
+                                float *dA, float *dB, int64_t T, int64_t d_in, int64_t d_out,
+                                int64_t r, float scale, void *ws, size_t ws_bytes,
+                                void *hip_stream);
+lora_status_t frozen_linear_bwd_dx_q(const void *dy, const void *W_codes, const float *W_scale,
+                                     const float *W_offset, int bits, int64_t group, void *dx,
+                                     int64_t T, int64_t d_in, int64_t d_out, void *ws,
+                                     size_t ws_bytes, void *hip_stream);
+
 /* Static text for a status code. */
 const char *lora_status_str(lora_status_t status);
 

@@ -30,10 +30,14 @@ enum KernelId {
   K_GEMM_FROZEN_DX,   // dx = dy W (rank 0)
   K_LORA_DOWN,        // u  = x A^T (+ LoRA-step operands)
   K_LORA_DY_B,        // du = s dy B (+ LoRA-step operand)
+  K_GEMM_FWD_Q,       // gemm_fwd with the quantized W dequantized on the fly
+  K_GEMM_BWD_DX_Q,    // gemm_bwd_dx, quantized W
+  K_GEMM_FROZEN_DX_Q, // gemm_frozen_dx, quantized W
   K_COUNT
 };
-const char *kKernelNames[K_COUNT] = {"gemm_fwd", "gemm_bwd_dx", "gemm_frozen_dx", "lora_down",
-                                     "lora_dy_b"};
+const char *kKernelNames[K_COUNT] = {"gemm_fwd",   "gemm_bwd_dx",   "gemm_frozen_dx",
+                                     "lora_down",  "lora_dy_b",     "gemm_fwd_q",
+                                     "gemm_bwd_dx_q", "gemm_frozen_dx_q"};
 
 struct EventPair {
   hipEvent_t a, b;
@@ -164,36 +168,68 @@ lora_status_t check_ws(void *ws, size_t ws_bytes, size_t need) {
   return LORA_OK;
 }
 
+// A quantized frozen weight W [d_out, d_in]: unsigned codes of `bits` bits
+// ([d_out][d_in * bits / 8] bytes; two 4-bit codes per byte, the even input in
+// the low nibble), W = scale * code + offset with one fp32 scale and offset per
+// group of `group` consecutive inputs of a row ([d_out][d_in / group]).
+struct QWeight {
+  const void *codes;
+  const float *scale, *offset;
+  int bits, log2g;
+};
+
+lora_status_t check_qweight(const void *codes, const float *scale, const float *offset, int bits,
+                            int64_t group, int64_t d_in, int64_t d_out, int64_t r,
+                            lora_dtype_t dt, QWeight *q, std::vector<Range> *ins) {
+  if (dt != LORA_BF16) return fail(LORA_EUNSUPPORTED, "a quantized weight needs dt = LORA_BF16");
+  if (bits != 4 && bits != 8) return fail(LORA_EINVAL, "bits must be 4 or 8");
+  if (!codes || !scale || !offset) return fail(LORA_EINVAL, "codes, scale and offset are required");
+  if (!aligned16(codes) || !aligned16(scale) || !aligned16(offset))
+    return fail(LORA_EINVAL, "pointers must be 16-byte aligned");
+  if (group < 16 || (group & (group - 1)) != 0 || d_in % group != 0)
+    return fail(LORA_EUNSUPPORTED, "group must be a power of two >= 16 that divides d_in");
+  if (r > 64) return fail(LORA_EUNSUPPORTED, "rank r must be at most 64 with a quantized weight");
+  int log2g = 0;
+  while ((int64_t(1) << log2g) < group) ++log2g;
+  *q = QWeight{codes, scale, offset, bits, log2g};
+  ins->push_back(rng(codes, d_out * d_in * bits / 8));
+  ins->push_back(rng(scale, d_out * (d_in / group) * 4));
+  ins->push_back(rng(offset, d_out * (d_in / group) * 4));
+  return LORA_OK;
+}
+
+void set_qweight(GemmArgs &g, const QWeight *q) {
+  if (!q) return;
+  g.B = q->codes;
+  g.qscale = q->scale;
+  g.qoffset = q->offset;
+  g.qlog2g = q->log2g;
+}
+
+hipError_t run_gemm(const GemmArgs &g, Dtype d, const QWeight *q, bool kmajor, const SideArgs *side,
+                    hipStream_t st) {
+  return q ? launch_gemm_q(g, q->bits, kmajor, side, st) : launch_gemm(g, d, kmajor, side, st);
+}
+
 lora_status_t hip_fail(hipError_t e, const char *what) {
   std::snprintf(g_err, sizeof g_err, "%s: %s", what, hipGetErrorString(e));
   return LORA_EHIP;
 }
 
-}  // namespace
-
-extern "C" {
-
-size_t lora_linear_workspace_bytes(lora_op_t op, int64_t T, int64_t d_in, int64_t d_out,
-                                   int64_t r, lora_dtype_t dt) {
-  if (check_shapes(T, d_in, d_out, op == LORA_OP_FROZEN_DX ? 0 : r, dt) != LORA_OK)
-    return (size_t)-1;
-  switch (op) {
-    case LORA_OP_FWD:
-      return fwd_layout(T, d_in, d_out, r, dt).total;
-    case LORA_OP_BWD:
-      return bwd_layout(T, d_in, d_out, r, dt).total;
-    case LORA_OP_FROZEN_DX:
-      return 0;
-  }
-  return (size_t)-1;
-}
-
-lora_status_t lora_linear_fwd(const void *x, const void *W, const void *A, const void *B,
-                              void *y, float *u_save, int64_t T, int64_t d_in, int64_t d_out,
-                              int64_t r, float scale, lora_dtype_t dt, void *ws,
-                              size_t ws_bytes, void *hip_stream) {
+// Forward with a bf16/fp32 W, or (qc != NULL) a quantized one.
+lora_status_t fwd_impl(const void *x, const void *W, const void *qc, const float *qs,
+                       const float *qo, int bits, int64_t group, const void *A, const void *B,
+                       void *y, float *u_save, int64_t T, int64_t d_in, int64_t d_out, int64_t r,
+                       float scale, lora_dtype_t dt, void *ws, size_t ws_bytes, void *hip_stream) {
   lora_status_t s = check_shapes(T, d_in, d_out, r, dt);
   if (s != LORA_OK) return s;
+  QWeight qw{};
+  std::vector<Range> qins;
+  if (qc) {
+    if ((s = check_qweight(qc, qs, qo, bits, group, d_in, d_out, r, dt, &qw, &qins)) != LORA_OK)
+      return s;
+    W = qc;
+  }
   if (!x || !W || !y) return fail(LORA_EINVAL, "x, W and y are required");
   if (r > 0 && (!A || !B)) return fail(LORA_EINVAL, "A and B are required when r > 0");
   if (r > 0 && !std::isfinite(scale)) return fail(LORA_EINVAL, "scale must be finite");
@@ -204,7 +240,9 @@ lora_status_t lora_linear_fwd(const void *x, const void *W, const void *A, const
   const size_t es = esize(dt);
   const size_t need = lora_linear_workspace_bytes(LORA_OP_FWD, T, d_in, d_out, r, dt);
   if ((s = check_ws(ws, ws_bytes, need)) != LORA_OK) return s;
-  std::vector<Range> ins = {rng(x, T * d_in * es), rng(W, d_out * d_in * es)};
+  std::vector<Range> ins = {rng(x, T * d_in * es)};
+  if (qc) ins.insert(ins.end(), qins.begin(), qins.end());
+  else ins.push_back(rng(W, d_out * d_in * es));
   std::vector<Range> outs = {rng(y, T * d_out * es)};
   if (r > 0) {
     ins.push_back(rng(A, r * d_in * es));
@@ -252,32 +290,42 @@ lora_status_t lora_linear_fwd(const void *x, const void *W, const void *A, const
       g.usum_src = upart; g.usum_out = u_save; g.usum_parts = ns; g.usum_r = (int)r;
     }
   }
-  Timed t(K_GEMM_FWD, st);
-  hipError_t e = launch_gemm(g, d, false, nullptr, st);
+  set_qweight(g, qc ? &qw : nullptr);
+  Timed t(qc ? K_GEMM_FWD_Q : K_GEMM_FWD, st);
+  hipError_t e = run_gemm(g, d, qc ? &qw : nullptr, false, nullptr, st);
   t.done();
   if (e != hipSuccess) return hip_fail(e, "gemm_fwd launch");
   return LORA_OK;
 }
 
-lora_status_t lora_linear_bwd(const void *x, const void *W, const void *A, const void *B,
-                              const float *u_saved, const void *dy, void *dx, float *dA,
-                              float *dB, int64_t T, int64_t d_in, int64_t d_out, int64_t r,
-                              float scale, lora_dtype_t dt, void *ws, size_t ws_bytes,
-                              void *hip_stream) {
+lora_status_t bwd_impl(const void *x, const void *W, const void *qc, const float *qs,
+                       const float *qo, int bits, int64_t group, const void *A, const void *B,
+                       const float *u_saved, const void *dy, void *dx, float *dA, float *dB,
+                       int64_t T, int64_t d_in, int64_t d_out, int64_t r, float scale,
+                       lora_dtype_t dt, void *ws, size_t ws_bytes, void *hip_stream) {
   lora_status_t s = check_shapes(T, d_in, d_out, r, dt);
   if (s != LORA_OK) return s;
+  QWeight qw{};
+  std::vector<Range> qins;
+  if (qc) {
+    if ((s = check_qweight(qc, qs, qo, bits, group, d_in, d_out, r, dt, &qw, &qins)) != LORA_OK)
+      return s;
+    W = qc;
+  }
   if (!dy || !W) return fail(LORA_EINVAL, "dy and W are required");
   if (r > 0 && (!x || !A || !B || !dA || !dB))
     return fail(LORA_EINVAL, "x, A, B, dA and dB are required when r > 0");
   if (r == 0 && !dx) return fail(LORA_EINVAL, "nothing to compute: r = 0 and dx is NULL");
   if (r > 0 && !std::isfinite(scale)) return fail(LORA_EINVAL, "scale must be finite");
-  const void *ptrs[] = {x, W, A, B, u_saved, dy, dx, dA, dB};
+  const void *ptrs[] = {x, qc ? nullptr : W, A, B, u_saved, dy, dx, dA, dB};
   for (const void *p : ptrs)
     if (p && !aligned16(p)) return fail(LORA_EINVAL, "pointers must be 16-byte aligned");
   const size_t es = esize(dt);
   const size_t need = lora_linear_workspace_bytes(LORA_OP_BWD, T, d_in, d_out, r, dt);
   if ((s = check_ws(ws, ws_bytes, need)) != LORA_OK) return s;
-  std::vector<Range> ins = {rng(W, d_out * d_in * es), rng(dy, T * d_out * es)};
+  std::vector<Range> ins = {rng(dy, T * d_out * es)};
+  if (qc) ins.insert(ins.end(), qins.begin(), qins.end());
+  else ins.push_back(rng(W, d_out * d_in * es));
   std::vector<Range> outs;
   if (dx) outs.push_back(rng(dx, T * d_in * es));
   if (r > 0) {
@@ -299,9 +347,10 @@ lora_status_t lora_linear_bwd(const void *x, const void *W, const void *A, const
   g.B = W; g.ldb = d_in;
   g.M = dx ? (int)T : 0; g.N = (int)d_in; g.K = (int)d_out;
   g.C = dx; g.ldc = d_in;
+  set_qweight(g, qc ? &qw : nullptr);
   if (r == 0) {
-    Timed t(K_GEMM_BWD_DX, st);
-    e = launch_gemm(g, d, true, nullptr, st);
+    Timed t(qc ? K_GEMM_BWD_DX_Q : K_GEMM_BWD_DX, st);
+    e = run_gemm(g, d, qc ? &qw : nullptr, true, nullptr, st);
     t.done();
     return e == hipSuccess ? LORA_OK : hip_fail(e, "gemm_bwd_dx launch");
   }
@@ -348,25 +397,31 @@ lora_status_t lora_linear_bwd(const void *x, const void *W, const void *A, const
   g.A2 = wsb + L.dutail; g.lda2 = L.ldt;
   g.B2 = ns > 1 ? (const void *)(wsb + L.acat) : A; g.ldb2 = d_in;
   g.r = (int)(ns * r);
-  Timed t(K_GEMM_BWD_DX, st);
-  e = launch_gemm(g, d, true, &sd, st);
+  Timed t(qc ? K_GEMM_BWD_DX_Q : K_GEMM_BWD_DX, st);
+  e = run_gemm(g, d, qc ? &qw : nullptr, true, &sd, st);
   t.done();
   if (e != hipSuccess) return hip_fail(e, "gemm_bwd_dx launch");
   return LORA_OK;
 }
 
-lora_status_t frozen_linear_bwd_dx(const void *dy, const void *W, void *dx, int64_t T,
-                                   int64_t d_in, int64_t d_out, lora_dtype_t dt, void *ws,
-                                   size_t ws_bytes, void *hip_stream) {
-  (void)ws;
-  (void)ws_bytes;
+lora_status_t frozen_impl(const void *dy, const void *W, const void *qc, const float *qs,
+                          const float *qo, int bits, int64_t group, void *dx, int64_t T,
+                          int64_t d_in, int64_t d_out, lora_dtype_t dt, void *hip_stream) {
   lora_status_t s = check_shapes(T, d_in, d_out, 0, dt);
   if (s != LORA_OK) return s;
+  QWeight qw{};
+  std::vector<Range> ins;
+  if (qc) {
+    if ((s = check_qweight(qc, qs, qo, bits, group, d_in, d_out, 0, dt, &qw, &ins)) != LORA_OK)
+      return s;
+    W = qc;
+  }
   if (!dy || !W || !dx) return fail(LORA_EINVAL, "dy, W and dx are required");
   if (!aligned16(dy) || !aligned16(W) || !aligned16(dx))
     return fail(LORA_EINVAL, "pointers must be 16-byte aligned");
   const size_t es = esize(dt);
-  std::vector<Range> ins = {rng(W, d_out * d_in * es), rng(dy, T * d_out * es)};
+  if (!qc) ins.push_back(rng(W, d_out * d_in * es));
+  ins.push_back(rng(dy, T * d_out * es));
   std::vector<Range> outs = {rng(dx, T * d_in * es)};
   if (any_overlap(outs, ins)) return fail(LORA_EINVAL, "an output overlaps an input");
   hipStream_t st = (hipStream_t)hip_stream;
@@ -375,10 +430,87 @@ lora_status_t frozen_linear_bwd_dx(const void *dy, const void *W, void *dx, int6
   g.B = W; g.ldb = d_in;
   g.M = (int)T; g.N = (int)d_in; g.K = (int)d_out;
   g.C = dx; g.ldc = d_in;
-  Timed t(K_GEMM_FROZEN_DX, st);
-  hipError_t e = launch_gemm(g, dt == LORA_BF16 ? DT_BF16 : DT_F32, true, nullptr, st);
+  set_qweight(g, qc ? &qw : nullptr);
+  Timed t(qc ? K_GEMM_FROZEN_DX_Q : K_GEMM_FROZEN_DX, st);
+  hipError_t e = run_gemm(g, dt == LORA_BF16 ? DT_BF16 : DT_F32, qc ? &qw : nullptr, true, nullptr, st);
   t.done();
   return e == hipSuccess ? LORA_OK : hip_fail(e, "gemm_frozen_dx launch");
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t lora_linear_workspace_bytes(lora_op_t op, int64_t T, int64_t d_in, int64_t d_out,
+                                   int64_t r, lora_dtype_t dt) {
+  if (check_shapes(T, d_in, d_out, op == LORA_OP_FROZEN_DX ? 0 : r, dt) != LORA_OK)
+    return (size_t)-1;
+  switch (op) {
+    case LORA_OP_FWD:
+      return fwd_layout(T, d_in, d_out, r, dt).total;
+    case LORA_OP_BWD:
+      return bwd_layout(T, d_in, d_out, r, dt).total;
+    case LORA_OP_FROZEN_DX:
+      return 0;
+  }
+  return (size_t)-1;
+}
+
+lora_status_t lora_linear_fwd(const void *x, const void *W, const void *A, const void *B,
+                              void *y, float *u_save, int64_t T, int64_t d_in, int64_t d_out,
+                              int64_t r, float scale, lora_dtype_t dt, void *ws,
+                              size_t ws_bytes, void *hip_stream) {
+  return fwd_impl(x, W, nullptr, nullptr, nullptr, 0, 0, A, B, y, u_save, T, d_in, d_out, r,
+                  scale, dt, ws, ws_bytes, hip_stream);
+}
+
+lora_status_t lora_linear_fwd_q(const void *x, const void *W_codes, const float *W_scale,
+                                const float *W_offset, int bits, int64_t group, const void *A,
+                                const void *B, void *y, float *u_save, int64_t T, int64_t d_in,
+                                int64_t d_out, int64_t r, float scale, void *ws, size_t ws_bytes,
+                                void *hip_stream) {
+  if (!W_codes) return fail(LORA_EINVAL, "codes, scale and offset are required");
+  return fwd_impl(x, nullptr, W_codes, W_scale, W_offset, bits, group, A, B, y, u_save, T, d_in,
+                  d_out, r, scale, LORA_BF16, ws, ws_bytes, hip_stream);
+}
+
+lora_status_t lora_linear_bwd(const void *x, const void *W, const void *A, const void *B,
+                              const float *u_saved, const void *dy, void *dx, float *dA,
+                              float *dB, int64_t T, int64_t d_in, int64_t d_out, int64_t r,
+                              float scale, lora_dtype_t dt, void *ws, size_t ws_bytes,
+                              void *hip_stream) {
+  return bwd_impl(x, W, nullptr, nullptr, nullptr, 0, 0, A, B, u_saved, dy, dx, dA, dB, T, d_in,
+                  d_out, r, scale, dt, ws, ws_bytes, hip_stream);
+}
+
+lora_status_t lora_linear_bwd_q(const void *x, const void *W_codes, const float *W_scale,
+                                const float *W_offset, int bits, int64_t group, const void *A,
+                                const void *B, const float *u_saved, const void *dy, void *dx,
+                                float *dA, float *dB, int64_t T, int64_t d_in, int64_t d_out,
+                                int64_t r, float scale, void *ws, size_t ws_bytes,
+                                void *hip_stream) {
+  if (!W_codes) return fail(LORA_EINVAL, "codes, scale and offset are required");
+  return bwd_impl(x, nullptr, W_codes, W_scale, W_offset, bits, group, A, B, u_saved, dy, dx, dA,
+                  dB, T, d_in, d_out, r, scale, LORA_BF16, ws, ws_bytes, hip_stream);
+}
+
+lora_status_t frozen_linear_bwd_dx(const void *dy, const void *W, void *dx, int64_t T,
+                                   int64_t d_in, int64_t d_out, lora_dtype_t dt, void *ws,
+                                   size_t ws_bytes, void *hip_stream) {
+  (void)ws;
+  (void)ws_bytes;
+  return frozen_impl(dy, W, nullptr, nullptr, nullptr, 0, 0, dx, T, d_in, d_out, dt, hip_stream);
+}
+
+lora_status_t frozen_linear_bwd_dx_q(const void *dy, const void *W_codes, const float *W_scale,
+                                     const float *W_offset, int bits, int64_t group, void *dx,
+                                     int64_t T, int64_t d_in, int64_t d_out, void *ws,
+                                     size_t ws_bytes, void *hip_stream) {
+  (void)ws;
+  (void)ws_bytes;
+  if (!W_codes) return fail(LORA_EINVAL, "codes, scale and offset are required");
+  return frozen_impl(dy, nullptr, W_codes, W_scale, W_offset, bits, group, dx, T, d_in, d_out,
+                     LORA_BF16, hip_stream);
 }
 
 const char *lora_status_str(lora_status_t status) {

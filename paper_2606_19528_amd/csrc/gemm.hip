@@ -53,7 +53,8 @@ __device__ __forceinline__ void static_for(F &&f) {
   }
 }
 
-template <class E, int BM, int BN, int WM, int WN, int WK, int BMODE, int BKB, int NBUF, int RD, int FS>
+template <class E, int BM, int BN, int WM, int WN, int WK, int BMODE, int BKB, int NBUF, int RD, int FS,
+          int QB = 0>
 __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int group_m,
                                                                  SideArgs side, int nside) {
   typedef typename E::T T;
@@ -90,6 +91,12 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   static_assert(NBUF == 2 || NBUF == 3, "LDS ring depth");
   static_assert(RD >= 2 && RD <= 4, "register ring depth");
   static_assert(!FS || NBUF == 2, "staged fragments use two LDS buffers");
+  // Quantized B (QB = 4 or 8 bits): each thread dequantizes one piece of 16
+  // consecutive weights of a W row per stage.
+  constexpr int QPIECES = BMODE == B_ROW ? BN * (BKE / 16) : BKE * (BN / 16);
+  static_assert(QB == 0 || QB == 4 || QB == 8, "code width");
+  static_assert(QB == 0 || (ES == 2 && FS && BMODE != B_KMAJ_REG && QPIECES == NT),
+                "quantized B: bf16, staged fragments, one 16-weight piece per thread");
 
   __shared__ __align__(16) char smem[LDS];
 
@@ -153,7 +160,11 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   }
 
   const int nk_main = (g.K + BKE - 1) / BKE;
-  const int nk = nk_main + (g.r > 0 ? (g.r + BKE - 1) / BKE : 0);  // + LoRA steps
+  const int nk_lora = g.r > 0 ? (g.r + BKE - 1) / BKE : 0;
+  const int nk = nk_main + nk_lora;
+  // Stage order: the LoRA steps follow the main ones, except with a quantized
+  // B, where they come first (stage 0, loaded and stored by the prologue), so
+  // that the main loop only ever runs the dequantizing path.
 
   // Buffer resources.  The tile's rows past M (and, for row-major B, past N)
   // lie beyond num_records; k past K (or j past r) is masked per stage by
@@ -209,17 +220,42 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
     }
   }
 
+  // Quantized B: the thread's piece of 16 weights (W row `qrow`, first weight
+  // of the piece `qcol` within the stage or tile), codes through one buffer
+  // resource, per-group scale and offset through two more.
+  const int qrow = BMODE == B_ROW ? tid / (BKE / 16) : tid / (BN / 16);
+  const int qcol = BMODE == B_ROW ? (tid % (BKE / 16)) * 16 : (tid % (BN / 16)) * 16;
+  const int64_t q_rowbytes = (int64_t)g.ldb * (QB ? QB : 8) / 8;
+  const int64_t q_ldg = g.ldb >> g.qlog2g;  // groups per W row
+  __amdgpu_buffer_rsrc_t rsQ, rsQs, rsQo;
+  if constexpr (QB && BMODE == B_ROW) {
+    const int nrows = min(g.N - n0, BN);
+    rsQ = __builtin_amdgcn_make_buffer_rsrc((void *)((const char *)g.B + n0 * q_rowbytes), (short)0,
+                                            (int)(nrows * q_rowbytes), 0x00020000);
+    rsQs = __builtin_amdgcn_make_buffer_rsrc((void *)(g.qscale + n0 * q_ldg), (short)0,
+                                             (int)(nrows * q_ldg * 4), 0x00020000);
+    rsQo = __builtin_amdgcn_make_buffer_rsrc((void *)(g.qoffset + n0 * q_ldg), (short)0,
+                                             (int)(nrows * q_ldg * 4), 0x00020000);
+  }
+  constexpr int QW = QB == 4 ? 2 : 4;  // dwords of codes per piece
+  uint32_t rqc[QB ? RD : 1][QW];
+  float rqs[QB ? RD : 1], rqo[QB ? RD : 1];
+
   u32x4 ra[RD][A_PER];
-  u32x4 rb[RD][RB];
+  u32x4 rb[QB ? 1 : RD][RB];  // quantized B: only the LoRA stage is bf16
 
   // ---- global -> register set S for stage kt (zeros past the end) ----------
   // Stages kt < nk_main stream x/dy and W; the following ones stream the LoRA
   // operands (j = (kt - nk_main) * BKE ...).  The choice is a uniform select
   // of resources and offsets, so the step stays branch-free.
-  auto load_stage = [&](auto SET, int kt) {
+  auto is_lora = [&](int kt) { return QB ? kt < nk_lora : kt >= nk_main; };
+  auto stage_k0 = [&](int kt) {
+    return (QB ? (kt < nk_lora ? kt : kt - nk_lora) : (kt >= nk_main ? kt - nk_main : kt)) * BKE;
+  };
+  auto load_A = [&](auto SET, int kt) {
     constexpr int S = decltype(SET)::value;
-    const bool lora = kt >= nk_main;
-    const int k0 = (lora ? kt - nk_main : kt) * BKE;
+    const bool lora = is_lora(kt);
+    const int k0 = stage_k0(kt);
     const int krem = (lora ? g.r : g.K) - k0;  // valid k remaining (uniform)
     const int soff = k0 * ES;
     const __amdgpu_buffer_rsrc_t ra_rs = lora ? rsA2 : rsA;
@@ -228,6 +264,53 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
       ra[S][i] = __builtin_bit_cast(
           u32x4, __builtin_amdgcn_raw_buffer_load_b128(
                      ra_rs, kca[i] < krem ? (lora ? va2[i] : va[i]) : OOB, soff, 0));
+  };
+  // Codes, scale and offset of the thread's piece (main stages only); a piece
+  // past the end of W reads zero codes, scale and offset, i.e. weight 0.
+  auto load_Bq = [&](auto SET, int kt) {
+    constexpr int S = decltype(SET)::value;
+    if constexpr (QB) {
+      const int k0 = stage_k0(kt);
+      const int krem = g.K - k0;
+      __amdgpu_buffer_rsrc_t rq, rs, ro;
+      uint32_t vq, vs;
+      if constexpr (BMODE == B_ROW) {
+        const bool ok = k0 + qcol < g.K;
+        rq = rsQ; rs = rsQs; ro = rsQo;
+        vq = ok ? (uint32_t)(qrow * q_rowbytes + (int64_t)(k0 + qcol) * QB / 8) : OOB;
+        vs = ok ? (uint32_t)((qrow * q_ldg + ((k0 + qcol) >> g.qlog2g)) * 4) : OOB;
+      } else {
+        // W rows k0 .. k0 + BKE - 1 (rows past K out of range), columns of the tile
+        const int rows = krem > 0 ? min(krem, BKE) : 0;
+        rq = __builtin_amdgcn_make_buffer_rsrc((void *)((const char *)g.B + k0 * q_rowbytes), (short)0,
+                                               (int)(rows * q_rowbytes), 0x00020000);
+        rs = __builtin_amdgcn_make_buffer_rsrc((void *)(g.qscale + k0 * q_ldg), (short)0,
+                                               (int)(rows * q_ldg * 4), 0x00020000);
+        ro = __builtin_amdgcn_make_buffer_rsrc((void *)(g.qoffset + k0 * q_ldg), (short)0,
+                                               (int)(rows * q_ldg * 4), 0x00020000);
+        const bool ok = n0 + qcol < g.N;
+        vq = ok ? (uint32_t)(qrow * q_rowbytes + (int64_t)(n0 + qcol) * QB / 8) : OOB;
+        vs = ok ? (uint32_t)((qrow * q_ldg + ((n0 + qcol) >> g.qlog2g)) * 4) : OOB;
+      }
+      if constexpr (QB == 4) {
+        const auto c = __builtin_amdgcn_raw_buffer_load_b64(rq, vq, 0, 0);
+        rqc[S][0] = c[0];
+        rqc[S][1] = c[1];
+      } else {
+        const auto c = __builtin_amdgcn_raw_buffer_load_b128(rq, vq, 0, 0);
+#pragma unroll
+        for (int d = 0; d < 4; ++d) rqc[S][d] = c[d];
+      }
+      rqs[S] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, vs, 0, 0));
+      rqo[S] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(ro, vs, 0, 0));
+    }
+  };
+  auto load_B = [&](auto SET, int kt) {
+    constexpr int S = QB ? 0 : decltype(SET)::value;
+    const bool lora = is_lora(kt);
+    const int k0 = stage_k0(kt);
+    const int krem = (lora ? g.r : g.K) - k0;  // valid k remaining (uniform)
+    const int soff = k0 * ES;
     if constexpr (BMODE == B_ROW) {
       const __amdgpu_buffer_rsrc_t rb_rs = lora ? rsB2 : rsB;
 #pragma unroll
@@ -261,16 +344,55 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
     }
   };
 
+  auto load_stage = [&](auto SET, int kt) {
+    load_A(SET, kt);
+    if constexpr (QB) load_Bq(SET, kt);
+    else load_B(SET, kt);
+  };
+
   // ---- register set S -> LDS buffer `buf` -----------------------------------
-  auto store_stage = [&](auto SET, int buf) {
+  auto store_A = [&](auto SET, int buf) {
     constexpr int S = decltype(SET)::value;
     char *sA = smem + buf * STAGE;
-    char *sB = sA + A_BYTES;
 #pragma unroll
     for (int i = 0; i < A_PER; ++i) {
       const int c = tid + i * NT;
       if (A_CH % NT == 0 || c < A_CH) st16(sA + (c / CPR) * ROWA + (c % CPR) * 16, ra[S][i]);
     }
+  };
+  // Dequantize the thread's piece: w = scale * code + offset, rounded to bf16,
+  // two 16-byte chunks at the piece's place in the B tile.
+  auto store_Bq = [&](auto SET, int buf) {
+    constexpr int S = decltype(SET)::value;
+    if constexpr (QB) {
+      char *sB = smem + buf * STAGE + A_BYTES;
+      float f[16];
+      if constexpr (QB == 4) {
+        // dword d holds weights 8d .. 8d+7; byte j of it has weight 8d+2j in
+        // its low nibble and 8d+2j+1 in its high nibble.
+#pragma unroll
+        for (int d = 0; d < 2; ++d) {
+          const uint32_t lo = rqc[S][d] & 0x0F0F0F0Fu, hi = (rqc[S][d] >> 4) & 0x0F0F0F0Fu;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            f[8 * d + 2 * j] = fmaf(rqs[S], (float)((lo >> (8 * j)) & 0xFFu), rqo[S]);
+            f[8 * d + 2 * j + 1] = fmaf(rqs[S], (float)((hi >> (8 * j)) & 0xFFu), rqo[S]);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int d = 0; d < 4; ++d)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) f[4 * d + j] = fmaf(rqs[S], (float)((rqc[S][d] >> (8 * j)) & 0xFFu), rqo[S]);
+      }
+      char *dst = BMODE == B_ROW ? sB + qrow * ROWA + qcol * 2 : sB + qrow * ROWT + qcol * 2;
+      st16(dst, pack_vec(E(), f));
+      st16(dst + 16, pack_vec(E(), f + 8));
+    }
+  };
+  auto store_B = [&](auto SET, int buf) {
+    constexpr int S = QB ? 0 : decltype(SET)::value;
+    char *sB = smem + buf * STAGE + A_BYTES;
     if constexpr (BMODE == B_ROW) {
 #pragma unroll
       for (int i = 0; i < B_PER; ++i) {
@@ -296,6 +418,12 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
         }
       }
     }
+  };
+
+  auto store_stage = [&](auto SET, int buf) {
+    store_A(SET, buf);
+    if constexpr (QB) store_Bq(SET, buf);
+    else store_B(SET, buf);
   };
 
   f32x16 acc[FM][FN];
@@ -366,6 +494,7 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   // buffer index is a run-time value.  Each step is branch-free: loads of
   // stages past the end select out-of-range offsets (zeros, no memory traffic)
   // and stores of such stages land in an LDS buffer that is never read again.
+  static_assert(!QB || FS, "quantized B runs the staged-fragment schedule");
   if constexpr (FS) {
     // Staged fragments: every MFMA fragment of a stage is read from LDS one
     // step ahead into the second of two register sets, so the MFMAs of a
@@ -384,14 +513,31 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
 #pragma unroll
       for (int s2 = 0; s2 < SPW; ++s2) mma_frags(f[s2]);
     };
+    // (With a quantized B, stage 0 may be the bf16 LoRA step.)
+    auto pro_load = [&](auto SET, int kt) {
+      if (QB && is_lora(kt)) {
+        load_A(SET, kt);
+        load_B(SET, kt);
+      } else {
+        load_stage(SET, kt);
+      }
+    };
+    auto pro_store = [&](auto SET, int kt, int buf) {
+      if (QB && is_lora(kt)) {
+        store_A(SET, buf);
+        store_B(SET, buf);
+      } else {
+        store_stage(SET, buf);
+      }
+    };
     static_for<0, RD>([&](auto SI) {
       constexpr int st = decltype(SI)::value;
-      load_stage(IC<st>(), st);
+      pro_load(IC<st>(), st);
     });
     static_for<0, E_ST>([&](auto SI) {
       constexpr int st = decltype(SI)::value;
-      store_stage(IC<st % RD>(), st);
-      if constexpr (st + RD < D_LD) load_stage(IC<(st + RD) % RD>(), st + RD);
+      pro_store(IC<st % RD>(), st, st);
+      if constexpr (st + RD < D_LD) pro_load(IC<(st + RD) % RD>(), st + RD);
     });
     __syncthreads();
     read_stage(0, F[0]);
@@ -408,8 +554,8 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
         read_stage(1 - cb, F[(P + 1) % 2]);
         mma_stage(F[P % 2]);
         constexpr int NM = SPW * FM * FN;
-        constexpr int NV = A_PER + (BMODE == B_KMAJ_REG ? KB_PER * VEC : B_PER);
-        constexpr int NW = A_PER + (BMODE == B_KMAJ_REG ? KB_PER * VEC : B_PER);
+        constexpr int NV = A_PER + (QB ? 3 : BMODE == B_KMAJ_REG ? KB_PER * VEC : B_PER);
+        constexpr int NW = A_PER + (QB ? 2 : BMODE == B_KMAJ_REG ? KB_PER * VEC : B_PER);
         constexpr int NR = SPW * (FM + FN * (BMODE == B_KMAJ_TR ? 2 : 1));
         static_for<0, NM>([&](auto MI) {
           constexpr int m = decltype(MI)::value;
@@ -587,7 +733,8 @@ static int pick_group_m(int tiles_m, int tiles_n, int BM, int BN) {
   return gmv;
 }
 
-template <class E, int BM, int BN, int WM, int WN, int WK, int BMODE, int BKB, int NBUF, int RD, int FS>
+template <class E, int BM, int BN, int WM, int WN, int WK, int BMODE, int BKB, int NBUF, int RD, int FS,
+          int QB = 0>
 static hipError_t launch_cfg(const GemmArgs &g, const SideArgs *side, hipStream_t st) {
   const int tm = g.M > 0 ? (g.M + BM - 1) / BM : 0, tn = (g.N + BN - 1) / BN;
   SideArgs sa{};
@@ -598,7 +745,7 @@ static hipError_t launch_cfg(const GemmArgs &g, const SideArgs *side, hipStream_
   }
   const int grid = tm * tn + nside;
   if (grid == 0) return hipSuccess;
-  hipLaunchKernelGGL((gemm_kernel<E, BM, BN, WM, WN, WK, BMODE, BKB, NBUF, RD, FS>), dim3(grid),
+  hipLaunchKernelGGL((gemm_kernel<E, BM, BN, WM, WN, WK, BMODE, BKB, NBUF, RD, FS, QB>), dim3(grid),
                      dim3(64 * WM * WN * WK), 0, st, g, tm > 0 ? pick_group_m(tm, tn, BM, BN) : 1,
                      sa, nside);
   return hipGetLastError();
@@ -622,6 +769,17 @@ static int pick_shape(int M, int N) {
   const double c0 = cost(128, 128, 0.80), c1 = cost(256, 128, 0.87), c2 = cost(256, 256, 1.0);
   if (c2 <= c1 && c2 <= c0) return 2;
   return c1 < c0 ? 1 : 0;
+}
+
+hipError_t launch_gemm_q(const GemmArgs &g, int bits, bool b_kmajor, const SideArgs *side,
+                         hipStream_t st) {
+  if (bits == 4)
+    return b_kmajor ? launch_cfg<BF16, 128, 128, 2, 2, 2, B_KMAJ_TR, 128, 2, 3, 2, 4>(g, side, st)
+                    : launch_cfg<BF16, 128, 128, 2, 2, 2, B_ROW, 128, 2, 3, 2, 4>(g, side, st);
+  if (bits == 8)
+    return b_kmajor ? launch_cfg<BF16, 128, 128, 2, 2, 2, B_KMAJ_TR, 128, 2, 3, 2, 8>(g, side, st)
+                    : launch_cfg<BF16, 128, 128, 2, 2, 2, B_ROW, 128, 2, 3, 2, 8>(g, side, st);
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_gemm(const GemmArgs &g, Dtype dt, bool b_kmajor, const SideArgs *side,

@@ -61,11 +61,22 @@ struct GemmArgs {
   const float *usum_src;
   float *usum_out;
   int usum_parts, usum_r;
+  // Quantized B (launch_gemm_q): B holds unsigned codes of W ([rows][ldb]
+  // weights, bits/8 bytes each, two 4-bit codes per byte with the even weight
+  // in the low nibble), w = qscale * code + qoffset with one scale and offset
+  // per group of 2^qlog2g consecutive weights of a W row ([rows][ldb >> qlog2g]).
+  const float *qscale;
+  const float *qoffset;
+  int qlog2g;
 };
 
 // GEMM launch; `side` (may be NULL) adds the token-reduction workgroups.
 hipError_t launch_gemm(const GemmArgs &g, Dtype dt, bool b_kmajor, const SideArgs *side,
                        hipStream_t st);
+// bf16 GEMM whose B is the quantized frozen weight (bits = 4 or 8), dequantized
+// into LDS; the LoRA step (r <= 64) runs first.
+hipError_t launch_gemm_q(const GemmArgs &g, int bits, bool b_kmajor, const SideArgs *side,
+                         hipStream_t st);
 
 // Number of side workgroups needed for `side` (a multiple of 8).
 int side_workgroups(const SideArgs &s, Dtype dt);

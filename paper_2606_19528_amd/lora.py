@@ -46,6 +46,14 @@ def lib() -> ctypes.CDLL:
     L.lora_linear_bwd.restype = i32
     L.frozen_linear_bwd_dx.argtypes = [vp, vp, vp, i64, i64, i64, i32, vp, sz, vp]
     L.frozen_linear_bwd_dx.restype = i32
+    L.lora_linear_fwd_q.argtypes = [vp, vp, vp, vp, i32, i64, vp, vp, vp, vp, i64, i64, i64, i64,
+                                    f32, vp, sz, vp]
+    L.lora_linear_fwd_q.restype = i32
+    L.lora_linear_bwd_q.argtypes = [vp, vp, vp, vp, i32, i64, vp, vp, vp, vp, vp, vp, vp, i64, i64,
+                                    i64, i64, f32, vp, sz, vp]
+    L.lora_linear_bwd_q.restype = i32
+    L.frozen_linear_bwd_dx_q.argtypes = [vp, vp, vp, vp, i32, i64, vp, i64, i64, i64, vp, sz, vp]
+    L.frozen_linear_bwd_dx_q.restype = i32
     L.lora_status_str.argtypes = [i32]
     L.lora_status_str.restype = ctypes.c_char_p
     L.lora_last_error.argtypes = []
@@ -149,6 +157,57 @@ def frozen_linear_bwd_dx(dy, W, dx, ws=None, stream=None):
                                     0 if ws is None else ws.numel() * ws.element_size(),
                                     _stream(stream))
     _check(st, "frozen_linear_bwd_dx")
+    return dx
+
+
+# --- quantized frozen base (codes + per-group scale / offset) ----------------------
+def _qw(Wq):
+    """(codes, scale, offset, bits, group, d_out, d_in) of a quantized weight given
+    as a dict with keys codes (uint8 [d_out, d_in*bits/8]), scale and offset
+    (fp32 [d_out, d_in/group]) and bits."""
+    codes, sc, off, bits = Wq["codes"], Wq["scale"], Wq["offset"], int(Wq["bits"])
+    d_out = codes.shape[0]
+    d_in = codes.shape[1] * 8 // bits
+    group = d_in // sc.shape[1]
+    return codes, sc, off, bits, group, d_out, d_in
+
+
+def lora_linear_fwd_q(x, Wq, A, B, y, u_save=None, scale: float = 1.0, ws=None, stream=None):
+    """lora_linear_fwd with the frozen W quantized (dict, see _qw)."""
+    codes, sc, off, bits, group, d_out, d_in = _qw(Wq)
+    T = x.shape[0]
+    r = 0 if A is None else A.shape[0]
+    ws, ws_bytes = _ws(ws, lora_linear_workspace_bytes(LORA_OP_FWD, T, d_in, d_out, r, LORA_BF16), x)
+    st = lib().lora_linear_fwd_q(_ptr(x), _ptr(codes), _ptr(sc), _ptr(off), bits, group, _ptr(A),
+                                 _ptr(B), _ptr(y), _ptr(u_save), T, d_in, d_out, r, float(scale),
+                                 _ptr(ws), ws_bytes, _stream(stream))
+    _check(st, "lora_linear_fwd_q")
+    return y
+
+
+def lora_linear_bwd_q(x, Wq, A, B, u_saved, dy, dx, dA, dB, scale: float = 1.0, ws=None,
+                      stream=None):
+    """lora_linear_bwd with the frozen W quantized (dict, see _qw)."""
+    codes, sc, off, bits, group, d_out, d_in = _qw(Wq)
+    T = dy.shape[0]
+    r = 0 if A is None else A.shape[0]
+    ws, ws_bytes = _ws(ws, lora_linear_workspace_bytes(LORA_OP_BWD, T, d_in, d_out, r, LORA_BF16), dy)
+    st = lib().lora_linear_bwd_q(_ptr(x), _ptr(codes), _ptr(sc), _ptr(off), bits, group, _ptr(A),
+                                 _ptr(B), _ptr(u_saved), _ptr(dy), _ptr(dx), _ptr(dA), _ptr(dB), T,
+                                 d_in, d_out, r, float(scale), _ptr(ws), ws_bytes, _stream(stream))
+    _check(st, "lora_linear_bwd_q")
+    return dx, dA, dB
+
+
+def frozen_linear_bwd_dx_q(dy, Wq, dx, ws=None, stream=None):
+    """frozen_linear_bwd_dx with W quantized (dict, see _qw)."""
+    codes, sc, off, bits, group, d_out, d_in = _qw(Wq)
+    T = dy.shape[0]
+    st = lib().frozen_linear_bwd_dx_q(_ptr(dy), _ptr(codes), _ptr(sc), _ptr(off), bits, group,
+                                      _ptr(dx), T, d_in, d_out, _ptr(ws),
+                                      0 if ws is None else ws.numel() * ws.element_size(),
+                                      _stream(stream))
+    _check(st, "frozen_linear_bwd_dx_q")
     return dx
 
 

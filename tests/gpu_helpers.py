@@ -54,6 +54,30 @@ def gpu_lora(inp: dict, s: float, recompute_u: bool = False, want_dx: bool = Tru
     return out
 
 
+def gpu_lora_q(inp: dict, Wq: dict, s: float, recompute_u: bool = False) -> dict:
+    """gpu_lora with the frozen W given quantized (workloads.quant_weight);
+    inp["W"] is ignored."""
+    d = {k: v.to("cuda") for k, v in inp.items() if k != "W"}
+    q = {k: (v.to("cuda") if hasattr(v, "to") else v) for k, v in Wq.items()}
+    x, A, B, dy = d["x"], d["A"], d["B"], d["dy"]
+    T, K = x.shape
+    N = dy.shape[1]
+    r = A.shape[0]
+    y = torch.empty(T, N, dtype=torch.bfloat16, device="cuda")
+    u = torch.empty(T, r, dtype=torch.float32, device="cuda") if r else None
+    lm.lora_linear_fwd_q(x, q, A if r else None, B if r else None, y, u, s)
+    dx = torch.empty(T, K, dtype=torch.bfloat16, device="cuda")
+    dA = torch.empty(r, K, dtype=torch.float32, device="cuda") if r else None
+    dB = torch.empty(N, r, dtype=torch.float32, device="cuda") if r else None
+    lm.lora_linear_bwd_q(x, q, A if r else None, B if r else None, None if recompute_u else u, dy,
+                         dx, dA, dB, s)
+    torch.cuda.synchronize()
+    out = {"y": y.cpu(), "dx": dx.cpu()}
+    if r:
+        out.update(u=u.cpu(), dA=dA.cpu(), dB=dB.cpu())
+    return out
+
+
 def oracle_lora(orc, inp: dict, s: float, rows=None) -> dict:
     """Oracle results; y and dx restricted to `rows` (all rows if None)."""
     x, W, A, B, dy = (inp[k] for k in ("x", "W", "A", "B", "dy"))

@@ -149,6 +149,65 @@ def test_frozen_rejects(kw, code):
     assert frozen(**kw) == code
 
 
+def fwd_q(**kw):
+    a = dict(x=P(1), codes=P(2), sc=P(11), off=P(12), bits=4, group=128, A=P(3), B=P(4), y=P(5),
+             u=P(6), T=64, K=256, N=256, r=8, s=2.0, ws=P(7), wsb=1 << 24)
+    a.update(kw)
+    return lm.lib().lora_linear_fwd_q(a["x"], a["codes"], a["sc"], a["off"], a["bits"], a["group"],
+                                      a["A"], a["B"], a["y"], a["u"], a["T"], a["K"], a["N"],
+                                      a["r"], a["s"], a["ws"], a["wsb"], None)
+
+
+def bwd_q(**kw):
+    a = dict(x=P(1), codes=P(2), sc=P(11), off=P(12), bits=8, group=64, A=P(3), B=P(4), u=P(6),
+             dy=P(8), dx=P(9), dA=P(10), dB=P(13), T=64, K=256, N=256, r=8, s=2.0, ws=P(7),
+             wsb=1 << 24)
+    a.update(kw)
+    return lm.lib().lora_linear_bwd_q(a["x"], a["codes"], a["sc"], a["off"], a["bits"], a["group"],
+                                      a["A"], a["B"], a["u"], a["dy"], a["dx"], a["dA"], a["dB"],
+                                      a["T"], a["K"], a["N"], a["r"], a["s"], a["ws"], a["wsb"],
+                                      None)
+
+
+def frozen_q(**kw):
+    a = dict(dy=P(8), codes=P(2), sc=P(11), off=P(12), bits=8, group=128, dx=P(9), T=64, K=256,
+             N=256)
+    a.update(kw)
+    return lm.lib().frozen_linear_bwd_dx_q(a["dy"], a["codes"], a["sc"], a["off"], a["bits"],
+                                           a["group"], a["dx"], a["T"], a["K"], a["N"], None, 0,
+                                           None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(bits=3), EINVAL), (dict(bits=16), EINVAL), (dict(codes=None), EINVAL),
+    (dict(sc=None), EINVAL), (dict(off=misaligned(12)), EINVAL),
+    (dict(group=8), EUNSUP), (dict(group=96), EUNSUP), (dict(group=512), EUNSUP),
+    (dict(r=65), EUNSUP), (dict(K=250), EUNSUP), (dict(x=None), EINVAL),
+    (dict(y=P(2)), EINVAL),                     # y aliases the codes
+    (dict(wsb=10), EWS),
+])
+def test_fwd_q_rejects(kw, code):
+    assert fwd_q(**kw) == code
+    assert lm.lib().lora_last_error()
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(bits=2), EINVAL), (dict(group=48), EUNSUP), (dict(r=80), EUNSUP),
+    (dict(dx=P(11)), EINVAL),                   # dx aliases the scales
+    (dict(dy=None), EINVAL), (dict(dA=None), EINVAL),
+])
+def test_bwd_q_rejects(kw, code):
+    assert bwd_q(**kw) == code
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(bits=5), EINVAL), (dict(group=1024), EUNSUP), (dict(dx=P(2)), EINVAL),
+    (dict(codes=misaligned(2)), EINVAL), (dict(dy=None), EINVAL),
+])
+def test_frozen_q_rejects(kw, code):
+    assert frozen_q(**kw) == code
+
+
 def test_rank0_ignores_lora_pointers():
     # r = 0: A, B, u, dA, dB are ignored, so NULL or misaligned values do not matter
     # (the call would then launch; only validation failures are exercised on the CPU,

@@ -145,6 +145,31 @@ def frozen_inputs(T: int, d_in: int, d_out: int, seed: int = 0,
     return {"W": W.to(dtype).contiguous(), "dy": dy.to(dtype).contiguous()}
 
 
+def quant_weight(d_out: int, d_in: int, bits: int = 4, group: int = 128, seed: int = 0,
+                 device="cpu") -> dict:
+    """A quantized frozen weight in the layout of the library's quantized entry
+    points: codes ~ U{0 .. 2^bits - 1} packed along d_in (two 4-bit codes per
+    byte, even input in the low nibble), and per (row, group) an fp32 scale
+    ~ 0.02 * sqrt(12) / 2^bits * U(0.5, 1.5) and an fp32 offset centring the
+    codes' range near zero, so that the weights spread like the N(0, 0.02)
+    bf16 weights of lora_inputs.  Drawn in that order (codes, scale factor,
+    offset jitter) from one seeded generator."""
+    g = _gen(seed, device)
+    levels = 1 << bits
+    q = torch.randint(0, levels, (d_out, d_in), generator=g, device=device, dtype=torch.int32)
+    if bits == 4:
+        codes = (q[:, 0::2] | (q[:, 1::2] << 4)).to(torch.uint8)
+    else:
+        codes = q.to(torch.uint8)
+    ng = d_in // group
+    step = 0.02 * (12.0 ** 0.5) / levels
+    scale = step * (0.5 + torch.rand(d_out, ng, generator=g, device=device))
+    jitter = 0.25 * (torch.rand(d_out, ng, generator=g, device=device) - 0.5)
+    offset = -scale * ((levels - 1) / 2.0 + jitter)
+    return {"codes": codes.contiguous(), "scale": scale.float().contiguous(),
+            "offset": offset.float().contiguous(), "bits": bits}
+
+
 def sample_rows(T: int, n: int = 64, seed: int = 1234) -> list:
     """Deterministic sorted sample of row indices, always including the first and
     last rows (the ragged-tail tile), of size min(n, T)."""
