@@ -13,6 +13,8 @@ per-definition functions into the forward and backward passes:
     backward:  G = dY B ; dU = s G ; dX = dY W + dU A ; dA = dU^T X ;
                dB = s dY^T U
     quantized base:  W = S * W_q + Bo per group (dequant), then as above
+    LM head:   J = union of top-k table rows of the trainable targets;
+               loss_t = logsumexp_{j in J} h_t.w_j - h_t.w_{y_t};  dH (ce_reduced)
 
 (LoRA as described in the paper's background on parameter-efficient
 fine-tuning, with r and alpha from its hyperparameter table; frozen-base
@@ -38,7 +40,7 @@ GCC_FLAGS = ["-O2", "-fPIC", "-shared", "-fopenmp", "-std=c11"]
 
 def build_shared(src: str = _SRC, out: str = _LIB_PATH) -> str:
     """Compile the oracle source into a shared object (gcc -O2, no fast-math)."""
-    cmd = ["gcc", *GCC_FLAGS, "-o", out, src]
+    cmd = ["gcc", *GCC_FLAGS, "-o", out, src, "-lm"]
     subprocess.run(cmd, check=True)
     return out
 
@@ -59,8 +61,10 @@ def _declare(lib: ctypes.CDLL) -> ctypes.CDLL:
     lib.oracle_lora_db.argtypes = [_dp, _dp, _i64, _i64, _i64, ctypes.c_double, _dp]
     lib.oracle_dequant.argtypes = [ctypes.POINTER(ctypes.c_uint8), _dp, _dp, _i64, _i64,
                                    ctypes.c_int, _i64, _dp]
+    lib.oracle_ce_reduced.argtypes = [_dp, _dp, _i64, _i64, _lp, _i64, _lp, _i64, _lp, _dp, _dp]
     for name in ("oracle_lora_u", "oracle_lora_y_rows", "oracle_lora_grad_u",
-                 "oracle_lora_dx_rows", "oracle_lora_da", "oracle_lora_db", "oracle_dequant"):
+                 "oracle_lora_dx_rows", "oracle_lora_da", "oracle_lora_db", "oracle_dequant",
+                 "oracle_ce_reduced"):
         getattr(lib, name).restype = None
     lib.oracle_threads.argtypes = []
     lib.oracle_threads.restype = ctypes.c_int
@@ -198,6 +202,35 @@ class Oracle:
         self.lib.oracle_dequant(Wq.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8)), _ptr(S),
                                 _ptr(Bo), N, K, bits, G, _ptr(W))
         return W
+
+    # --- reduced-vocabulary LM head with logits masking ---------------------------
+    @staticmethod
+    def reduced_vocab(table, k, targets, rows):
+        """J = union over the listed positions t of the first k entries of the
+        table row of the target y_t (sorted ascending), and the position of
+        each listed target in J."""
+        table = np.asarray(table)
+        targets = np.asarray(targets, dtype=np.int64)
+        rows = np.asarray(rows, dtype=np.int64)
+        J = np.unique(table[targets[rows], :k].reshape(-1)).astype(np.int64)
+        tpos = np.searchsorted(J, targets[rows]).astype(np.int64)
+        return J, tpos
+
+    def ce_reduced(self, H, W, rows, J, tpos):
+        """Per-position losses (for the listed rows) and dH (fp64 [T, D]) of the
+        reduced-vocabulary cross entropy; see oracle_ce_reduced."""
+        H, W = _f64(H), _f64(W)
+        T, D = H.shape
+        rows = np.ascontiguousarray(rows, dtype=np.int64)
+        J = np.ascontiguousarray(J, dtype=np.int64)
+        tpos = np.ascontiguousarray(tpos, dtype=np.int64)
+        assert W.shape[1] == D and rows.size == tpos.size
+        loss = np.empty(rows.size, dtype=np.float64)
+        dH = np.empty((T, D), dtype=np.float64)
+        self.lib.oracle_ce_reduced(_ptr(H), _ptr(W), T, D, rows.ctypes.data_as(_lp), rows.size,
+                                   J.ctypes.data_as(_lp), J.size, tpos.ctypes.data_as(_lp),
+                                   _ptr(loss), _ptr(dH))
+        return loss, dH
 
     def frozen_dx(self, dY, W, rows=None):
         """Rank-0 frozen linear input gradient dX = dY W."""

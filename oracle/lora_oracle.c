@@ -35,8 +35,10 @@
  * For a quantized frozen base the weight W is first reconstructed in fp64 by
  * oracle_dequant (below) and then used exactly as above.
  */
+#include <math.h>
 #include <stddef.h>
 #include <stdint.h>
+#include <stdlib.h>
 
 /* U[t][j] = sum_k X[t][k] * A[j][k]  (LoRA down-projection, saved for the
  * backward pass). */
@@ -170,6 +172,48 @@ void oracle_dequant(const uint8_t *Wq, const double *S, const double *Bo,
       const int64_t g = k / G;
       W[n * K + k] = S[n * ngroups + g] * (double)q + Bo[n * ngroups + g];
     }
+  }
+}
+
+/* Reduced-vocabulary cross entropy of the frozen LM head with logits masking
+ * (paper: "Softmax Approximation" -- logits over the rows J of the embedding
+ * matrix only; "Logits Masking" -- logits only for the trainable positions;
+ * the masked causal-LM loss sums -log p_t over those positions).
+ * For each listed position t = rows[i] (i < nrows):
+ *   z[j]    = sum_d H[t][d] * W[J[j]][d]                 j < nJ
+ *   lse     = m + log(sum_j exp(z[j] - m)),  m = max_j z[j]
+ *   loss[i] = lse - z[tpos[i]]        (tpos[i]: position of the target in J)
+ *   dH[t][d] = sum_j exp(z[j] - lse) * W[J[j]][d] - W[J[tpos[i]]][d]
+ * (the gradient of sum_i loss[i]); rows of dH not listed are set to zero.
+ * H [T, D], W [V, D] (only the rows in J are read), dH [T, D]. */
+void oracle_ce_reduced(const double *H, const double *W, int64_t T, int64_t D,
+                       const int64_t *rows, int64_t nrows, const int64_t *J,
+                       int64_t nJ, const int64_t *tpos, double *loss, double *dH) {
+  for (int64_t i = 0; i < T * D; ++i) dH[i] = 0.0;
+#pragma omp parallel for schedule(dynamic)
+  for (int64_t i = 0; i < nrows; ++i) {
+    const int64_t t = rows[i];
+    double *z = (double *)malloc(sizeof(double) * (size_t)nJ);
+    double m = -INFINITY;
+    for (int64_t j = 0; j < nJ; ++j) {
+      double acc = 0.0;
+      for (int64_t d = 0; d < D; ++d) acc += H[t * D + d] * W[J[j] * D + d];
+      z[j] = acc;
+      if (acc > m) m = acc;
+    }
+    double s = 0.0;
+    for (int64_t j = 0; j < nJ; ++j) s += exp(z[j] - m);
+    const double lse = m + log(s);
+    loss[i] = lse - z[tpos[i]];
+    double *out = dH + t * D;
+    for (int64_t j = 0; j < nJ; ++j) {
+      const double p = exp(z[j] - lse);
+      const double *w = W + J[j] * D;
+      for (int64_t d = 0; d < D; ++d) out[d] += p * w[d];
+    }
+    const double *wt = W + J[tpos[i]] * D;
+    for (int64_t d = 0; d < D; ++d) out[d] -= wt[d];
+    free(z);
   }
 }
 

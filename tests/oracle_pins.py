@@ -14,6 +14,10 @@ Dequantization" algorithm; tokens as rows):
     dA = s (dY B)^T X,          dB = s dY^T (X A^T).
 A quantized frozen base is dequantized first, as in that algorithm:
     W = s W_q + b, one scale s and offset b per group of G inputs of a row.
+The frozen LM head's reduced-vocabulary cross entropy with logits masking
+(its "Softmax Approximation" and "Logits Masking" sections):
+    loss_t = logsumexp_{j in J} h_t.w_j - h_t.w_{y_t} for trainable t,
+    J = union of the first k entries of the similarity-table rows of the targets.
 """
 from __future__ import annotations
 
@@ -293,13 +297,121 @@ def pin_dequant_groups(o):
     assert np.array_equal(o.dequant(ones8, S, np.zeros_like(Bo), 8, G), np.repeat(S, G, axis=1))
 
 
+# --- reduced-vocabulary LM head cross entropy with logits masking --------------
+def pin_ce_worked_example(o):
+    """Hand-worked: D = 1, vocabulary embeddings w = (1, 0, -1), hidden states
+    h = 1 (target token 0) and h = 2 (target token 2).  Position 1 has
+    logits (2, 0, -2): loss = log(e^2 + 1 + e^-2) + 2 and
+    dh = (e^2 - e^-2) / (e^2 + 1 + e^-2) + 1 (its target embedding is -1);
+    position 0 likewise with logits (1, 0, -1)."""
+    import math
+    H = np.array([[1.0], [2.0]])
+    W = np.array([[1.0], [0.0], [-1.0]])
+    loss, dH = o.ce_reduced(H, W, [0, 1], [0, 1, 2], [0, 2])
+    z0 = math.e + 1.0 + 1.0 / math.e
+    z1 = math.e ** 2 + 1.0 + math.e ** -2
+    assert abs(loss[0] - (math.log(z0) - 1.0)) < 1e-14
+    assert abs(loss[1] - (math.log(z1) + 2.0)) < 1e-14
+    assert abs(dH[0, 0] - ((math.e - 1.0 / math.e) / z0 - 1.0)) < 1e-14
+    assert abs(dH[1, 0] - ((math.e ** 2 - math.e ** -2) / z1 + 1.0)) < 1e-14
+
+
+def _torch_ce(H, W, cols, rows, targets_local):
+    """Cross entropy of the logits H[rows] W[cols]^T through torch (fp64) and
+    the gradient of its sum with respect to H."""
+    import torch
+    h = torch.tensor(H, dtype=torch.float64, requires_grad=True)
+    z = h[rows] @ torch.tensor(W, dtype=torch.float64)[cols].T
+    l = torch.nn.functional.cross_entropy(z, torch.tensor(targets_local), reduction="none")
+    l.sum().backward()
+    return l.detach().numpy(), h.grad.numpy()
+
+
+def pin_ce_full_vocab_is_torch_cross_entropy(o):
+    """J = the whole vocabulary and every position trainable: the ordinary
+    softmax cross entropy (torch) and its gradient."""
+    g = _rng(50)
+    T, V, D = 7, 23, 5
+    H, W = g.standard_normal((T, D)), g.standard_normal((V, D))
+    y = g.integers(0, V, size=T)
+    rows, J = np.arange(T), np.arange(V)
+    loss, dH = o.ce_reduced(H, W, rows, J, y)
+    l_t, g_t = _torch_ce(H, W, J, rows, y)
+    assert _relmax(loss, l_t) <= TIGHT
+    assert _relmax(dH, g_t) <= TIGHT
+
+
+def pin_ce_reduced_vocab_is_restricted_softmax(o):
+    """A reduced J: the cross entropy of the logits restricted to the columns J
+    with the target's position in J as the class (torch)."""
+    g = _rng(51)
+    T, V, D = 6, 40, 4
+    H, W = g.standard_normal((T, D)), g.standard_normal((V, D))
+    J = np.sort(g.choice(V, size=13, replace=False))
+    tpos = g.integers(0, J.size, size=T)
+    loss, dH = o.ce_reduced(H, W, np.arange(T), J, tpos)
+    l_t, g_t = _torch_ce(H, W, J, np.arange(T), tpos)
+    assert _relmax(loss, l_t) <= TIGHT
+    assert _relmax(dH, g_t) <= TIGHT
+
+
+def pin_ce_logits_masking_identity(o):
+    """Logits masking (only the trainable rows) gives the same per-position
+    losses and gradients as computing every row and masking the loss: the
+    listed rows match, the others have zero gradient."""
+    g = _rng(52)
+    T, V, D = 9, 30, 6
+    H, W = g.standard_normal((T, D)), g.standard_normal((V, D))
+    J = np.arange(0, V, 2)
+    tpos_all = g.integers(0, J.size, size=T)
+    l_all, d_all = o.ce_reduced(H, W, np.arange(T), J, tpos_all)
+    keep = np.array([1, 4, 5, 8])
+    l_m, d_m = o.ce_reduced(H, W, keep, J, tpos_all[keep])
+    assert np.array_equal(l_m, l_all[keep])
+    assert np.array_equal(d_m[keep], d_all[keep])
+    drop = np.setdiff1d(np.arange(T), keep)
+    assert not np.any(d_m[drop])
+
+
+def pin_ce_finite_differences(o):
+    """d(sum of losses)/dH by central differences (the loss is smooth)."""
+    g = _rng(53)
+    T, V, D = 3, 8, 3
+    H, W = g.standard_normal((T, D)), g.standard_normal((V, D))
+    J, tpos = np.array([0, 2, 3, 7]), np.array([1, 3, 0])
+    _, dH = o.ce_reduced(H, W, np.arange(T), J, tpos)
+    eps = 1e-6
+    for t in range(T):
+        for d in range(D):
+            Hp, Hm = H.copy(), H.copy()
+            Hp[t, d] += eps
+            Hm[t, d] -= eps
+            fd = (o.ce_reduced(Hp, W, np.arange(T), J, tpos)[0].sum()
+                  - o.ce_reduced(Hm, W, np.arange(T), J, tpos)[0].sum()) / (2 * eps)
+            assert abs(fd - dH[t, d]) <= 1e-7 * max(1.0, abs(dH[t, d]))
+
+
+def pin_reduced_vocab_union(o):
+    """J is the union of the first k entries of the targets' table rows; with
+    a table whose first entry of row i is i itself, J holds every target."""
+    table = np.array([[0, 5, 2], [1, 0, 4], [2, 3, 1], [3, 2, 6], [4, 1, 0], [5, 0, 6], [6, 3, 5]])
+    targets = np.array([3, 3, 5, 1, 6])
+    J, tpos = o.reduced_vocab(table, 2, targets, np.array([0, 2, 3]))
+    assert list(J) == [0, 1, 2, 3, 5]          # {3,2} | {5,0} | {1,0}
+    assert list(J[tpos]) == [3, 5, 1]
+    J1, _ = o.reduced_vocab(table, 1, targets, np.arange(5))
+    assert list(J1) == [1, 3, 5, 6]
+
+
 ALL_PINS = [
     pin_scalar_closed_form, pin_small_closed_form, pin_rank0_textbook_gemm,
     pin_down_projection_gemm, pin_finite_differences, pin_dense_identities,
     pin_zero_B, pin_zero_A, pin_zero_W, pin_linear_in_scale,
     pin_token_split_additivity, pin_row_permutation, pin_row_sampling,
     pin_torch_autograd, pin_dequant_worked_example, pin_dequant_unit_scale_is_the_codes,
-    pin_dequant_groups,
+    pin_dequant_groups, pin_ce_worked_example, pin_ce_full_vocab_is_torch_cross_entropy,
+    pin_ce_reduced_vocab_is_restricted_softmax, pin_ce_logits_masking_identity,
+    pin_ce_finite_differences, pin_reduced_vocab_union,
 ]
 
 

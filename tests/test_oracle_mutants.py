@@ -47,6 +47,15 @@ MUTANTS = [
     ("dq_8bit_as_nibble", "q = Wq[n * row_bytes + k];", "q = Wq[n * row_bytes + k] & 0x0F;"),
     ("dq_wrong_byte", "const uint8_t byte = Wq[n * row_bytes + k / 2];",
      "const uint8_t byte = Wq[n * row_bytes + k / 2 + (k / 2 + 1 < row_bytes)];"),
+    ("ce_target_gradient_dropped", "for (int64_t d = 0; d < D; ++d) out[d] -= wt[d];",
+     "for (int64_t d = 0; d < D; ++d) out[d] -= 0.0 * wt[d];"),
+    ("ce_wrong_target_logit", "loss[i] = lse - z[tpos[i]];", "loss[i] = lse - z[0];"),
+    ("ce_log_missing", "const double lse = m + log(s);", "const double lse = m + s;"),
+    ("ce_unnormalised_probability", "const double p = exp(z[j] - lse);", "const double p = exp(z[j] - m);"),
+    ("ce_ignores_J", "for (int64_t d = 0; d < D; ++d) acc += H[t * D + d] * W[J[j] * D + d];",
+     "for (int64_t d = 0; d < D; ++d) acc += H[t * D + d] * W[j * D + d];"),
+    ("ce_wrong_row_of_H", "for (int64_t d = 0; d < D; ++d) acc += H[t * D + d] * W[J[j] * D + d];",
+     "for (int64_t d = 0; d < D; ++d) acc += H[i * D + d] * W[J[j] * D + d];"),
 ]
 
 CHILD = textwrap.dedent("""
@@ -67,7 +76,7 @@ def test_pins_reject_mutant(tmp_path, mid, orig, mut):
     msrc = tmp_path / "mutant.c"
     msrc.write_text(src.replace(orig, mut))
     lib = tmp_path / "libmutant.so"
-    subprocess.run(["gcc", "-O2", "-fPIC", "-shared", "-std=c11", "-o", str(lib), str(msrc)],
+    subprocess.run(["gcc", "-O2", "-fPIC", "-shared", "-std=c11", "-o", str(lib), str(msrc), "-lm"],
                    check=True)
     code = CHILD.format(root=ROOT, tests=os.path.join(ROOT, "tests"), lib=str(lib))
     env = dict(os.environ, OMP_NUM_THREADS="1")
