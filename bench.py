@@ -25,7 +25,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 import paper_2606_19528_amd as lm  # noqa: E402
-from workloads import WORKLOADS, frozen_inputs, linear_seed, lora_inputs, quant_weight  # noqa: E402
+from workloads import (WORKLOADS, frozen_inputs, head_inputs, linear_seed, lora_inputs,  # noqa: E402
+                       quant_weight)
 
 METRIC = "LoRA linear fwd+bwd TFLOP/s (% bf16 MFMA peak) + peak device workspace bytes"
 PEAK_BF16_TFLOPS = 2516.6   # 256 CU x 4096 dense bf16 flop/clk x 2.4 GHz
@@ -168,6 +169,42 @@ def per_kernel_ms(fn, steps):
     return out
 
 
+def bench_lm_head(dev, steps=5, warmup=2, T=4096, V=128256, D=3072, k=1000, trainable=0.3):
+    """The frozen LM head of the 3B model at the paper's top-1000 / 30 %
+    trainable setting: reduced vocabulary J, then loss and dh over the
+    trainable positions only; beside it the full-vocabulary head over every
+    position (the same kernels with J = [0, V) and all rows), which is what
+    the reduction avoids."""
+    d = {k_: v.to(dev) for k_, v in head_inputs(T, V, D, k, trainable, seed=3).items()}
+    nrows = d["rows"].numel()
+    J, tpos = lm.lm_head_build_vocab(d["table"], k, d["targets"], d["rows"])
+    nJ = J.numel()
+    loss = torch.empty(T, dtype=torch.float32, device=dev)
+    total = torch.empty(1, dtype=torch.float32, device=dev)
+    dh = torch.empty(T, D, dtype=torch.bfloat16, device=dev)
+    ws = torch.empty(lm.lm_head_workspace_bytes(2, T, V, D, T, V), dtype=torch.uint8, device=dev)
+    wsv = torch.empty(lm.lm_head_workspace_bytes(0, T, V, D, nrows), dtype=torch.uint8, device=dev)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        lm.lm_head_build_vocab(d["table"], k, d["targets"], d["rows"], ws=wsv)
+    ms_vocab = (time.perf_counter() - t0) / steps * 1e3   # includes the wait for |J|
+    red = lambda: lm.lm_head_reduced_ce(d["h"], d["W"], d["rows"], J, tpos, loss[:nrows],  # noqa: E731
+                                        total, dh, 1.0, ws=ws)
+    ms_red = time_steps(red, steps, warmup)
+    allrows = torch.arange(T, dtype=torch.int32, device=dev)
+    Jall = torch.arange(V, dtype=torch.int32, device=dev)
+    tall = d["targets"]
+    full = lambda: lm.lm_head_reduced_ce(d["h"], d["W"], allrows, Jall, tall, loss, total, dh,  # noqa: E731
+                                         1.0, ws=ws)
+    ms_full = time_steps(full, 2, 1)
+    fl_red = 6.0 * nrows * nJ * D
+    return {"T": T, "V": V, "D": D, "k": k, "trainable_positions": nrows, "reduced_vocab": nJ,
+            "ms_build_vocab": round(ms_vocab, 4), "ms_loss_and_dh": round(ms_red, 4),
+            "tflops_loss_and_dh": round(fl_red / (ms_red * 1e-3) / 1e12, 2),
+            "ms_full_vocab_all_positions": round(ms_full, 4),
+            "tflops_full": round(6.0 * T * V * D / (ms_full * 1e-3) / 1e12, 2)}
+
+
 def kernel_flops(workload):
     """Algorithmic flops of one launch of each GEMM kernel, per linear shape."""
     T = workload.tokens
@@ -229,6 +266,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="llama_q_proj", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-head", action="store_true",
+                    help="skip the secondary measurement of the reduced-vocabulary LM head")
     ap.add_argument("--no-quant", action="store_true",
                     help="skip the secondary measurement with the quantized frozen base")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -330,6 +369,9 @@ def main():
             "unit": "TFLOP/s", "frozen_weight_bytes": int(wbytes),
             "kernels_ms_per_step": {k: round(v[0] / args.steps, 5) for k, v in pk.items()}}
         log(f"[bench] quantized base: {msq:.4f} ms/step")
+    if not args.no_head:
+        out["lm_head_reduced"] = bench_lm_head(dev)
+        log(f"[bench] lm head: {out['lm_head_reduced']}")
     if args.calib_copy_mib:
         n = args.calib_copy_mib * (1 << 20) // 4
         src = torch.ones(n, dtype=torch.float32, device=dev)

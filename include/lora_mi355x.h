@@ -148,6 +148,54 @@ lora_status_t frozen_linear_bwd_dx_q(const void *dy, const void *W_codes, const 
                                      int64_t T, int64_t d_in, int64_t d_out, void *ws,
                                      size_t ws_bytes, void *hip_stream);
 
+/* ---- Frozen LM head: reduced-vocabulary cross entropy with logits masking --
+ * The paper's "Softmax Approximation" computes the logits only over a reduced
+ * vocabulary J, the union of the first k entries of the similarity-table rows
+ * of the targets, and its "Logits Masking" only for the trainable positions;
+ * the masked causal-LM loss sums -log p_t over those positions.  With h
+ * [T, D] the final hidden states, W [V, D] the frozen output embedding (row v
+ * = token v), rows [nrows] the trainable positions (distinct) and y [T] the
+ * targets:
+ *   J          = sorted union over i of table[y[rows[i]]][0 .. k-1]
+ *   z_i[j]     = h[rows[i]] . W[J[j]]                     (never stored)
+ *   loss[i]    = logsumexp_j z_i[j] - z_i[tpos[i]],  tpos[i] = position of
+ *                y[rows[i]] in J
+ *   dh[rows[i]] = dscale (sum_j softmax(z_i)[j] W[J[j]] - W[y[rows[i]]]),
+ *   dh[t] = 0 for positions t not listed.  W is frozen (no weight gradient).
+ * The logits are reduced tile by tile to row maxima and sums of exponentials
+ * inside the GEMM; the backward recomputes them in chunks of 8192 columns of
+ * J, so neither the logits nor their gradient is ever held in full.
+ *
+ * Integer arrays are int32 device arrays.  Workspace sizes:
+ * lm_head_workspace_bytes(op, T, V, D, nrows, nJ) with op LM_HEAD_OP_VOCAB
+ * (for lm_head_build_vocab; nJ ignored), LM_HEAD_OP_LOSS (loss only) or
+ * LM_HEAD_OP_LOSS_DH; (size_t)-1 for sizes the calls would reject. */
+typedef enum { LM_HEAD_OP_VOCAB = 0, LM_HEAD_OP_LOSS = 1, LM_HEAD_OP_LOSS_DH = 2 } lm_head_op_t;
+size_t lm_head_workspace_bytes(int op, int64_t T, int64_t V, int64_t D, int64_t nrows,
+                               int64_t nJ);
+
+/* J [V] (capacity) and tpos [nrows] from the similarity table [V, ldtab]
+ * (its first k columns are used; row v should start with v itself, which
+ * puts every target in J), the targets y [T] and the trainable positions
+ * rows [nrows].  *nJ (host) receives |J|: this call waits for its stream to
+ * finish.  Entries outside their ranges are skipped and give tpos = -1 (the
+ * loss of such a position is NaN).  Errors: LORA_EINVAL for NULL or
+ * misaligned pointers, bad sizes or overlapping outputs, LORA_EWORKSPACE. */
+lora_status_t lm_head_build_vocab(const int32_t *table, int64_t V, int64_t ldtab, int64_t k,
+                                  const int32_t *targets, int64_t T, const int32_t *rows,
+                                  int64_t nrows, int32_t *J, int32_t *tpos, int64_t *nJ, void *ws,
+                                  size_t ws_bytes, void *hip_stream);
+
+/* loss_rows [nrows] fp32 per trainable position, loss_total (optional, one
+ * fp32) their sum, and, when dh (bf16 [T, D]) is not NULL, the gradient of
+ * dscale * sum(loss_rows) with respect to h.  h, W bf16; D a multiple of 8.
+ * Errors as above, plus LORA_EUNSUPPORTED for D. */
+lora_status_t lm_head_reduced_ce(const void *h, const void *W, int64_t T, int64_t V, int64_t D,
+                                 const int32_t *rows, int64_t nrows, const int32_t *J, int64_t nJ,
+                                 const int32_t *tpos, float *loss_rows, float *loss_total,
+                                 void *dh, float dscale, void *ws, size_t ws_bytes,
+                                 void *hip_stream);
+
 /* Static text for a status code. */
 const char *lora_status_str(lora_status_t status);
 

@@ -3,6 +3,7 @@
 // enqueued; the library allocates no device memory.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -33,11 +34,17 @@ enum KernelId {
   K_GEMM_FWD_Q,       // gemm_fwd with the quantized W dequantized on the fly
   K_GEMM_BWD_DX_Q,    // gemm_bwd_dx, quantized W
   K_GEMM_FROZEN_DX_Q, // gemm_frozen_dx, quantized W
+  K_HEAD_VOCAB,       // reduced vocabulary (mark, compact, target positions)
+  K_HEAD_GATHER,      // gathers of the trainable hidden rows and of the rows of J
+  K_HEAD_LOGITS,      // logits GEMM with the row-statistics epilogue (+ combine)
+  K_HEAD_DZ,          // logits recomputed, softmax gradient epilogue
+  K_HEAD_DH,          // dh += dz W_J (fp32), then the bf16 dh rows
   K_COUNT
 };
 const char *kKernelNames[K_COUNT] = {"gemm_fwd",   "gemm_bwd_dx",   "gemm_frozen_dx",
                                      "lora_down",  "lora_dy_b",     "gemm_fwd_q",
-                                     "gemm_bwd_dx_q", "gemm_frozen_dx_q"};
+                                     "gemm_bwd_dx_q", "gemm_frozen_dx_q", "head_vocab",
+                                     "head_gather", "head_logits", "head_dz", "head_dh"};
 
 struct EventPair {
   hipEvent_t a, b;
@@ -156,6 +163,56 @@ BwdLayout bwd_layout(int64_t T, int64_t K, int64_t N, int64_t r, lora_dtype_t dt
   off += round256((size_t)T * L.ldt * esize(dt));
   L.acat = off;  // [nsplit * r][K]: A repeated once per partial
   off += L.sp_du.nsplit > 1 ? round256((size_t)L.sp_du.nsplit * r * K * esize(dt)) : 0;
+  L.total = off;
+  return L;
+}
+
+// LM head workspaces.
+constexpr int64_t kHeadChunk = 8192;  // vocabulary columns per backward chunk (multiple of 128)
+struct VocabLayout {
+  size_t mark, pos_of, count, total;
+};
+VocabLayout vocab_layout(int64_t V) {
+  VocabLayout L{};
+  size_t off = 0;
+  L.mark = off;
+  off += round256((size_t)V * 4);
+  L.pos_of = off;
+  off += round256((size_t)V * 4);
+  L.count = off;
+  off += 256;
+  L.total = off;
+  return L;
+}
+struct CeLayout {
+  size_t hT, WJ, tmax, tsum, ztgt, lse, dz, dhacc, inv, total;
+  int64_t tiles;
+};
+CeLayout ce_layout(int64_t T, int64_t D, int64_t nrows, int64_t nJ, bool want_dh) {
+  CeLayout L{};
+  L.tiles = (nJ + 127) / 128;
+  size_t off = 0;
+  L.hT = off;
+  off += round256((size_t)nrows * D * 2);
+  L.WJ = off;
+  off += round256((size_t)nJ * D * 2);
+  L.tmax = off;
+  off += round256((size_t)L.tiles * nrows * 4);
+  L.tsum = off;
+  off += round256((size_t)L.tiles * nrows * 4);
+  L.ztgt = off;
+  off += round256((size_t)nrows * 4);
+  L.lse = off;
+  off += round256((size_t)nrows * 4);
+  if (want_dh) {
+    const int64_t ch = nJ < kHeadChunk ? (nJ + 7) / 8 * 8 : kHeadChunk;
+    L.dz = off;
+    off += round256((size_t)nrows * ch * 2);
+    L.dhacc = off;
+    off += round256((size_t)nrows * D * 4);
+    L.inv = off;
+    off += round256((size_t)T * 4);
+  }
   L.total = off;
   return L;
 }
@@ -511,6 +568,147 @@ lora_status_t frozen_linear_bwd_dx_q(const void *dy, const void *W_codes, const 
   if (!W_codes) return fail(LORA_EINVAL, "codes, scale and offset are required");
   return frozen_impl(dy, nullptr, W_codes, W_scale, W_offset, bits, group, dx, T, d_in, d_out,
                      LORA_BF16, hip_stream);
+}
+
+size_t lm_head_workspace_bytes(int op, int64_t T, int64_t V, int64_t D, int64_t nrows,
+                               int64_t nJ) {
+  if (T < 1 || V < 1 || D < 8 || D % 8 || nrows < 1 || nrows > T || V > kMaxElems || D > kMaxDim ||
+      T > kMaxElems / D || V > kMaxElems / D)
+    return (size_t)-1;
+  if (op == LM_HEAD_OP_VOCAB) return vocab_layout(V).total;
+  if (nJ < 1 || nJ > V) return (size_t)-1;
+  if (op == LM_HEAD_OP_LOSS) return ce_layout(T, D, nrows, nJ, false).total;
+  if (op == LM_HEAD_OP_LOSS_DH) return ce_layout(T, D, nrows, nJ, true).total;
+  return (size_t)-1;
+}
+
+lora_status_t lm_head_build_vocab(const int32_t *table, int64_t V, int64_t ldtab, int64_t k,
+                                  const int32_t *targets, int64_t T, const int32_t *rows,
+                                  int64_t nrows, int32_t *J, int32_t *tpos, int64_t *nJ, void *ws,
+                                  size_t ws_bytes, void *hip_stream) {
+  if (!table || !targets || !rows || !J || !tpos || !nJ)
+    return fail(LORA_EINVAL, "table, targets, rows, J, tpos and nJ are required");
+  if (V < 1 || V > kMaxElems || T < 1 || T > kMaxElems || nrows < 1 || nrows > T)
+    return fail(LORA_EINVAL, "need V >= 1, T >= 1 and 1 <= nrows <= T");
+  if (k < 1 || k > ldtab || ldtab > kMaxElems / V || (int64_t)nrows * k > kMaxElems)
+    return fail(LORA_EINVAL, "need 1 <= k <= ldtab and a table below 2^31 entries");
+  const void *ptrs[] = {table, targets, rows, J, tpos};
+  for (const void *p : ptrs)
+    if (!aligned16(p)) return fail(LORA_EINVAL, "pointers must be 16-byte aligned");
+  const VocabLayout L = vocab_layout(V);
+  lora_status_t s;
+  if ((s = check_ws(ws, ws_bytes, L.total)) != LORA_OK) return s;
+  std::vector<Range> ins = {rng(table, V * ldtab * 4), rng(targets, T * 4), rng(rows, nrows * 4)};
+  std::vector<Range> outs = {rng(J, V * 4), rng(tpos, nrows * 4), rng(ws, (int64_t)L.total)};
+  if (any_overlap(outs, ins)) return fail(LORA_EINVAL, "an output overlaps an input or another output");
+  hipStream_t st = (hipStream_t)hip_stream;
+  char *wsb = (char *)ws;
+  HeadVocabArgs a{};
+  a.table = table; a.ldtab = ldtab; a.k = (int)k; a.V = (int)V; a.T = (int)T;
+  a.targets = targets; a.rows = rows; a.nrows = (int)nrows;
+  a.mark = (uint32_t *)(wsb + L.mark); a.J = J; a.pos_of = (int32_t *)(wsb + L.pos_of);
+  a.tpos = tpos; a.count = (int32_t *)(wsb + L.count);
+  Timed t(K_HEAD_VOCAB, st);
+  hipError_t e = launch_vocab_build(a, st);
+  t.done();
+  if (e != hipSuccess) return hip_fail(e, "head_vocab launch");
+  int32_t count = 0;
+  if ((e = hipMemcpyAsync(&count, a.count, 4, hipMemcpyDeviceToHost, st)) != hipSuccess)
+    return hip_fail(e, "reading |J|");
+  if ((e = hipStreamSynchronize(st)) != hipSuccess) return hip_fail(e, "reading |J|");
+  *nJ = count;
+  return LORA_OK;
+}
+
+lora_status_t lm_head_reduced_ce(const void *h, const void *W, int64_t T, int64_t V, int64_t D,
+                                 const int32_t *rows, int64_t nrows, const int32_t *J, int64_t nJ,
+                                 const int32_t *tpos, float *loss_rows, float *loss_total,
+                                 void *dh, float dscale, void *ws, size_t ws_bytes,
+                                 void *hip_stream) {
+  if (!h || !W || !rows || !J || !tpos || !loss_rows)
+    return fail(LORA_EINVAL, "h, W, rows, J, tpos and loss_rows are required");
+  if (T < 1 || V < 1 || nrows < 1 || nrows > T || nJ < 1 || nJ > V)
+    return fail(LORA_EINVAL, "need 1 <= nrows <= T and 1 <= nJ <= V");
+  if (D < 8 || D % 8) return fail(LORA_EUNSUPPORTED, "D must be a positive multiple of 8");
+  if (D > kMaxDim || T > kMaxElems / D || V > kMaxElems / D)
+    return fail(LORA_EUNSUPPORTED, "D at most 2^20 and h, W below 2^31 elements");
+  if (dh && !std::isfinite(dscale)) return fail(LORA_EINVAL, "dscale must be finite");
+  const void *ptrs[] = {h, W, rows, J, tpos, loss_rows, loss_total, dh};
+  for (const void *p : ptrs)
+    if (p && !aligned16(p)) return fail(LORA_EINVAL, "pointers must be 16-byte aligned");
+  const CeLayout L = ce_layout(T, D, nrows, nJ, dh != nullptr);
+  lora_status_t s;
+  if ((s = check_ws(ws, ws_bytes, L.total)) != LORA_OK) return s;
+  std::vector<Range> ins = {rng(h, T * D * 2), rng(W, V * D * 2), rng(rows, nrows * 4),
+                            rng(J, nJ * 4), rng(tpos, nrows * 4)};
+  std::vector<Range> outs = {rng(loss_rows, nrows * 4), rng(ws, (int64_t)L.total)};
+  if (loss_total) outs.push_back(rng(loss_total, 4));
+  if (dh) outs.push_back(rng(dh, T * D * 2));
+  if (any_overlap(outs, ins)) return fail(LORA_EINVAL, "an output overlaps an input or another output");
+
+  hipStream_t st = (hipStream_t)hip_stream;
+  char *wsb = (char *)ws;
+  void *hT = wsb + L.hT, *WJ = wsb + L.WJ;
+  float *tmax = (float *)(wsb + L.tmax), *tsum = (float *)(wsb + L.tsum);
+  float *ztgt = (float *)(wsb + L.ztgt), *lse = (float *)(wsb + L.lse);
+  hipError_t e;
+  {
+    Timed t(K_HEAD_GATHER, st);
+    e = launch_gather_rows(h, D, (int)T, rows, (int)nrows, (int)D, hT, st);
+    if (e == hipSuccess) e = launch_gather_rows(W, D, (int)V, J, (int)nJ, (int)D, WJ, st);
+    t.done();
+    if (e != hipSuccess) return hip_fail(e, "head_gather launch");
+  }
+  // logits z = h_T W_J^T, never stored: per-tile row max / sum of exp, target logit
+  GemmArgs g{};
+  g.A = hT; g.lda = D;
+  g.B = WJ; g.ldb = D;
+  g.M = (int)nrows; g.N = (int)nJ; g.K = (int)D;
+  g.tpos = tpos; g.col0 = 0;
+  g.ce_max = tmax; g.ce_sum = tsum; g.ce_tgt = ztgt;
+  {
+    Timed t(K_HEAD_LOGITS, st);
+    e = launch_fill_nan(ztgt, nrows, st);  // a target outside J leaves its loss NaN
+    if (e == hipSuccess) e = launch_gemm_epi(g, EPI_CE_STATS, st);
+    if (e == hipSuccess)
+      e = launch_ce_combine(tmax, tsum, (int)L.tiles, (int)nrows, ztgt, lse, loss_rows, loss_total, st);
+    t.done();
+    if (e != hipSuccess) return hip_fail(e, "head_logits launch");
+  }
+  if (!dh) return LORA_OK;
+  // dh_T = sum over chunks of the vocabulary of dz_chunk W_J[chunk], with
+  // dz = dscale (softmax - one-hot(target)) recomputed per chunk.
+  const int64_t ch = nJ < kHeadChunk ? (nJ + 7) / 8 * 8 : kHeadChunk;
+  float *dhacc = (float *)(wsb + L.dhacc);
+  for (int64_t c0 = 0; c0 < nJ; c0 += ch) {
+    const int64_t w = std::min<int64_t>(ch, nJ - c0);
+    const int64_t ldz = (w + 7) / 8 * 8;
+    GemmArgs z{};
+    z.A = hT; z.lda = D;
+    z.B = (const char *)WJ + c0 * D * 2; z.ldb = D;
+    z.M = (int)nrows; z.N = (int)w; z.K = (int)D;
+    z.C = wsb + L.dz; z.ldc = ldz;
+    z.tpos = tpos; z.col0 = (int)c0; z.lse = lse; z.dscale = dscale;
+    {
+      Timed t(K_HEAD_DZ, st);
+      e = launch_gemm_epi(z, EPI_CE_DZ, st);
+      t.done();
+      if (e != hipSuccess) return hip_fail(e, "head_dz launch");
+    }
+    GemmArgs d{};
+    d.A = wsb + L.dz; d.lda = ldz;
+    d.B = (const char *)WJ + c0 * D * 2; d.ldb = D;
+    d.M = (int)nrows; d.N = (int)D; d.K = (int)w;
+    d.C = dhacc; d.ldc = D; d.c_accumulate = c0 > 0;
+    Timed t(K_HEAD_DH, st);
+    e = launch_gemm_epi(d, EPI_F32, st);
+    t.done();
+    if (e != hipSuccess) return hip_fail(e, "head_dh launch");
+  }
+  Timed t(K_HEAD_DH, st);
+  e = launch_dh_finish(dhacc, rows, (int)nrows, (int32_t *)(wsb + L.inv), (int)T, (int)D, dh, st);
+  t.done();
+  return e == hipSuccess ? LORA_OK : hip_fail(e, "head_dh launch");
 }
 
 const char *lora_status_str(lora_status_t status) {

@@ -54,7 +54,7 @@ __device__ __forceinline__ void static_for(F &&f) {
 }
 
 template <class E, int BM, int BN, int WM, int WN, int WK, int BMODE, int BKB, int NBUF, int RD, int FS,
-          int QB = 0>
+          int QB = 0, int EPI = EPI_STORE>
 __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int group_m,
                                                                  SideArgs side, int nside) {
   typedef typename E::T T;
@@ -95,6 +95,9 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   // consecutive weights of a W row per stage.
   constexpr int QPIECES = BMODE == B_ROW ? BN * (BKE / 16) : BKE * (BN / 16);
   static_assert(QB == 0 || QB == 4 || QB == 8, "code width");
+  static_assert(EPI == EPI_STORE || (ES == 2 && FS), "cross-entropy / fp32 epilogues: bf16 kernels");
+  static_assert(EPI != EPI_CE_STATS || (NT == 4 * BM && BM * (BN + 1) * 4 <= LDS),
+                "row statistics: four threads per tile row, the fp32 tile in LDS");
   static_assert(QB == 0 || (ES == 2 && FS && BMODE != B_KMAJ_REG && QPIECES == NT),
                 "quantized B: bf16, staged fragments, one 16-weight piece per thread");
 
@@ -696,6 +699,98 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   }
 
   // ---- epilogue: lane holds D[n][m] at m = lane % 32, n = 8q + 4(lane / 32) + e
+  if constexpr (EPI == EPI_CE_STATS) {
+    // Row statistics of this tile of logits: max and sum of exp over its valid
+    // columns, and the target's logit when the target column lies in the tile.
+    // The fp32 tile goes through LDS; four threads share a row and combine
+    // their partial max and sum in a fixed order.
+    __syncthreads();
+    float *zt = (float *)smem;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      if (WK > 1 && b % WK != wk) continue;
+      const int i = b / FN, j = b % FN;
+      const int row = wm * WTM + i * 32 + lrow;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          zt[row * (BN + 1) + wn * WTN + j * 32 + 8 * q + 4 * (lane >> 5) + e] = acc[i][j][4 * q + e];
+    }
+    __syncthreads();
+    const int row = tid >> 2, sub = tid & 3;
+    constexpr int CPT = BN / 4;  // columns per thread
+    const int ncol = min(BN, g.N - n0);
+    const float *zr = zt + row * (BN + 1);
+    float mx = -INFINITY;
+    for (int c = sub * CPT; c < min(ncol, (sub + 1) * CPT); ++c) mx = fmaxf(mx, zr[c]);
+    mx = fmaxf(mx, __shfl_xor(mx, 1));
+    mx = fmaxf(mx, __shfl_xor(mx, 2));
+    float sm = 0.0f;
+    for (int c = sub * CPT; c < min(ncol, (sub + 1) * CPT); ++c) sm += __expf(zr[c] - mx);
+    sm += __shfl_xor(sm, 1);
+    sm += __shfl_xor(sm, 2);
+    const int m = m0 + row;
+    if (sub == 0 && m < g.M) {
+      g.ce_max[(int64_t)nt * g.M + m] = mx;
+      g.ce_sum[(int64_t)nt * g.M + m] = sm;
+      const int tp = g.tpos[m] - g.col0 - n0;
+      if (tp >= 0 && tp < ncol) g.ce_tgt[m] = zr[tp];
+    }
+    return;
+  }
+  if constexpr (EPI == EPI_CE_DZ) {
+    // dz = dscale * (exp(z - lse[m]) - [column is the target]), bf16; columns
+    // from N up to the padded row length ldc are written as zeros.
+    T *C = (T *)g.C;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      if (WK > 1 && b % WK != wk) continue;
+      const int i = b / FN, j = b % FN;
+      const int m = m0 + wm * WTM + i * 32 + lrow;
+      if (m >= g.M) continue;
+      const float l = g.lse[m];
+      const int tp = g.tpos[m] - g.col0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int n = n0 + wn * WTN + j * 32 + 8 * q + 4 * (lane >> 5);
+        if (n < g.ldc) {
+          float v[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            v[e] = n + e < g.N ? g.dscale * (__expf(acc[i][j][4 * q + e] - l) - (n + e == tp ? 1.0f : 0.0f))
+                               : 0.0f;
+          const uint32_t lo = (uint32_t)E::from_float(v[0]) | ((uint32_t)E::from_float(v[1]) << 16);
+          const uint32_t hi = (uint32_t)E::from_float(v[2]) | ((uint32_t)E::from_float(v[3]) << 16);
+          *(uint2 *)((T *)g.C + (int64_t)m * g.ldc + n) = make_uint2(lo, hi);
+        }
+      }
+    }
+    (void)C;
+    return;
+  }
+  if constexpr (EPI == EPI_F32) {
+    // fp32 output, overwritten or (c_accumulate) added to.
+    float *C = (float *)g.C;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      if (WK > 1 && b % WK != wk) continue;
+      const int i = b / FN, j = b % FN;
+      const int m = m0 + wm * WTM + i * 32 + lrow;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int n = n0 + wn * WTN + j * 32 + 8 * q + 4 * (lane >> 5);
+        if (m < g.M && n < g.N) {
+          f32x4 *dst = (f32x4 *)(C + (int64_t)m * g.ldc + n);
+          f32x4 v = f32x4{acc[i][j][4 * q + 0], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                          acc[i][j][4 * q + 3]};
+          if (g.c_accumulate) v += *dst;
+          *dst = v;
+        }
+      }
+    }
+    return;
+  }
   T *C = (T *)g.C;
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
@@ -734,7 +829,7 @@ static int pick_group_m(int tiles_m, int tiles_n, int BM, int BN) {
 }
 
 template <class E, int BM, int BN, int WM, int WN, int WK, int BMODE, int BKB, int NBUF, int RD, int FS,
-          int QB = 0>
+          int QB = 0, int EPI = EPI_STORE>
 static hipError_t launch_cfg(const GemmArgs &g, const SideArgs *side, hipStream_t st) {
   const int tm = g.M > 0 ? (g.M + BM - 1) / BM : 0, tn = (g.N + BN - 1) / BN;
   SideArgs sa{};
@@ -745,7 +840,7 @@ static hipError_t launch_cfg(const GemmArgs &g, const SideArgs *side, hipStream_
   }
   const int grid = tm * tn + nside;
   if (grid == 0) return hipSuccess;
-  hipLaunchKernelGGL((gemm_kernel<E, BM, BN, WM, WN, WK, BMODE, BKB, NBUF, RD, FS, QB>), dim3(grid),
+  hipLaunchKernelGGL((gemm_kernel<E, BM, BN, WM, WN, WK, BMODE, BKB, NBUF, RD, FS, QB, EPI>), dim3(grid),
                      dim3(64 * WM * WN * WK), 0, st, g, tm > 0 ? pick_group_m(tm, tn, BM, BN) : 1,
                      sa, nside);
   return hipGetLastError();
@@ -769,6 +864,18 @@ static int pick_shape(int M, int N) {
   const double c0 = cost(128, 128, 0.80), c1 = cost(256, 128, 0.87), c2 = cost(256, 256, 1.0);
   if (c2 <= c1 && c2 <= c0) return 2;
   return c1 < c0 ? 1 : 0;
+}
+
+hipError_t launch_gemm_epi(const GemmArgs &g, int epi, hipStream_t st) {
+  switch (epi) {
+    case EPI_CE_STATS:
+      return launch_cfg<BF16, 128, 128, 2, 2, 2, B_ROW, 128, 2, 3, 2, 0, EPI_CE_STATS>(g, nullptr, st);
+    case EPI_CE_DZ:
+      return launch_cfg<BF16, 128, 128, 2, 2, 2, B_ROW, 128, 2, 3, 2, 0, EPI_CE_DZ>(g, nullptr, st);
+    case EPI_F32:
+      return launch_cfg<BF16, 128, 128, 2, 2, 2, B_KMAJ_TR, 128, 2, 3, 2, 0, EPI_F32>(g, nullptr, st);
+  }
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_gemm_q(const GemmArgs &g, int bits, bool b_kmajor, const SideArgs *side,

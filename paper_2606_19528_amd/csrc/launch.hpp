@@ -68,7 +68,55 @@ struct GemmArgs {
   const float *qscale;
   const float *qoffset;
   int qlog2g;
+  // Cross-entropy epilogues (launch_gemm_epi); this GEMM's output column n is
+  // column col0 + n of the reduced vocabulary, tpos[m] the target's column.
+  const int32_t *tpos;
+  int col0;
+  float *ce_max, *ce_sum, *ce_tgt;  // EPI_CE_STATS: [tiles_n][M], [tiles_n][M], [M]
+  const float *lse;                 // EPI_CE_DZ
+  float dscale;
+  int c_accumulate;                 // EPI_F32: C fp32 += product instead of =
 };
+
+// Epilogues of launch_gemm_epi (bf16 operands, 128 x 128 tiles):
+//   EPI_CE_STATS  no C; per row and 128-column tile t of logits z:
+//                 ce_max[t][m] = max_n z, ce_sum[t][m] = sum_n exp(z - max),
+//                 ce_tgt[m] = z at the target column (B row-major);
+//   EPI_CE_DZ     C bf16 [M][ldc] = dscale (exp(z - lse[m]) - [n is the
+//                 target]) for n < N, 0 for N <= n < ldc (B row-major);
+//   EPI_F32       C fp32 [M][ldc] (+)= A B (B k-major).
+enum { EPI_STORE = 0, EPI_CE_STATS = 1, EPI_CE_DZ = 2, EPI_F32 = 3 };
+hipError_t launch_gemm_epi(const GemmArgs &g, int epi, hipStream_t st);
+
+// Reduced vocabulary: J = sorted union over i < nrows of
+// table[targets[rows[i]]][0 .. k-1]; pos_of[v] = position of v in J;
+// tpos[i] = position of targets[rows[i]]; count[0] = |J| (device).
+// mark: V words of scratch.  Indices outside their range (rows[i] not in
+// [0, T), a target or table entry not in [0, V)) are skipped (tpos -1).
+struct HeadVocabArgs {
+  const int32_t *table;
+  int64_t ldtab;
+  int k, V, T;
+  const int32_t *targets, *rows;
+  int nrows;
+  uint32_t *mark;
+  int32_t *J, *pos_of, *tpos, *count;
+};
+hipError_t launch_vocab_build(const HeadVocabArgs &a, hipStream_t st);
+// dst[i] = src[idx[i]] (bf16 rows of `cols`, a multiple of 8), i < n; zero
+// rows for indices outside [0, nsrc).
+hipError_t launch_gather_rows(const void *src, int64_t ld, int nsrc, const int32_t *idx, int n,
+                              int cols, void *dst, hipStream_t st);
+// lse / loss per row from the EPI_CE_STATS partials; total = sum of losses
+// (if not NULL), all in a fixed order.
+hipError_t launch_ce_combine(const float *tmax, const float *tsum, int ntiles, int M,
+                             const float *ztgt, float *lse, float *loss, float *total,
+                             hipStream_t st);
+// p[0 .. n) = quiet NaN.
+hipError_t launch_fill_nan(float *p, int64_t n, hipStream_t st);
+// dh [T][D] bf16: row rows[i] = acc[i], every other row 0 (inv: T words scratch).
+hipError_t launch_dh_finish(const float *acc, const int32_t *rows, int nrows, int32_t *inv, int T,
+                            int D, void *dh, hipStream_t st);
 
 // GEMM launch; `side` (may be NULL) adds the token-reduction workgroups.
 hipError_t launch_gemm(const GemmArgs &g, Dtype dt, bool b_kmajor, const SideArgs *side,

@@ -54,6 +54,14 @@ def lib() -> ctypes.CDLL:
     L.lora_linear_bwd_q.restype = i32
     L.frozen_linear_bwd_dx_q.argtypes = [vp, vp, vp, vp, i32, i64, vp, i64, i64, i64, vp, sz, vp]
     L.frozen_linear_bwd_dx_q.restype = i32
+    L.lm_head_workspace_bytes.argtypes = [i32, i64, i64, i64, i64, i64]
+    L.lm_head_workspace_bytes.restype = sz
+    L.lm_head_build_vocab.argtypes = [vp, i64, i64, i64, vp, i64, vp, i64, vp, vp,
+                                      ctypes.POINTER(i64), vp, sz, vp]
+    L.lm_head_build_vocab.restype = i32
+    L.lm_head_reduced_ce.argtypes = [vp, vp, i64, i64, i64, vp, i64, vp, i64, vp, vp, vp, vp, f32,
+                                     vp, sz, vp]
+    L.lm_head_reduced_ce.restype = i32
     L.lora_status_str.argtypes = [i32]
     L.lora_status_str.restype = ctypes.c_char_p
     L.lora_last_error.argtypes = []
@@ -209,6 +217,51 @@ def frozen_linear_bwd_dx_q(dy, Wq, dx, ws=None, stream=None):
                                       _stream(stream))
     _check(st, "frozen_linear_bwd_dx_q")
     return dx
+
+
+# --- frozen LM head: reduced-vocabulary cross entropy with logits masking -----------
+LM_HEAD_OP_VOCAB, LM_HEAD_OP_LOSS, LM_HEAD_OP_LOSS_DH = 0, 1, 2
+
+
+def lm_head_workspace_bytes(op: int, T: int, V: int, D: int, nrows: int, nJ: int = 1) -> int:
+    n = lib().lm_head_workspace_bytes(op, T, V, D, nrows, nJ)
+    if n == ctypes.c_size_t(-1).value:
+        raise LoraError(LORA_EINVAL, "lm_head_workspace_bytes", "sizes rejected")
+    return int(n)
+
+
+def lm_head_build_vocab(table, k: int, targets, rows, ws=None, stream=None):
+    """(J [nJ] int32, tpos [nrows] int32) on the device; waits for the stream."""
+    import torch
+
+    V, ldtab = table.shape
+    T = targets.shape[0]
+    nrows = rows.shape[0]
+    J = torch.empty(V, dtype=torch.int32, device=table.device)
+    tpos = torch.empty(nrows, dtype=torch.int32, device=table.device)
+    ws, ws_bytes = _ws(ws, lm_head_workspace_bytes(LM_HEAD_OP_VOCAB, T, V, 8, nrows), table)
+    nJ = ctypes.c_int64(0)
+    st = lib().lm_head_build_vocab(_ptr(table), V, ldtab, k, _ptr(targets), T, _ptr(rows), nrows,
+                                   _ptr(J), _ptr(tpos), ctypes.byref(nJ), _ptr(ws), ws_bytes,
+                                   _stream(stream))
+    _check(st, "lm_head_build_vocab")
+    return J[: nJ.value], tpos
+
+
+def lm_head_reduced_ce(h, W, rows, J, tpos, loss_rows, loss_total=None, dh=None,
+                       dscale: float = 1.0, ws=None, stream=None):
+    """Per-position losses (and their sum, and dh) of the reduced-vocabulary
+    cross entropy over the trainable positions `rows`."""
+    T, D = h.shape
+    V = W.shape[0]
+    nrows, nJ = rows.shape[0], J.shape[0]
+    op = LM_HEAD_OP_LOSS if dh is None else LM_HEAD_OP_LOSS_DH
+    ws, ws_bytes = _ws(ws, lm_head_workspace_bytes(op, T, V, D, nrows, nJ), h)
+    st = lib().lm_head_reduced_ce(_ptr(h), _ptr(W), T, V, D, _ptr(rows), nrows, _ptr(J), nJ,
+                                  _ptr(tpos), _ptr(loss_rows), _ptr(loss_total), _ptr(dh),
+                                  float(dscale), _ptr(ws), ws_bytes, _stream(stream))
+    _check(st, "lm_head_reduced_ce")
+    return loss_rows
 
 
 # --- kernel timing hook (benchmarks) -----------------------------------------------

@@ -208,6 +208,59 @@ def test_frozen_q_rejects(kw, code):
     assert frozen_q(**kw) == code
 
 
+def vocab(**kw):
+    a = dict(table=P(1), V=1000, ldtab=16, k=8, targets=P(2), T=64, rows=P(3), nrows=20, J=P(4),
+             tpos=P(5), nJ=ctypes.byref(ctypes.c_int64(0)), ws=P(6), wsb=1 << 24)
+    a.update(kw)
+    return lm.lib().lm_head_build_vocab(a["table"], a["V"], a["ldtab"], a["k"], a["targets"], a["T"],
+                                        a["rows"], a["nrows"], a["J"], a["tpos"], a["nJ"], a["ws"],
+                                        a["wsb"], None)
+
+
+def head_ce(**kw):
+    a = dict(h=P(1), W=P(2), T=64, V=1000, D=256, rows=P(3), nrows=20, J=P(4), nJ=300, tpos=P(5),
+             loss=P(6), total=P(7), dh=P(8), dscale=1.0, ws=P(9), wsb=1 << 28)
+    a.update(kw)
+    return lm.lib().lm_head_reduced_ce(a["h"], a["W"], a["T"], a["V"], a["D"], a["rows"], a["nrows"],
+                                       a["J"], a["nJ"], a["tpos"], a["loss"], a["total"], a["dh"],
+                                       a["dscale"], a["ws"], a["wsb"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(table=None), EINVAL), (dict(nJ=None), EINVAL), (dict(k=0), EINVAL), (dict(k=17), EINVAL),
+    (dict(nrows=65), EINVAL), (dict(V=0), EINVAL), (dict(rows=misaligned(3)), EINVAL),
+    (dict(wsb=100), EWS), (dict(J=P(1)), EINVAL),   # J aliases the table
+])
+def test_build_vocab_rejects(kw, code):
+    assert vocab(**kw) == code
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(h=None), EINVAL), (dict(loss=None), EINVAL), (dict(nJ=0), EINVAL), (dict(nJ=1001), EINVAL),
+    (dict(nrows=0), EINVAL), (dict(D=12), EUNSUP), (dict(dscale=float("nan")), EINVAL),
+    (dict(dh=misaligned(8)), EINVAL), (dict(wsb=1000), EWS),
+    (dict(dh=P(1)), EINVAL),                    # dh aliases h
+    (dict(loss=P(5)), EINVAL),                  # losses alias tpos
+])
+def test_reduced_ce_rejects(kw, code):
+    assert head_ce(**kw) == code
+
+
+def test_head_workspace_query():
+    w = lm.lib().lm_head_workspace_bytes
+    assert w(0, 64, 1000, 256, 20, 0) >= 2 * 1000 * 4
+    loss = w(1, 4096, 128256, 3072, 1229, 40000)
+    both = w(2, 4096, 128256, 3072, 1229, 40000)
+    # gathered operands + partials; the backward adds one 8192-column chunk of
+    # dz, the fp32 dh rows and the position map -- never the full logits
+    tiles = (40000 + 127) // 128
+    assert 1229 * 3072 * 2 + 40000 * 3072 * 2 <= loss
+    assert loss <= 1229 * 3072 * 2 + 40000 * 3072 * 2 + 2 * tiles * 1229 * 4 + 2 * 1229 * 4 + 6 * 256
+    assert both - loss <= 1229 * 8192 * 2 + 1229 * 3072 * 4 + 4096 * 4 + 1024
+    assert w(1, 64, 1000, 256, 20, 1001) == BAD
+    assert w(3, 64, 1000, 256, 20, 10) == BAD
+
+
 def test_rank0_ignores_lora_pointers():
     # r = 0: A, B, u, dA, dB are ignored, so NULL or misaligned values do not matter
     # (the call would then launch; only validation failures are exercised on the CPU,

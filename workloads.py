@@ -170,6 +170,37 @@ def quant_weight(d_out: int, d_in: int, bits: int = 4, group: int = 128, seed: i
             "offset": offset.float().contiguous(), "bits": bits}
 
 
+def head_inputs(T: int, V: int, D: int, ktab: int, trainable: float = 0.3, clusters: int = 64,
+                spread: int = 32, seed: int = 0, device="cpu") -> dict:
+    """Synthetic stand-ins for the frozen LM head's inputs:
+      h ~ N(0, 1) [T, D] and W ~ N(0, 0.02) [V, D] (bf16), drawn in that order;
+      targets y [T]: `clusters` centres ~ U{0..V-1}, each target a centre plus
+      U{-spread..spread} (mod V), so that the targets share neighbourhoods as
+      the tokens of one text do;
+      table [V, ktab] int32: row v lists v, v+1, v-1, v+2, v-2, ... (mod V) --
+      a stand-in for the similarity table in which the nearest tokens of v are
+      its index neighbours (its first entry is v itself);
+      rows: the trainable positions, the last `trainable` fraction of the
+      sequence (the response after a prompt).
+    All int32 except h, W."""
+    g = _gen(seed, device)
+    f32 = torch.float32
+    h = torch.randn(T, D, generator=g, device=device, dtype=f32)
+    W = torch.randn(V, D, generator=g, device=device, dtype=f32) * 0.02
+    centres = torch.randint(0, V, (clusters,), generator=g, device=device)
+    pick = torch.randint(0, clusters, (T,), generator=g, device=device)
+    off = torch.randint(-spread, spread + 1, (T,), generator=g, device=device)
+    y = (centres[pick] + off) % V
+    c = torch.arange(ktab, device=device)
+    step = (c + 1) // 2 * torch.where(c % 2 == 1, 1, -1)
+    table = (torch.arange(V, device=device)[:, None] + step[None, :]) % V
+    n_train = max(1, int(round(T * trainable)))
+    rows = torch.arange(T - n_train, T, device=device)
+    return {"h": h.to(torch.bfloat16).contiguous(), "W": W.to(torch.bfloat16).contiguous(),
+            "targets": y.to(torch.int32).contiguous(), "table": table.to(torch.int32).contiguous(),
+            "rows": rows.to(torch.int32).contiguous()}
+
+
 def sample_rows(T: int, n: int = 64, seed: int = 1234) -> list:
     """Deterministic sorted sample of row indices, always including the first and
     last rows (the ragged-tail tile), of size min(n, T)."""
