@@ -188,6 +188,26 @@ class Oracle:
             out["dX"] = self.dx(dY, W, dU, A, rows=dx_rows)
         return out
 
+    def chain(self, X0, nodes, G_last):
+        """A chain of LoRA linears, x_i = f_i(x_{i-1}) with f_i the LoRA
+        forward above (nodes: dicts W, A, B, s), and its backward from
+        G_last = dL/dx_n by the chain rule (dy_i = dx_{i+1}).  Returns the
+        outputs [x_1 .. x_n] and per node dA, dB, plus dx_0.  (The paper's
+        checkpointed schedule recomputes and reloads, but computes exactly
+        these values.)"""
+        xs = [_f64(X0)]
+        for nd in nodes:
+            _, Y = self.forward(xs[-1], nd["W"], nd["A"], nd["B"], nd["s"])
+            xs.append(Y)
+        g = _f64(G_last)
+        grads = [None] * len(nodes)
+        for i in range(len(nodes) - 1, -1, -1):
+            nd = nodes[i]
+            bw = self.backward(xs[i], nd["W"], nd["A"], nd["B"], g, nd["s"])
+            grads[i] = {"dA": bw["dA"], "dB": bw["dB"]}
+            g = bw["dX"]
+        return xs[1:], grads, g
+
     def dequant(self, Wq, S, Bo, bits, G):
         """W = S * q + Bo per group of G inputs (fp64 [N, K]) from the codes in
         Wq ([N, K*bits/8] uint8) and the per-group scales S / offsets Bo."""

@@ -403,6 +403,46 @@ def pin_reduced_vocab_union(o):
     assert list(J1) == [1, 3, 5, 6]
 
 
+# --- chain of LoRA linears (checkpointed step) ----------------------------------
+def pin_chain_finite_differences(o):
+    """L = sum(x_2 * G) for a two-node chain: its gradients with respect to
+    x_0, A_1 and B_2 by central differences match the chained backward (the
+    loss is polynomial in each of them)."""
+    g = _rng(60)
+    T, d0, d1, d2, r = 3, 4, 5, 3, 2
+    X0 = g.standard_normal((T, d0))
+    n1 = dict(W=g.standard_normal((d1, d0)), A=g.standard_normal((r, d0)),
+              B=g.standard_normal((d1, r)), s=0.7)
+    n2 = dict(W=g.standard_normal((d2, d1)), A=g.standard_normal((r, d1)),
+              B=g.standard_normal((d2, r)), s=1.3)
+    G = g.standard_normal((T, d2))
+    xs, grads, dX0 = o.chain(X0, [n1, n2], G)
+
+    def loss(X0_, A1, B2):
+        return float(np.sum(o.chain(X0_, [dict(n1, A=A1), dict(n2, B=B2)], G)[0][-1] * G))
+
+    eps = 1e-5
+    for name, arr, grad in (("X0", X0, dX0), ("A1", n1["A"], grads[0]["dA"]),
+                            ("B2", n2["B"], grads[1]["dB"])):
+        for idx in np.ndindex(arr.shape):
+            P, M = arr.copy(), arr.copy()
+            P[idx] += eps
+            M[idx] -= eps
+            args_p = {"X0": (P, n1["A"], n2["B"]), "A1": (X0, P, n2["B"]), "B2": (X0, n1["A"], P)}[name]
+            args_m = {"X0": (M, n1["A"], n2["B"]), "A1": (X0, M, n2["B"]), "B2": (X0, n1["A"], M)}[name]
+            fd = (loss(*args_p) - loss(*args_m)) / (2 * eps)
+            assert abs(fd - grad[idx]) <= 1e-6 * max(1.0, abs(grad[idx])), (name, idx)
+
+
+def pin_chain_of_one_is_one_layer(o):
+    """A one-node chain is the single LoRA linear."""
+    c = _rand_case(4, 6, 5, 2, seed=61)
+    xs, grads, dX0 = o.chain(c["X"], [dict(W=c["W"], A=c["A"], B=c["B"], s=0.5)], c["dY"])
+    U, Y, bw = _full(o, c, 0.5)
+    assert np.array_equal(xs[0], Y) and np.array_equal(dX0, bw["dX"])
+    assert np.array_equal(grads[0]["dA"], bw["dA"]) and np.array_equal(grads[0]["dB"], bw["dB"])
+
+
 ALL_PINS = [
     pin_scalar_closed_form, pin_small_closed_form, pin_rank0_textbook_gemm,
     pin_down_projection_gemm, pin_finite_differences, pin_dense_identities,
@@ -411,7 +451,8 @@ ALL_PINS = [
     pin_torch_autograd, pin_dequant_worked_example, pin_dequant_unit_scale_is_the_codes,
     pin_dequant_groups, pin_ce_worked_example, pin_ce_full_vocab_is_torch_cross_entropy,
     pin_ce_reduced_vocab_is_restricted_softmax, pin_ce_logits_masking_identity,
-    pin_ce_finite_differences, pin_reduced_vocab_union,
+    pin_ce_finite_differences, pin_reduced_vocab_union, pin_chain_finite_differences,
+    pin_chain_of_one_is_one_layer,
 ]
 
 
