@@ -205,6 +205,65 @@ def bench_lm_head(dev, steps=5, warmup=2, T=4096, V=128256, D=3072, k=1000, trai
             "tflops_full": round(6.0 * T * V * D / (ms_full * 1e-3) / 1e12, 2)}
 
 
+def bench_ckpt(dev, T=2048, pairs=4, d=3072, h=8192, r=16, steps=5, warmup=2):
+    """A chain of 2*pairs LoRA linears d -> h -> d -> ... (the MLP shapes of the
+    3B model) run plainly (every node's input and u kept on the device) and
+    checkpointed (inputs offloaded to pinned host memory over PCIe, u
+    recomputed): time per fwd+bwd and the device bytes each keeps."""
+    dims = [d, h] * pairs + [d]
+    nodes = []
+    for i in range(len(dims) - 1):
+        inp = lora_inputs(T, dims[i], dims[i + 1], r, seed=500 + i, device=dev)
+        nodes.append({"W": inp["W"], "A": inp["A"], "B": inp["B"], "scale": 2.0,
+                      "dA": torch.empty(r, dims[i], device=dev),
+                      "dB": torch.empty(dims[i + 1], r, device=dev)})
+    x0 = torch.randn(T, d, device=dev).to(torch.bfloat16)
+    g = torch.randn(T, d, device=dev).to(torch.bfloat16)
+    # plain: all activations and u resident
+    xs = [x0] + [torch.empty(T, dims[i + 1], dtype=torch.bfloat16, device=dev) for i in range(len(nodes))]
+    us = [torch.empty(T, r, device=dev) for _ in nodes]
+    gbuf = [torch.empty(T * max(dims), dtype=torch.bfloat16, device=dev) for _ in range(2)]
+    wsz = max(max(lm.lora_linear_workspace_bytes(o, T, dims[i], dims[i + 1], r, lm.LORA_BF16)
+                  for o in (0, 1)) for i in range(len(nodes)))
+    ws = torch.empty(wsz, dtype=torch.uint8, device=dev)
+
+    def plain():
+        for i, nd in enumerate(nodes):
+            lm.lora_linear_fwd(xs[i], nd["W"], nd["A"], nd["B"], xs[i + 1], us[i], 2.0, ws=ws)
+        gi = g
+        for i in range(len(nodes) - 1, -1, -1):
+            nd = nodes[i]
+            dx = gbuf[i % 2][: T * dims[i]].view(T, dims[i])
+            lm.lora_linear_bwd(xs[i], nd["W"], nd["A"], nd["B"], us[i], gi, dx, nd["dA"], nd["dB"],
+                               2.0, ws=ws)
+            gi = dx
+
+    ms_plain = time_steps(plain, steps, warmup)
+    plain_bytes = sum(x.numel() * 2 for x in xs[1:]) + sum(u.numel() * 4 for u in us) + \
+        sum(b.numel() * 2 for b in gbuf) + wsz
+    cw, ch = lm.lora_ckpt_sizes(nodes, T)
+    cws = torch.empty(cw, dtype=torch.uint8, device=dev)
+    stash = torch.empty(ch, dtype=torch.uint8, pin_memory=True)
+    out = torch.empty(T, d, dtype=torch.bfloat16, device=dev)
+    dx0 = torch.empty(T, d, dtype=torch.bfloat16, device=dev)
+    cs, cp = torch.cuda.current_stream(), torch.cuda.Stream()
+
+    def ckpt():
+        lm.lora_ckpt_forward(nodes, x0, out, stash, cws, cs, cp)
+        lm.lora_ckpt_backward(nodes, g, dx0, stash, cws, cs, cp)
+
+    ms_ckpt = time_steps(ckpt, steps, warmup)
+    torch.cuda.synchronize()
+    flops = sum(4.0 * T * dims[i] * dims[i + 1] + 6.0 * T * r * (dims[i] + dims[i + 1])
+                for i in range(len(nodes)))
+    return {"T": T, "nodes": len(nodes), "dims": dims, "rank": r,
+            "ms_plain": round(ms_plain, 4), "ms_checkpointed": round(ms_ckpt, 4),
+            "tflops_plain": round(flops / (ms_plain * 1e-3) / 1e12, 2),
+            "tflops_checkpointed": round(flops / (ms_ckpt * 1e-3) / 1e12, 2),
+            "device_bytes_plain": int(plain_bytes), "device_bytes_checkpointed": int(cw + 2 * out.numel() * 2),
+            "host_stash_bytes": int(ch)}
+
+
 def kernel_flops(workload):
     """Algorithmic flops of one launch of each GEMM kernel, per linear shape."""
     T = workload.tokens
@@ -266,6 +325,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="llama_q_proj", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-ckpt", action="store_true",
+                    help="skip the secondary measurement of the checkpointed chain")
     ap.add_argument("--no-head", action="store_true",
                     help="skip the secondary measurement of the reduced-vocabulary LM head")
     ap.add_argument("--no-quant", action="store_true",
@@ -369,6 +430,9 @@ def main():
             "unit": "TFLOP/s", "frozen_weight_bytes": int(wbytes),
             "kernels_ms_per_step": {k: round(v[0] / args.steps, 5) for k, v in pk.items()}}
         log(f"[bench] quantized base: {msq:.4f} ms/step")
+    if not args.no_ckpt:
+        out["checkpointed_chain"] = bench_ckpt(dev)
+        log(f"[bench] checkpointed chain: {out['checkpointed_chain']}")
     if not args.no_head:
         out["lm_head_reduced"] = bench_lm_head(dev)
         log(f"[bench] lm head: {out['lm_head_reduced']}")

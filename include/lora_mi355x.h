@@ -196,6 +196,43 @@ lora_status_t lm_head_reduced_ce(const void *h, const void *W, int64_t T, int64_
                                  void *dh, float dscale, void *ws, size_t ws_bytes,
                                  void *hip_stream);
 
+/* ---- Checkpointed step over a chain of LoRA linears -------------------------
+ * The paper's algorithm "Memory-Efficient Checkpointing for LoRA Fine-tuning"
+ * on one GPU, for a chain of nodes x_i = node_i(x_{i-1}) (node i a LoRA
+ * linear, bf16): the forward keeps no LoRA activation and sends each node's
+ * input to pinned host memory on `copy_stream` while the following nodes run
+ * on `compute_stream`; the backward brings each input back one node ahead of
+ * its use, recomputes u from it (as lora_linear_bwd with u_saved = NULL) and
+ * backpropagates.  The loss node between the two (the paper's LM head) is
+ * the caller's: it turns the forward's output x_n into g_n = dL/dx_n.
+ * Device memory: two activation and two gradient buffers of the widest node
+ * plus one LoRA workspace (lora_ckpt_workspace_bytes), whatever n is; host
+ * memory: every node's input (lora_ckpt_host_bytes), which must be pinned
+ * (hipHostMalloc) for the copies to run asynchronously.  Both calls return
+ * once their work is enqueued; the host stash may be read or reused only
+ * after the backward's work on both streams has completed.  The streams have
+ * the default priority; one stream may serve as both.
+ * Errors: LORA_EINVAL (n < 1, T < 1, a node's d_in not the previous d_out, a
+ * missing pointer, a workspace not 256-byte aligned), LORA_EUNSUPPORTED (a
+ * node's shape), LORA_EWORKSPACE (host or device scratch too small),
+ * LORA_EHIP, and those of lora_linear_fwd / lora_linear_bwd. */
+typedef struct {
+  const void *W, *A, *B; /* bf16: W [d_out, d_in], A [r, d_in], B [d_out, r] */
+  float *dA, *dB;        /* fp32 outputs [r, d_in], [d_out, r] (overwritten) */
+  int64_t d_in, d_out, r;
+  float scale;
+} lora_node_t;
+size_t lora_ckpt_workspace_bytes(const lora_node_t *nodes, int n, int64_t T);
+size_t lora_ckpt_host_bytes(const lora_node_t *nodes, int n, int64_t T);
+/* x0 [T, d_in of node 0] is only read; out [T, d_out of node n-1] receives x_n. */
+lora_status_t lora_ckpt_forward(const lora_node_t *nodes, int n, int64_t T, const void *x0,
+                                void *out, void *host_stash, size_t host_bytes, void *ws,
+                                size_t ws_bytes, void *compute_stream, void *copy_stream);
+/* g_n [T, d_out of node n-1]; dx0 [T, d_in of node 0] or NULL. */
+lora_status_t lora_ckpt_backward(const lora_node_t *nodes, int n, int64_t T, const void *g_n,
+                                 void *dx0, const void *host_stash, size_t host_bytes, void *ws,
+                                 size_t ws_bytes, void *compute_stream, void *copy_stream);
+
 /* Static text for a status code. */
 const char *lora_status_str(lora_status_t status);
 

@@ -16,11 +16,15 @@
 using namespace lora;
 
 namespace {
-
 thread_local char g_err[256] = "";
+}  // namespace
+
+void lora::set_last_error(const char *msg) { std::snprintf(g_err, sizeof g_err, "%s", msg); }
+
+namespace {
 
 lora_status_t fail(lora_status_t s, const char *msg) {
-  std::snprintf(g_err, sizeof g_err, "%s", msg);
+  lora::set_last_error(msg);
   return s;
 }
 

@@ -9,6 +9,9 @@ namespace lora {
 
 enum Dtype { DT_BF16 = 0, DT_F32 = 1 };
 
+// Sets the text lora_last_error() returns to the calling thread.
+void set_last_error(const char *msg);
+
 // Side work run by extra workgroups of the backward GEMM launch (they
 // overlap with the dx tiles): token-reduced products
 //   dA = du^T x   out [r, L] (transposed store), scale 1

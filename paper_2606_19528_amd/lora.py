@@ -20,6 +20,13 @@ LORA_OP_FWD, LORA_OP_BWD, LORA_OP_FROZEN_DX = 0, 1, 2
 _lib = None
 
 
+class _Node(ctypes.Structure):
+    """lora_node_t of the C ABI."""
+    _fields_ = [("W", ctypes.c_void_p), ("A", ctypes.c_void_p), ("B", ctypes.c_void_p),
+                ("dA", ctypes.c_void_p), ("dB", ctypes.c_void_p), ("d_in", ctypes.c_int64),
+                ("d_out", ctypes.c_int64), ("r", ctypes.c_int64), ("scale", ctypes.c_float)]
+
+
 class LoraError(RuntimeError):
     def __init__(self, status: int, where: str, detail: str):
         super().__init__(f"{where}: status {status} ({detail})")
@@ -62,6 +69,15 @@ def lib() -> ctypes.CDLL:
     L.lm_head_reduced_ce.argtypes = [vp, vp, i64, i64, i64, vp, i64, vp, i64, vp, vp, vp, vp, f32,
                                      vp, sz, vp]
     L.lm_head_reduced_ce.restype = i32
+    NP = ctypes.POINTER(_Node)
+    L.lora_ckpt_workspace_bytes.argtypes = [NP, i32, i64]
+    L.lora_ckpt_workspace_bytes.restype = sz
+    L.lora_ckpt_host_bytes.argtypes = [NP, i32, i64]
+    L.lora_ckpt_host_bytes.restype = sz
+    L.lora_ckpt_forward.argtypes = [NP, i32, i64, vp, vp, vp, sz, vp, sz, vp, vp]
+    L.lora_ckpt_forward.restype = i32
+    L.lora_ckpt_backward.argtypes = [NP, i32, i64, vp, vp, vp, sz, vp, sz, vp, vp]
+    L.lora_ckpt_backward.restype = i32
     L.lora_status_str.argtypes = [i32]
     L.lora_status_str.restype = ctypes.c_char_p
     L.lora_last_error.argtypes = []
@@ -262,6 +278,55 @@ def lm_head_reduced_ce(h, W, rows, J, tpos, loss_rows, loss_total=None, dh=None,
                                   float(dscale), _ptr(ws), ws_bytes, _stream(stream))
     _check(st, "lm_head_reduced_ce")
     return loss_rows
+
+
+# --- checkpointed step over a chain of LoRA linears ---------------------------------
+def _nodes(nodes):
+    arr = (_Node * len(nodes))()
+    for i, nd in enumerate(nodes):
+        W, A, B = nd["W"], nd.get("A"), nd.get("B")
+        r = 0 if A is None else A.shape[0]
+        arr[i] = _Node(W.data_ptr(), None if A is None else A.data_ptr(),
+                       None if B is None else B.data_ptr(),
+                       None if nd.get("dA") is None else nd["dA"].data_ptr(),
+                       None if nd.get("dB") is None else nd["dB"].data_ptr(),
+                       W.shape[1], W.shape[0], r, float(nd.get("scale", 1.0)))
+    return arr
+
+
+def lora_ckpt_sizes(nodes, T: int):
+    """(device workspace bytes, pinned host stash bytes) of a checkpointed step."""
+    arr = _nodes(nodes)
+    w = lib().lora_ckpt_workspace_bytes(arr, len(nodes), T)
+    h = lib().lora_ckpt_host_bytes(arr, len(nodes), T)
+    if w == ctypes.c_size_t(-1).value:
+        raise LoraError(LORA_EINVAL, "lora_ckpt_workspace_bytes", "chain rejected")
+    return int(w), int(h)
+
+
+def lora_ckpt_forward(nodes, x0, out, host_stash, ws, compute_stream=None, copy_stream=None):
+    """Checkpointed forward: out = x_n; every node input goes to host_stash
+    (pinned) on copy_stream.  nodes: dicts W, A, B, dA, dB, scale."""
+    arr = _nodes(nodes)
+    T = x0.shape[0]
+    st = lib().lora_ckpt_forward(arr, len(nodes), T, _ptr(x0), _ptr(out), _ptr(host_stash),
+                                 host_stash.numel() * host_stash.element_size(), _ptr(ws),
+                                 ws.numel() * ws.element_size(), _stream(compute_stream),
+                                 _stream(copy_stream))
+    _check(st, "lora_ckpt_forward")
+    return out
+
+
+def lora_ckpt_backward(nodes, g_n, dx0, host_stash, ws, compute_stream=None, copy_stream=None):
+    """Checkpointed backward from g_n = dL/dx_n: fills every node's dA, dB and dx0."""
+    arr = _nodes(nodes)
+    T = g_n.shape[0]
+    st = lib().lora_ckpt_backward(arr, len(nodes), T, _ptr(g_n), _ptr(dx0), _ptr(host_stash),
+                                  host_stash.numel() * host_stash.element_size(), _ptr(ws),
+                                  ws.numel() * ws.element_size(), _stream(compute_stream),
+                                  _stream(copy_stream))
+    _check(st, "lora_ckpt_backward")
+    return dx0
 
 
 # --- kernel timing hook (benchmarks) -----------------------------------------------

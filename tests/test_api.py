@@ -261,6 +261,41 @@ def test_head_workspace_query():
     assert w(3, 64, 1000, 256, 20, 10) == BAD
 
 
+def _chain(dims, r=8):
+    nodes = (L._Node * (len(dims) - 1))()
+    for i in range(len(dims) - 1):
+        nodes[i] = L._Node(P(20 + i).value, P(40 + i).value, P(60 + i).value, P(80 + i).value,
+                           P(100 + i).value, dims[i], dims[i + 1], r, 2.0)
+    return nodes
+
+
+def test_ckpt_sizes_and_rejects():
+    lib = lm.lib()
+    nodes = _chain([256, 512, 256, 384])
+    ws = lib.lora_ckpt_workspace_bytes(nodes, 3, 128)
+    host = lib.lora_ckpt_host_bytes(nodes, 3, 128)
+    assert host == 128 * (256 + 512 + 256) * 2
+    # two activation + two gradient buffers of the widest node and one LoRA workspace
+    assert 4 * 128 * 512 * 2 <= ws <= 4 * 128 * 512 * 2 + 4 * 256 + (1 << 20)
+    # ... independent of the chain's depth
+    deep = _chain([256, 512] * 10 + [256])
+    assert lib.lora_ckpt_workspace_bytes(deep, 20, 128) == ws
+    bad = _chain([256, 512, 264])
+    bad[1].d_in = 520                            # does not follow node 0's d_out
+    assert lib.lora_ckpt_workspace_bytes(bad, 2, 128) == BAD
+    big = 1 << 40
+    x0, out, stash, wsp = P(1), P(2), P(3), ctypes.c_void_p(P(4).value)
+    assert lib.lora_ckpt_forward(nodes, 0, 128, x0, out, stash, big, wsp, big, None, None) == EINVAL
+    assert lib.lora_ckpt_forward(nodes, 3, 128, None, out, stash, big, wsp, big, None, None) == EINVAL
+    assert lib.lora_ckpt_forward(nodes, 3, 128, x0, out, stash, host - 1, wsp, big, None, None) == EWS
+    assert lib.lora_ckpt_forward(nodes, 3, 128, x0, out, stash, big, wsp, ws - 1, None, None) == EWS
+    assert lib.lora_ckpt_backward(nodes, 3, 128, None, None, stash, big, wsp, big, None, None) == EINVAL
+    assert lib.lora_ckpt_backward(nodes, 3, 128, x0, None, stash, big,
+                                  ctypes.c_void_p(P(4).value + 16), big, None, None) == EINVAL
+    nodes[1].A = None
+    assert lib.lora_ckpt_forward(nodes, 3, 128, x0, out, stash, big, wsp, big, None, None) == EINVAL
+
+
 def test_rank0_ignores_lora_pointers():
     # r = 0: A, B, u, dA, dB are ignored, so NULL or misaligned values do not matter
     # (the call would then launch; only validation failures are exercised on the CPU,
