@@ -13,6 +13,7 @@ per-definition functions into the forward and backward passes:
     backward:  G = dY B ; dU = s G ; dX = dY W + dU A ; dA = dU^T X ;
                dB = s dY^T U
     quantized base:  W = S * W_q + Bo per group (dequant), then as above
+    table:     row i = the k tokens most cosine-similar to token i (topk_table)
     LM head:   J = union of top-k table rows of the trainable targets;
                loss_t = logsumexp_{j in J} h_t.w_j - h_t.w_{y_t};  dH (ce_reduced)
 
@@ -62,9 +63,10 @@ def _declare(lib: ctypes.CDLL) -> ctypes.CDLL:
     lib.oracle_dequant.argtypes = [ctypes.POINTER(ctypes.c_uint8), _dp, _dp, _i64, _i64,
                                    ctypes.c_int, _i64, _dp]
     lib.oracle_ce_reduced.argtypes = [_dp, _dp, _i64, _i64, _lp, _i64, _lp, _i64, _lp, _dp, _dp]
+    lib.oracle_topk_table.argtypes = [_dp, _i64, _i64, _i64, _lp, _dp]
     for name in ("oracle_lora_u", "oracle_lora_y_rows", "oracle_lora_grad_u",
                  "oracle_lora_dx_rows", "oracle_lora_da", "oracle_lora_db", "oracle_dequant",
-                 "oracle_ce_reduced"):
+                 "oracle_ce_reduced", "oracle_topk_table"):
         getattr(lib, name).restype = None
     lib.oracle_threads.argtypes = []
     lib.oracle_threads.restype = ctypes.c_int
@@ -187,6 +189,16 @@ class Oracle:
         if want_dx:
             out["dX"] = self.dx(dY, W, dU, A, rows=dx_rows)
         return out
+
+    def topk_table(self, W, k):
+        """(A [V, k] int64, C [V, k] fp64): each token's k most cosine-similar
+        tokens (itself first for distinct directions) and their similarities."""
+        W = _f64(W)
+        V, D = W.shape
+        A = np.empty((V, k), dtype=np.int64)
+        C = np.empty((V, k), dtype=np.float64)
+        self.lib.oracle_topk_table(_ptr(W), V, D, k, A.ctypes.data_as(_lp), _ptr(C))
+        return A, C
 
     def chain(self, X0, nodes, G_last):
         """A chain of LoRA linears, x_i = f_i(x_{i-1}) with f_i the LoRA

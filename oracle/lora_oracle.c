@@ -217,6 +217,55 @@ void oracle_ce_reduced(const double *H, const double *W, int64_t T, int64_t D,
   }
 }
 
+/* Order of two (similarity, token) pairs: higher similarity first, the
+ * smaller token index first among equal similarities. */
+typedef struct {
+  double c;
+  int64_t j;
+} sim_pair;
+static int sim_pair_cmp(const void *pa, const void *pb) {
+  const sim_pair *a = (const sim_pair *)pa, *b = (const sim_pair *)pb;
+  if (a->c > b->c) return -1;
+  if (a->c < b->c) return 1;
+  return (a->j > b->j) - (a->j < b->j);
+}
+
+/* Top-k similarity table (paper: "Softmax Approximation" -- the cosine
+ * similarities C = W~^T W~ of the column-normalised embedding matrix, row i
+ * sorted in descending order, the first k indices kept).  Here the
+ * embeddings are the rows of W [V, D]:
+ *   C[i][j] = (w_i . w_j) / (|w_i| |w_j|)
+ *   A[i][0 .. k-1] = the indices j of row i sorted by C[i][j] descending
+ *                    (the smaller j first among equal similarities),
+ * and Cs[i][c] = C[i][A[i][c]].  A zero row has similarity 0 with all. */
+void oracle_topk_table(const double *W, int64_t V, int64_t D, int64_t k, int64_t *A,
+                       double *Cs) {
+  double *norm = (double *)malloc(sizeof(double) * (size_t)V);
+  for (int64_t v = 0; v < V; ++v) {
+    double acc = 0.0;
+    for (int64_t d = 0; d < D; ++d) acc += W[v * D + d] * W[v * D + d];
+    norm[v] = sqrt(acc);
+  }
+#pragma omp parallel for schedule(dynamic)
+  for (int64_t i = 0; i < V; ++i) {
+    sim_pair *row = (sim_pair *)malloc(sizeof(sim_pair) * (size_t)V);
+    for (int64_t j = 0; j < V; ++j) {
+      double dot = 0.0;
+      for (int64_t d = 0; d < D; ++d) dot += W[i * D + d] * W[j * D + d];
+      const double den = norm[i] * norm[j];
+      row[j].c = den > 0.0 ? dot / den : 0.0;
+      row[j].j = j;
+    }
+    qsort(row, (size_t)V, sizeof(sim_pair), sim_pair_cmp);
+    for (int64_t c = 0; c < k; ++c) {
+      A[i * k + c] = row[c].j;
+      Cs[i * k + c] = row[c].c;
+    }
+    free(row);
+  }
+  free(norm);
+}
+
 /* Number of OpenMP threads the oracle runs with (1 when built without
  * OpenMP); reported next to its timings. */
 #ifdef _OPENMP

@@ -403,6 +403,49 @@ def pin_reduced_vocab_union(o):
     assert list(J1) == [1, 3, 5, 6]
 
 
+# --- top-k similarity table ------------------------------------------------------
+def pin_topk_table_worked_example(o):
+    """Four 2-d embeddings at angles 0, 30, 90 and 180 degrees (scaled
+    differently: the table depends on directions only)."""
+    import math
+    W = np.array([[2.0, 0.0], [math.sqrt(3), 1.0], [0.0, 5.0], [-1.0, 0.0]])
+    A, C = o.topk_table(W, 4)
+    assert [list(r) for r in A] == [[0, 1, 2, 3], [1, 0, 2, 3], [2, 1, 0, 3], [3, 2, 1, 0]]
+    assert abs(C[0, 1] - math.cos(math.pi / 6)) < 1e-14 and abs(C[1, 2] - 0.5) < 1e-14
+    assert C[3, 3] == -1.0 and C[0, 2] == 0.0 and C[2, 2] == 0.0
+
+
+def pin_topk_table_is_argsort(o):
+    """Against numpy: a stable argsort of each row of the normalised Gram
+    matrix (descending), first k columns; the first entry of row i is i."""
+    g = _rng(70)
+    V, D, k = 60, 7, 9
+    W = g.standard_normal((V, D))
+    Wn = W / np.linalg.norm(W, axis=1, keepdims=True)
+    S = Wn @ Wn.T
+    ref = np.argsort(-S, axis=1, kind="stable")[:, :k]
+    A, C = o.topk_table(W, k)
+    assert np.array_equal(A, ref)
+    assert np.array_equal(A[:, 0], np.arange(V))
+    assert _relmax(C, np.take_along_axis(S, ref, axis=1)) <= 1e-13
+
+
+def pin_topk_table_invariances(o):
+    """Rescaling embeddings leaves the table unchanged; permuting the tokens
+    permutes it accordingly."""
+    g = _rng(71)
+    V, D, k = 40, 5, 6
+    W = g.standard_normal((V, D))
+    A, _ = o.topk_table(W, k)
+    A2, _ = o.topk_table(W * g.uniform(0.5, 3.0, size=(V, 1)), k)
+    assert np.array_equal(A, A2)
+    perm = g.permutation(V)
+    Ap, _ = o.topk_table(W[perm], k)
+    inv = np.argsort(perm)
+    assert np.array_equal(perm[Ap], A[perm])
+    del inv
+
+
 # --- chain of LoRA linears (checkpointed step) ----------------------------------
 def pin_chain_finite_differences(o):
     """L = sum(x_2 * G) for a two-node chain: its gradients with respect to
@@ -452,7 +495,8 @@ ALL_PINS = [
     pin_dequant_groups, pin_ce_worked_example, pin_ce_full_vocab_is_torch_cross_entropy,
     pin_ce_reduced_vocab_is_restricted_softmax, pin_ce_logits_masking_identity,
     pin_ce_finite_differences, pin_reduced_vocab_union, pin_chain_finite_differences,
-    pin_chain_of_one_is_one_layer,
+    pin_chain_of_one_is_one_layer, pin_topk_table_worked_example, pin_topk_table_is_argsort,
+    pin_topk_table_invariances,
 ]
 
 

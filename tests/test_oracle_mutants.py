@@ -56,6 +56,12 @@ MUTANTS = [
      "for (int64_t d = 0; d < D; ++d) acc += H[t * D + d] * W[j * D + d];"),
     ("ce_wrong_row_of_H", "for (int64_t d = 0; d < D; ++d) acc += H[t * D + d] * W[J[j] * D + d];",
      "for (int64_t d = 0; d < D; ++d) acc += H[i * D + d] * W[J[j] * D + d];"),
+    ("topk_ascending", "  if (a->c > b->c) return -1;\n  if (a->c < b->c) return 1;",
+     "  if (a->c > b->c) return 1;\n  if (a->c < b->c) return -1;"),
+    ("topk_unnormalised", "row[j].c = den > 0.0 ? dot / den : 0.0;", "row[j].c = dot;"),
+    ("topk_row_norm_only", "const double den = norm[i] * norm[j];", "const double den = norm[i];"),
+    ("topk_ties_larger_index_first", "return (a->j > b->j) - (a->j < b->j);",
+     "return (a->j < b->j) - (a->j > b->j);"),
 ]
 
 CHILD = textwrap.dedent("""
