@@ -264,6 +264,21 @@ def bench_ckpt(dev, T=2048, pairs=4, d=3072, h=8192, r=16, steps=5, warmup=2):
             "host_stash_bytes": int(ch)}
 
 
+def bench_topk(dev, V=128256, D=3072, k=1000):
+    """The similarity table of the 3B model's output embedding (k = 1000):
+    one build, after one warm-up build; the work is the V x V x D similarity
+    GEMM (the selection streams behind it)."""
+    W = (torch.randn(V, D, device=dev) * 0.02).to(torch.bfloat16)
+    table = torch.empty(V, k, dtype=torch.int32, device=dev)
+    ws = torch.empty(lm.lora.lib().topk_table_workspace_bytes(V, D, k), dtype=torch.uint8, device=dev)
+    ms = time_steps(lambda: lm.topk_table_build(W, k, table, ws=ws), 1, 1)
+    pk = per_kernel_ms(lambda: lm.topk_table_build(W, k, table, ws=ws), 1)
+    return {"V": V, "D": D, "k": k, "ms": round(ms, 2),
+            "tflops_similarity": round(2.0 * V * V * D / (ms * 1e-3) / 1e12, 2),
+            "kernels_ms": {n: round(v[0], 2) for n, v in pk.items()},
+            "table_bytes": V * k * 4}
+
+
 def kernel_flops(workload):
     """Algorithmic flops of one launch of each GEMM kernel, per linear shape."""
     T = workload.tokens
@@ -325,6 +340,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="llama_q_proj", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-topk", action="store_true",
+                    help="skip the secondary measurement of the top-k similarity table build")
     ap.add_argument("--no-ckpt", action="store_true",
                     help="skip the secondary measurement of the checkpointed chain")
     ap.add_argument("--no-head", action="store_true",
@@ -430,6 +447,9 @@ def main():
             "unit": "TFLOP/s", "frozen_weight_bytes": int(wbytes),
             "kernels_ms_per_step": {k: round(v[0] / args.steps, 5) for k, v in pk.items()}}
         log(f"[bench] quantized base: {msq:.4f} ms/step")
+    if not args.no_topk:
+        out["topk_table"] = bench_topk(dev)
+        log(f"[bench] top-k table: {out['topk_table']}")
     if not args.no_ckpt:
         out["checkpointed_chain"] = bench_ckpt(dev)
         log(f"[bench] checkpointed chain: {out['checkpointed_chain']}")

@@ -196,6 +196,26 @@ lora_status_t lm_head_reduced_ce(const void *h, const void *W, int64_t T, int64_
                                  void *dh, float dscale, void *ws, size_t ws_bytes,
                                  void *hip_stream);
 
+/* ---- Top-k similarity table ------------------------------------------------
+ * The lookup table of the reduced-vocabulary softmax (paper: "Softmax
+ * Approximation"): for each token i of the frozen embedding matrix W [V, D]
+ * (bf16, row v = token v) the k tokens of highest cosine similarity
+ * C[i][j] = (w_i . w_j) / (|w_i| |w_j|), in descending order (the smaller
+ * index first among equal similarities):
+ *   table [V, k] int32, values [V, k] fp32 (optional, the similarities).
+ * Row i starts with i itself when no other token points the same way.  The
+ * V x V similarities are never stored: a GEMM over a batch of rows and a
+ * chunk of columns appends the candidates above each row's running
+ * threshold, and a per-row selection keeps the k best after each chunk.
+ * Similarities are fp32 (bf16 products, fp32 sums): tokens within about
+ * 1e-6 of each other may come out in either order.  Requires 1 <= k <=
+ * min(V, 2048) and D a multiple of 8; workspace topk_table_workspace_bytes
+ * ((size_t)-1 for rejected sizes).  Errors: LORA_EINVAL, LORA_EUNSUPPORTED
+ * (D, sizes), LORA_EWORKSPACE, LORA_EHIP. */
+size_t topk_table_workspace_bytes(int64_t V, int64_t D, int64_t k);
+lora_status_t topk_table_build(const void *W, int64_t V, int64_t D, int64_t k, int32_t *table,
+                               float *values, void *ws, size_t ws_bytes, void *hip_stream);
+
 /* ---- Checkpointed step over a chain of LoRA linears -------------------------
  * The paper's algorithm "Memory-Efficient Checkpointing for LoRA Fine-tuning"
  * on one GPU, for a chain of nodes x_i = node_i(x_{i-1}) (node i a LoRA

@@ -63,7 +63,7 @@ def _declare(lib: ctypes.CDLL) -> ctypes.CDLL:
     lib.oracle_dequant.argtypes = [ctypes.POINTER(ctypes.c_uint8), _dp, _dp, _i64, _i64,
                                    ctypes.c_int, _i64, _dp]
     lib.oracle_ce_reduced.argtypes = [_dp, _dp, _i64, _i64, _lp, _i64, _lp, _i64, _lp, _dp, _dp]
-    lib.oracle_topk_table.argtypes = [_dp, _i64, _i64, _i64, _lp, _dp]
+    lib.oracle_topk_table.argtypes = [_dp, _i64, _i64, _i64, _lp, _i64, _lp, _dp]
     for name in ("oracle_lora_u", "oracle_lora_y_rows", "oracle_lora_grad_u",
                  "oracle_lora_dx_rows", "oracle_lora_da", "oracle_lora_db", "oracle_dequant",
                  "oracle_ce_reduced", "oracle_topk_table"):
@@ -190,14 +190,18 @@ class Oracle:
             out["dX"] = self.dx(dY, W, dU, A, rows=dx_rows)
         return out
 
-    def topk_table(self, W, k):
-        """(A [V, k] int64, C [V, k] fp64): each token's k most cosine-similar
-        tokens (itself first for distinct directions) and their similarities."""
+    def topk_table(self, W, k, rows=None):
+        """(A [n, k] int64, C [n, k] fp64): each token's k most cosine-similar
+        tokens (itself first for distinct directions) and their similarities,
+        for every token (rows None) or the listed ones."""
         W = _f64(W)
         V, D = W.shape
-        A = np.empty((V, k), dtype=np.int64)
-        C = np.empty((V, k), dtype=np.float64)
-        self.lib.oracle_topk_table(_ptr(W), V, D, k, A.ctypes.data_as(_lp), _ptr(C))
+        rp, nr, keep = _rows(rows)
+        n = V if rows is None else nr
+        A = np.empty((n, k), dtype=np.int64)
+        C = np.empty((n, k), dtype=np.float64)
+        self.lib.oracle_topk_table(_ptr(W), V, D, k, rp, nr, A.ctypes.data_as(_lp), _ptr(C))
+        del keep
         return A, C
 
     def chain(self, X0, nodes, G_last):

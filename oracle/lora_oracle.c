@@ -237,17 +237,21 @@ static int sim_pair_cmp(const void *pa, const void *pb) {
  *   C[i][j] = (w_i . w_j) / (|w_i| |w_j|)
  *   A[i][0 .. k-1] = the indices j of row i sorted by C[i][j] descending
  *                    (the smaller j first among equal similarities),
- * and Cs[i][c] = C[i][A[i][c]].  A zero row has similarity 0 with all. */
-void oracle_topk_table(const double *W, int64_t V, int64_t D, int64_t k, int64_t *A,
-                       double *Cs) {
+ * and Cs[i][c] = C[i][A[i][c]].  A zero row has similarity 0 with all.
+ * rows == NULL computes every row i into A[i]; otherwise row rows[r] goes to
+ * A[r] (r < nrows). */
+void oracle_topk_table(const double *W, int64_t V, int64_t D, int64_t k, const int64_t *rows,
+                       int64_t nrows, int64_t *A, double *Cs) {
   double *norm = (double *)malloc(sizeof(double) * (size_t)V);
   for (int64_t v = 0; v < V; ++v) {
     double acc = 0.0;
     for (int64_t d = 0; d < D; ++d) acc += W[v * D + d] * W[v * D + d];
     norm[v] = sqrt(acc);
   }
+  const int64_t count = rows ? nrows : V;
 #pragma omp parallel for schedule(dynamic)
-  for (int64_t i = 0; i < V; ++i) {
+  for (int64_t r = 0; r < count; ++r) {
+    const int64_t i = rows ? rows[r] : r;
     sim_pair *row = (sim_pair *)malloc(sizeof(sim_pair) * (size_t)V);
     for (int64_t j = 0; j < V; ++j) {
       double dot = 0.0;
@@ -258,8 +262,8 @@ void oracle_topk_table(const double *W, int64_t V, int64_t D, int64_t k, int64_t
     }
     qsort(row, (size_t)V, sizeof(sim_pair), sim_pair_cmp);
     for (int64_t c = 0; c < k; ++c) {
-      A[i * k + c] = row[c].j;
-      Cs[i * k + c] = row[c].c;
+      A[r * k + c] = row[c].j;
+      Cs[r * k + c] = row[c].c;
     }
     free(row);
   }

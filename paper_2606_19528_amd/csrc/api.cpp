@@ -43,12 +43,15 @@ enum KernelId {
   K_HEAD_LOGITS,      // logits GEMM with the row-statistics epilogue (+ combine)
   K_HEAD_DZ,          // logits recomputed, softmax gradient epilogue
   K_HEAD_DH,          // dh += dz W_J (fp32), then the bf16 dh rows
+  K_TOPK_SIM,         // similarity GEMM with the candidate epilogue (+ row norms)
+  K_TOPK_SELECT,      // per-row selection of the k best candidates
   K_COUNT
 };
 const char *kKernelNames[K_COUNT] = {"gemm_fwd",   "gemm_bwd_dx",   "gemm_frozen_dx",
                                      "lora_down",  "lora_dy_b",     "gemm_fwd_q",
                                      "gemm_bwd_dx_q", "gemm_frozen_dx_q", "head_vocab",
-                                     "head_gather", "head_logits", "head_dz", "head_dh"};
+                                     "head_gather", "head_logits", "head_dz", "head_dh",
+                                     "topk_sim", "topk_select"};
 
 struct EventPair {
   hipEvent_t a, b;
@@ -217,6 +220,32 @@ CeLayout ce_layout(int64_t T, int64_t D, int64_t nrows, int64_t nJ, bool want_dh
     L.inv = off;
     off += round256((size_t)T * 4);
   }
+  L.total = off;
+  return L;
+}
+
+// Top-k table workspace: row norms, and per batch of rows a threshold, a
+// count and a candidate list of k + one column chunk per row.
+constexpr int64_t kTopkChunk = 4096, kTopkBatch = 16384;
+struct TopkLayout {
+  size_t rn, thr, cnt, val, idx, total;
+  int64_t R, cap;
+};
+TopkLayout topk_layout(int64_t V, int64_t k) {
+  TopkLayout L{};
+  L.R = std::min(V, kTopkBatch);
+  L.cap = k + kTopkChunk;
+  size_t off = 0;
+  L.rn = off;
+  off += round256((size_t)V * 4);
+  L.thr = off;
+  off += round256((size_t)L.R * 4);
+  L.cnt = off;
+  off += round256((size_t)L.R * 4);
+  L.val = off;
+  off += round256((size_t)L.R * L.cap * 4);
+  L.idx = off;
+  off += round256((size_t)L.R * L.cap * 4);
   L.total = off;
   return L;
 }
@@ -713,6 +742,72 @@ lora_status_t lm_head_reduced_ce(const void *h, const void *W, int64_t T, int64_
   e = launch_dh_finish(dhacc, rows, (int)nrows, (int32_t *)(wsb + L.inv), (int)T, (int)D, dh, st);
   t.done();
   return e == hipSuccess ? LORA_OK : hip_fail(e, "head_dh launch");
+}
+
+size_t topk_table_workspace_bytes(int64_t V, int64_t D, int64_t k) {
+  if (V < 1 || D < 8 || D % 8 || k < 1 || k > std::min<int64_t>(V, 2048) || D > kMaxDim ||
+      V > kMaxElems / D || V > kMaxElems / k)
+    return (size_t)-1;
+  return topk_layout(V, k).total;
+}
+
+lora_status_t topk_table_build(const void *W, int64_t V, int64_t D, int64_t k, int32_t *table,
+                               float *values, void *ws, size_t ws_bytes, void *hip_stream) {
+  if (!W || !table) return fail(LORA_EINVAL, "W and table are required");
+  if (V < 1 || k < 1 || k > std::min<int64_t>(V, 2048))
+    return fail(LORA_EINVAL, "need V >= 1 and 1 <= k <= min(V, 2048)");
+  if (D < 8 || D % 8) return fail(LORA_EUNSUPPORTED, "D must be a positive multiple of 8");
+  if (D > kMaxDim || V > kMaxElems / D || V > kMaxElems / k)
+    return fail(LORA_EUNSUPPORTED, "D at most 2^20 and W, table below 2^31 elements");
+  if (!aligned16(W) || !aligned16(table) || (values && !aligned16(values)))
+    return fail(LORA_EINVAL, "pointers must be 16-byte aligned");
+  const TopkLayout L = topk_layout(V, k);
+  lora_status_t s;
+  if ((s = check_ws(ws, ws_bytes, L.total)) != LORA_OK) return s;
+  std::vector<Range> ins = {rng(W, V * D * 2)};
+  std::vector<Range> outs = {rng(table, V * k * 4), rng(ws, (int64_t)L.total)};
+  if (values) outs.push_back(rng(values, V * k * 4));
+  if (any_overlap(outs, ins)) return fail(LORA_EINVAL, "an output overlaps an input or another output");
+  hipStream_t st = (hipStream_t)hip_stream;
+  char *wsb = (char *)ws;
+  float *rn = (float *)(wsb + L.rn);
+  TopkArgs ta{};
+  ta.val = (float *)(wsb + L.val); ta.idx = (int32_t *)(wsb + L.idx);
+  ta.cnt = (int *)(wsb + L.cnt); ta.thr = (float *)(wsb + L.thr);
+  ta.cap = (int)L.cap; ta.k = (int)k; ta.table = table; ta.tvals = values;
+  hipError_t e;
+  {
+    Timed t(K_TOPK_SIM, st);
+    e = launch_row_rnorm(W, (int)V, (int)D, rn, st);
+    t.done();
+    if (e != hipSuccess) return hip_fail(e, "topk_sim launch");
+  }
+  for (int64_t r0 = 0; r0 < V; r0 += L.R) {
+    const int rb = (int)std::min<int64_t>(L.R, V - r0);
+    if ((e = launch_topk_reset(ta.thr, ta.cnt, rb, st)) != hipSuccess) return hip_fail(e, "topk reset");
+    ta.row0 = r0;
+    for (int64_t c0 = 0; c0 < V; c0 += kTopkChunk) {
+      GemmArgs g{};
+      g.A = (const char *)W + r0 * D * 2; g.lda = D;
+      g.B = (const char *)W + c0 * D * 2; g.ldb = D;
+      g.M = rb; g.N = (int)std::min<int64_t>(kTopkChunk, V - c0); g.K = (int)D;
+      g.col0 = (int)c0; g.rn_a = rn + r0; g.rn_b = rn + c0;
+      g.tk_thr = ta.thr; g.tk_cnt = ta.cnt; g.tk_val = ta.val; g.tk_idx = ta.idx;
+      g.tk_cap = (int)L.cap;
+      {
+        Timed t(K_TOPK_SIM, st);
+        e = launch_gemm_epi(g, EPI_TOPK, st);
+        t.done();
+        if (e != hipSuccess) return hip_fail(e, "topk_sim launch");
+      }
+      const int final = c0 + kTopkChunk >= V;
+      Timed t(K_TOPK_SELECT, st);
+      e = launch_topk_select(ta, rb, final, st);
+      t.done();
+      if (e != hipSuccess) return hip_fail(e, "topk_select launch");
+    }
+  }
+  return LORA_OK;
 }
 
 const char *lora_status_str(lora_status_t status) {

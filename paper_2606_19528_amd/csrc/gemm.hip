@@ -96,8 +96,8 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   constexpr int QPIECES = BMODE == B_ROW ? BN * (BKE / 16) : BKE * (BN / 16);
   static_assert(QB == 0 || QB == 4 || QB == 8, "code width");
   static_assert(EPI == EPI_STORE || (ES == 2 && FS), "cross-entropy / fp32 epilogues: bf16 kernels");
-  static_assert(EPI != EPI_CE_STATS || (NT == 4 * BM && BM * (BN + 1) * 4 <= LDS),
-                "row statistics: four threads per tile row, the fp32 tile in LDS");
+  static_assert((EPI != EPI_CE_STATS && EPI != EPI_TOPK) || (NT == 4 * BM && BM * (BN + 1) * 4 <= LDS),
+                "row statistics / candidates: four threads per tile row, the fp32 tile in LDS");
   static_assert(QB == 0 || (ES == 2 && FS && BMODE != B_KMAJ_REG && QPIECES == NT),
                 "quantized B: bf16, staged fragments, one 16-weight piece per thread");
 
@@ -739,6 +739,59 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
     }
     return;
   }
+  if constexpr (EPI == EPI_TOPK) {
+    // Cosines c = z * rn_a[m] * rn_b[n] of this tile; every one above the
+    // row's threshold is appended to the row's candidate list.  Four threads
+    // share a row: their counts give each its place after one atomic add on
+    // the row's count (the list's order is irrelevant, its content is not).
+    __syncthreads();
+    float *zt = (float *)smem;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      if (WK > 1 && b % WK != wk) continue;
+      const int i = b / FN, j = b % FN;
+      const int row = wm * WTM + i * 32 + lrow;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          zt[row * (BN + 1) + wn * WTN + j * 32 + 8 * q + 4 * (lane >> 5) + e] = acc[i][j][4 * q + e];
+    }
+    __syncthreads();
+    const int row = tid >> 2, sub = tid & 3;
+    constexpr int CPT = BN / 4;
+    const int m = m0 + row;
+    if (m >= g.M) return;  // all four threads of the row leave together
+    const int ncol = min(BN, g.N - n0);
+    const int c_lo = sub * CPT, c_hi = min(ncol, (sub + 1) * CPT);
+    const float *zr = zt + row * (BN + 1);
+    const float ra = g.rn_a[m], th = g.tk_thr[m];
+    int mine = 0;
+    for (int c = c_lo; c < c_hi; ++c) mine += zr[c] * ra * g.rn_b[n0 + c] > th;
+    const int l0 = lane & ~3;
+    const int n0c = __shfl(mine, l0), n1c = __shfl(mine, l0 + 1), n2c = __shfl(mine, l0 + 2),
+              n3c = __shfl(mine, l0 + 3);
+    const int total = n0c + n1c + n2c + n3c;
+    const int before = (sub > 0 ? n0c : 0) + (sub > 1 ? n1c : 0) + (sub > 2 ? n2c : 0);
+    int base = 0;
+    if (sub == 0 && total > 0) base = atomicAdd(g.tk_cnt + m, total);
+    base = __shfl(base, l0);
+    if (total == 0) return;
+    int slot = base + before;
+    float *vr = g.tk_val + (int64_t)m * g.tk_cap;
+    int32_t *ir = g.tk_idx + (int64_t)m * g.tk_cap;
+    for (int c = c_lo; c < c_hi; ++c) {
+      const float v = zr[c] * ra * g.rn_b[n0 + c];
+      if (v > th) {
+        if (slot < g.tk_cap) {  // never past the list (the sizes rule it out)
+          vr[slot] = v;
+          ir[slot] = g.col0 + n0 + c;
+        }
+        ++slot;
+      }
+    }
+    return;
+  }
   if constexpr (EPI == EPI_CE_DZ) {
     // dz = dscale * (exp(z - lse[m]) - [column is the target]), bf16; columns
     // from N up to the padded row length ldc are written as zeros.
@@ -874,6 +927,8 @@ hipError_t launch_gemm_epi(const GemmArgs &g, int epi, hipStream_t st) {
       return launch_cfg<BF16, 128, 128, 2, 2, 2, B_ROW, 128, 2, 3, 2, 0, EPI_CE_DZ>(g, nullptr, st);
     case EPI_F32:
       return launch_cfg<BF16, 128, 128, 2, 2, 2, B_KMAJ_TR, 128, 2, 3, 2, 0, EPI_F32>(g, nullptr, st);
+    case EPI_TOPK:
+      return launch_cfg<BF16, 128, 128, 2, 2, 2, B_ROW, 128, 2, 3, 2, 0, EPI_TOPK>(g, nullptr, st);
   }
   return hipErrorInvalidValue;
 }

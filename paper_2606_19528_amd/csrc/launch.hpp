@@ -79,6 +79,15 @@ struct GemmArgs {
   const float *lse;                 // EPI_CE_DZ
   float dscale;
   int c_accumulate;                 // EPI_F32: C fp32 += product instead of =
+  // EPI_TOPK: cosine = z * rn_a[m] * rn_b[n]; appended (value, col0 + n) to
+  // row m's list (tk_val / tk_idx, tk_cap slots, count tk_cnt[m]) when above
+  // tk_thr[m].
+  const float *rn_a, *rn_b;
+  const float *tk_thr;
+  int *tk_cnt;
+  float *tk_val;
+  int32_t *tk_idx;
+  int tk_cap;
 };
 
 // Epilogues of launch_gemm_epi (bf16 operands, 128 x 128 tiles):
@@ -87,8 +96,9 @@ struct GemmArgs {
 //                 ce_tgt[m] = z at the target column (B row-major);
 //   EPI_CE_DZ     C bf16 [M][ldc] = dscale (exp(z - lse[m]) - [n is the
 //                 target]) for n < N, 0 for N <= n < ldc (B row-major);
-//   EPI_F32       C fp32 [M][ldc] (+)= A B (B k-major).
-enum { EPI_STORE = 0, EPI_CE_STATS = 1, EPI_CE_DZ = 2, EPI_F32 = 3 };
+//   EPI_F32       C fp32 [M][ldc] (+)= A B (B k-major);
+//   EPI_TOPK      no C; candidates of the similarity table (B row-major).
+enum { EPI_STORE = 0, EPI_CE_STATS = 1, EPI_CE_DZ = 2, EPI_F32 = 3, EPI_TOPK = 4 };
 hipError_t launch_gemm_epi(const GemmArgs &g, int epi, hipStream_t st);
 
 // Reduced vocabulary: J = sorted union over i < nrows of
@@ -115,6 +125,23 @@ hipError_t launch_gather_rows(const void *src, int64_t ld, int nsrc, const int32
 hipError_t launch_ce_combine(const float *tmax, const float *tsum, int ntiles, int M,
                              const float *ztgt, float *lse, float *loss, float *total,
                              hipStream_t st);
+// Top-k similarity table: per-row candidate lists of a batch of rows.
+struct TopkArgs {
+  float *val;
+  int32_t *idx;
+  int *cnt;
+  float *thr;
+  int cap, k;
+  int32_t *table;  // [V][k], rows row0 .. row0 + R - 1 written by the final select
+  float *tvals;    // optional [V][k]
+  int64_t row0;
+};
+hipError_t launch_row_rnorm(const void *W, int V, int D, float *rn, hipStream_t st);
+hipError_t launch_topk_reset(float *thr, int *cnt, int R, hipStream_t st);
+// keep each of the R rows' k best candidates (final = 0) or sort them into
+// the table (final = 1); cap <= 8192, k <= 2048.
+hipError_t launch_topk_select(const TopkArgs &a, int R, int final, hipStream_t st);
+
 // p[0 .. n) = quiet NaN.
 hipError_t launch_fill_nan(float *p, int64_t n, hipStream_t st);
 // dh [T][D] bf16: row rows[i] = acc[i], every other row 0 (inv: T words scratch).

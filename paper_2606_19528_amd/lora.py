@@ -78,6 +78,10 @@ def lib() -> ctypes.CDLL:
     L.lora_ckpt_forward.restype = i32
     L.lora_ckpt_backward.argtypes = [NP, i32, i64, vp, vp, vp, sz, vp, sz, vp, vp]
     L.lora_ckpt_backward.restype = i32
+    L.topk_table_workspace_bytes.argtypes = [i64, i64, i64]
+    L.topk_table_workspace_bytes.restype = sz
+    L.topk_table_build.argtypes = [vp, i64, i64, i64, vp, vp, vp, sz, vp]
+    L.topk_table_build.restype = i32
     L.lora_status_str.argtypes = [i32]
     L.lora_status_str.restype = ctypes.c_char_p
     L.lora_last_error.argtypes = []
@@ -278,6 +282,25 @@ def lm_head_reduced_ce(h, W, rows, J, tpos, loss_rows, loss_total=None, dh=None,
                                   float(dscale), _ptr(ws), ws_bytes, _stream(stream))
     _check(st, "lm_head_reduced_ce")
     return loss_rows
+
+
+# --- top-k similarity table ---------------------------------------------------------
+def topk_table_build(W, k: int, table=None, values=None, ws=None, stream=None):
+    """table [V, k] int32 (and optionally values [V, k] fp32) of each token's k
+    most cosine-similar tokens."""
+    import torch
+
+    V, D = W.shape
+    if table is None:
+        table = torch.empty(V, k, dtype=torch.int32, device=W.device)
+    n = lib().topk_table_workspace_bytes(V, D, k)
+    if n == ctypes.c_size_t(-1).value:
+        raise LoraError(LORA_EINVAL, "topk_table_workspace_bytes", "sizes rejected")
+    ws, ws_bytes = _ws(ws, int(n), W)
+    st = lib().topk_table_build(_ptr(W), V, D, k, _ptr(table), _ptr(values), _ptr(ws), ws_bytes,
+                                _stream(stream))
+    _check(st, "topk_table_build")
+    return table
 
 
 # --- checkpointed step over a chain of LoRA linears ---------------------------------

@@ -444,6 +444,11 @@ def pin_topk_table_invariances(o):
     inv = np.argsort(perm)
     assert np.array_equal(perm[Ap], A[perm])
     del inv
+    # a sample of rows is those rows of the full table
+    rows = [3, 17, 39]
+    Ar, Cr = o.topk_table(W, k, rows=rows)
+    Af, Cf = o.topk_table(W, k)
+    assert np.array_equal(Ar, Af[rows]) and np.array_equal(Cr, Cf[rows])
 
 
 # --- chain of LoRA linears (checkpointed step) ----------------------------------

@@ -296,6 +296,23 @@ def test_ckpt_sizes_and_rejects():
     assert lib.lora_ckpt_forward(nodes, 3, 128, x0, out, stash, big, wsp, big, None, None) == EINVAL
 
 
+def test_topk_table_sizes_and_rejects():
+    lib = lm.lib()
+    w = lib.topk_table_workspace_bytes
+    # norms + per batch of rows (at most 16384) k + 4096 candidates per row
+    n = w(128256, 3072, 1000)
+    R = 16384
+    assert R * (1000 + 4096) * 8 <= n <= R * (1000 + 4096) * 8 + 128256 * 4 + 2 * R * 4 + 6 * 256
+    assert w(1000, 64, 1001) == BAD and w(5000, 64, 2049) == BAD and w(100, 12, 5) == BAD
+    t = lib.topk_table_build
+    assert t(None, 1000, 64, 10, P(2), None, P(3), 1 << 30, None) == EINVAL
+    assert t(P(1), 1000, 64, 0, P(2), None, P(3), 1 << 30, None) == EINVAL
+    assert t(P(1), 1000, 60, 10, P(2), None, P(3), 1 << 30, None) == EUNSUP
+    assert t(P(1), 1000, 64, 10, P(2), None, P(3), 100, None) == EWS
+    assert t(P(1), 1000, 64, 10, P(1), None, P(3), 1 << 30, None) == EINVAL   # table aliases W
+    assert t(P(1), 1000, 64, 10, misaligned(2), None, P(3), 1 << 30, None) == EINVAL
+
+
 def test_rank0_ignores_lora_pointers():
     # r = 0: A, B, u, dA, dB are ignored, so NULL or misaligned values do not matter
     # (the call would then launch; only validation failures are exercised on the CPU,

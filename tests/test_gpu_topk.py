@@ -1,0 +1,88 @@
+"""GPU parity of the top-k cosine-similarity table against the fp64 oracle.
+
+The similarities are fp32 sums of bf16 products, so tokens whose exact
+similarities lie within EPS of each other may come out in either order.  Per
+checked row the test requires: k distinct indices, the token itself first,
+the exact similarity of the c-th entry within EPS of the oracle's c-th
+similarity (so the ranking agrees up to near-ties), the reported values
+within EPS of the exact ones, and every token whose similarity clears the
+oracle's k-th by more than EPS present (what is unique must match)."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2606_19528_amd as lm  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+EPS = 2e-5
+
+
+def _announce(msg):
+    print(f"[case] {msg}", file=sys.stderr, flush=True)
+
+
+def _embeddings(V, D, seed):
+    g = torch.Generator().manual_seed(seed)
+    return (torch.randn(V, D, generator=g) * 0.02).to(torch.bfloat16)
+
+
+def _check_rows(orc, W, table, values, k, rows):
+    Wd = W.double().numpy()
+    Ao, Co = orc.topk_table(W, k, rows=rows)
+    nrm = np.linalg.norm(Wd, axis=1)
+    for r, i in enumerate(rows):
+        a = table[i].numpy().astype(np.int64)
+        assert len(set(a.tolist())) == k and a.min() >= 0 and a.max() < W.shape[0], i
+        assert a[0] == i, (i, a[:4])
+        exact = (Wd[a] @ Wd[i]) / (nrm[a] * nrm[i])
+        assert np.max(np.abs(exact - Co[r])) <= EPS, (i, np.max(np.abs(exact - Co[r])))
+        assert np.max(np.abs(values[i].double().numpy() - exact)) <= EPS, i
+        clear = Ao[r][Co[r] > Co[r][-1] + EPS]
+        assert set(clear.tolist()) <= set(a.tolist()), i
+
+
+@pytest.mark.parametrize("shape", [(700, 64, 16), (3000, 128, 50), (9000, 64, 200), (257, 24, 257)])
+def test_topk_table_full(orc, shape):
+    V, D, k = shape
+    _announce(f"topk V={V} D={D} k={k}")
+    W = _embeddings(V, D, seed=V + D)
+    table = torch.empty(V, k, dtype=torch.int32, device="cuda")
+    values = torch.empty(V, k, dtype=torch.float32, device="cuda")
+    lm.topk_table_build(W.cuda(), k, table, values)
+    torch.cuda.synchronize()
+    _check_rows(orc, W, table.cpu(), values.cpu(), k, list(range(V)))
+
+
+def test_topk_table_several_row_batches(orc):
+    # more rows than one batch (16384) and several column chunks; sampled rows
+    V, D, k = 20000, 64, 64
+    _announce(f"topk V={V} D={D} k={k} (sampled rows)")
+    W = _embeddings(V, D, seed=3)
+    table = torch.empty(V, k, dtype=torch.int32, device="cuda")
+    values = torch.empty(V, k, dtype=torch.float32, device="cuda")
+    lm.topk_table_build(W.cuda(), k, table, values)
+    torch.cuda.synchronize()
+    rows = sorted({0, 4095, 4096, 16383, 16384, V - 1, *range(7, V, 997)})
+    _check_rows(orc, W, table.cpu(), values.cpu(), k, rows)
+
+
+def test_topk_table_3b_vocabulary(orc):
+    # the 3B model's output embedding shape, k = 1000; sampled rows
+    V, D, k = 128256, 3072, 1000
+    _announce(f"topk V={V} D={D} k={k} (sampled rows)")
+    W = _embeddings(V, D, seed=5)
+    table = torch.empty(V, k, dtype=torch.int32, device="cuda")
+    values = torch.empty(V, k, dtype=torch.float32, device="cuda")
+    lm.topk_table_build(W.cuda(), k, table, values)
+    torch.cuda.synchronize()
+    _check_rows(orc, W, table.cpu(), values.cpu(), k, [0, 1, 16384, 65537, V - 1])
+
+
+def test_topk_table_deterministic():
+    W = _embeddings(5000, 64, seed=11).cuda()
+    a = lm.topk_table_build(W, 100)
+    b = lm.topk_table_build(W, 100)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
