@@ -48,107 +48,169 @@ __device__ __forceinline__ uint64_t make_key(float v, int32_t j) {
   return ((uint64_t)ordered(v) << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)j);
 }
 
-constexpr int SEL_NT = 512;
-constexpr int SEL_MAX = 8192;  // candidates per row (k + chunk)
+constexpr int SEL_NT = 256, SEL_NW = SEL_NT / 64;  // the histogram has one bucket per thread
+constexpr int SEL_MAX = 8192;  // candidate slots plus sort slots per row
+
+__device__ __forceinline__ uint64_t wave_min_u64(uint64_t v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, off);
+    const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), off);
+    const uint64_t o = ((uint64_t)hi << 32) | lo;
+    v = o < v ? o : v;
+  }
+  return v;
+}
 
 // Per row (one workgroup): the k best of the row's candidates.  final = 0:
-// keep them (in the list's first k slots) and set the threshold to the k-th
-// best similarity; final = 1: sort them (best first) into the table row.
+// keep them (in the list's first k slots, in list order) and set the
+// threshold to the k-th best similarity; final = 1: sort them (best first)
+// into the table row.
+//
+// The k-th largest key is found by an MSB-first radix select, 8 bits a pass:
+// a histogram of the keys that share the prefix chosen so far, then one wave
+// locates the bucket holding the rank-th largest key with a suffix scan over
+// its 256 counts.  The select stops as soon as that bucket holds exactly the
+// keys still needed (usually after three or four passes, once the prefix
+// isolates one similarity value); every key at or above the prefix is then
+// among the k best.
+static_assert(SEL_NT == 256, "one histogram bucket per thread");
 __global__ __launch_bounds__(SEL_NT) void topk_select_kernel(float *cval, int32_t *cidx, int *cnt,
                                                              float *thr, int cap, int k, int final,
                                                              int32_t *table, float *tvals,
                                                              int64_t row0) {
-  __shared__ uint64_t key[SEL_MAX];
-  __shared__ int hist[256];
-  __shared__ int part[SEL_NT];
+  extern __shared__ uint64_t key[];  // [cap] candidates, then (final) [p2] kept keys
+  __shared__ int hist[2][256];
+  __shared__ int wcount[SEL_NW];
+  __shared__ uint64_t wmin[SEL_NW];
   __shared__ uint64_t s_prefix;
-  __shared__ int s_rank;
-  const int row = blockIdx.x, t = threadIdx.x;
+  __shared__ int s_rank, s_done;
+  const int row = blockIdx.x, t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int n = min(cnt[row], cap);
   float *rv = cval + (int64_t)row * cap;
   int32_t *ri = cidx + (int64_t)row * cap;
   if (!final && n <= k) return;
   for (int i = t; i < n; i += SEL_NT) key[i] = make_key(rv[i], ri[i]);
-  __syncthreads();
   uint64_t kth = 0;  // every key >= kth is among the k best (all when n <= k)
   if (n > k) {
-    // MSB-first radix select of the k-th largest key, 8 bits per pass
+    hist[0][t] = 0;
+    hist[1][t] = 0;
     if (t == 0) {
       s_prefix = 0;
       s_rank = k;
+      s_done = 0;
     }
-    for (int shift = 56; shift >= 0; shift -= 8) {
-      for (int b = t; b < 256; b += SEL_NT) hist[b] = 0;
-      __syncthreads();
+    __syncthreads();
+    for (int shift = 56, pb = 0;; shift -= 8, pb ^= 1) {
       const uint64_t prefix = s_prefix;
       const uint64_t hmask = shift == 56 ? 0 : ~0ull << (shift + 8);
-      for (int i = t; i < n; i += SEL_NT)
-        if ((key[i] & hmask) == prefix) atomicAdd(&hist[(key[i] >> shift) & 0xFF], 1);
-      __syncthreads();
-      if (t == 0) {
-        int rank = s_rank, b = 255;
-        while (hist[b] < rank) rank -= hist[b--];
-        s_prefix = prefix | ((uint64_t)b << shift);
-        s_rank = rank;
+      for (int i = t; i < n; i += SEL_NT) {
+        const uint64_t kk = key[i];
+        if ((kk & hmask) == prefix) atomicAdd(&hist[pb][(kk >> shift) & 0xFF], 1);
       }
       __syncthreads();
+      if (wave == 0) {
+        // lane l holds buckets 4l .. 4l+3; above = keys in higher buckets
+        const int rank = s_rank;
+        int h[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) h[j] = hist[pb][4 * lane + j];
+        const int sl = h[0] + h[1] + h[2] + h[3];
+        int x = sl;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+          const int y = __shfl_down(x, off);
+          if (lane + off < 64) x += y;
+        }
+        int above = x - sl;
+#pragma unroll
+        for (int j = 3; j >= 0; --j) {
+          if (above < rank && above + h[j] >= rank) {
+            s_prefix = prefix | ((uint64_t)(4 * lane + j) << shift);
+            s_rank = rank - above;
+            s_done = h[j] == rank - above;
+          }
+          above += h[j];
+        }
+      } else {
+        for (int b = t - 64; b < 256; b += SEL_NT - 64) hist[pb ^ 1][b] = 0;
+      }
+      __syncthreads();
+      if (s_done || shift == 0) break;
     }
     kth = s_prefix;
   }
-  // compact the keys >= kth into the first slots, in list order (block scan)
-  const int per = (n + SEL_NT - 1) / SEL_NT;
-  const int lo = min(n, t * per), hi = min(n, lo + per);
+  // Compact the keys >= kth in list order: each wave takes a contiguous
+  // range, counts its keys by ballot, then writes them after the lower waves'.
+  const int per = ((n + SEL_NW - 1) / SEL_NW + 63) / 64 * 64;
+  const int lo = min(n, wave * per), hi = min(n, lo + per);
   int c = 0;
-  for (int i = lo; i < hi; ++i) c += key[i] >= kth;
-  part[t] = c;
-  __syncthreads();
-  for (int off = 1; off < SEL_NT; off <<= 1) {
-    const int add = t >= off ? part[t - off] : 0;
-    __syncthreads();
-    part[t] += add;
-    __syncthreads();
+  uint64_t mn = ~0ull;
+  for (int i0 = lo; i0 < hi; i0 += 64) {
+    const int i = i0 + lane;
+    const bool keep = i < hi && key[i] >= kth;
+    c += __popcll(__ballot(keep));
+    if (keep) mn = key[i] < mn ? key[i] : mn;
   }
-  int pos = part[t] - c;
-  uint64_t mine[SEL_MAX / SEL_NT];
-  int nm = 0;
-  for (int i = lo; i < hi; ++i)
-    if (key[i] >= kth) mine[nm++] = key[i];
+  mn = wave_min_u64(mn);
+  if (lane == 0) {
+    wcount[wave] = c;
+    wmin[wave] = mn;
+  }
   __syncthreads();
-  for (int q = 0; q < nm; ++q) key[pos + q] = mine[q];
+  int pos = 0;
+  uint64_t kmin = ~0ull;
+  for (int w = 0; w < SEL_NW; ++w) {
+    if (w < wave) pos += wcount[w];
+    kmin = wmin[w] < kmin ? wmin[w] : kmin;
+  }
   const int kept = min(n, k);
-  if (!final) {
-    __syncthreads();
-    for (int i = t; i < kept; i += SEL_NT) {
-      rv[i] = unordered((uint32_t)(key[i] >> 32));
-      ri[i] = (int32_t)(0xFFFFFFFFu - (uint32_t)key[i]);
+  uint64_t *out = key + cap;
+  for (int i0 = lo; i0 < hi; i0 += 64) {
+    const int i = i0 + lane;
+    const bool keep = i < hi && key[i] >= kth;
+    const uint64_t bal = __ballot(keep);
+    if (keep) {
+      const int q = pos + __popcll(bal & ((1ull << lane) - 1));
+      const uint64_t kk = key[i];
+      if (final) {
+        out[q] = kk;
+      } else {
+        rv[q] = unordered((uint32_t)(kk >> 32));
+        ri[q] = (int32_t)(0xFFFFFFFFu - (uint32_t)kk);
+      }
     }
+    pos += __popcll(bal);
+  }
+  if (!final) {
+    // the k-th best similarity: the smallest kept key's value
     if (t == 0) {
       cnt[row] = kept;
-      thr[row] = unordered((uint32_t)(kth >> 32));
+      thr[row] = unordered((uint32_t)(kmin >> 32));
     }
     return;
   }
   // final: bitonic sort of the kept keys, descending (pad with 0 = smallest)
   int p2 = 1;
   while (p2 < kept) p2 <<= 1;
-  for (int i = kept + t; i < p2; i += SEL_NT) key[i] = 0;
+  for (int i = kept + t; i < p2; i += SEL_NT) out[i] = 0;
   __syncthreads();
   for (int size = 2; size <= p2; size <<= 1) {
     for (int stride = size >> 1; stride > 0; stride >>= 1) {
       for (int i = t; i < p2 / 2; i += SEL_NT) {
         const int a = 2 * i - (i & (stride - 1)), b = a + stride;
         const bool desc = (a & size) == 0;
-        const uint64_t ka = key[a], kb = key[b];
+        const uint64_t ka = out[a], kb = out[b];
         if ((ka < kb) == desc) {
-          key[a] = kb;
-          key[b] = ka;
+          out[a] = kb;
+          out[b] = ka;
         }
       }
       __syncthreads();
     }
   }
   for (int i = t; i < k; i += SEL_NT) {
-    const uint64_t kk = i < kept ? key[i] : 0;
+    const uint64_t kk = i < kept ? out[i] : 0;
     table[(row0 + row) * k + i] = i < kept ? (int32_t)(0xFFFFFFFFu - (uint32_t)kk) : -1;
     if (tvals) tvals[(row0 + row) * k + i] = i < kept ? unordered((uint32_t)(kk >> 32)) : 0.0f;
   }
@@ -174,8 +236,17 @@ hipError_t launch_topk_reset(float *thr, int *cnt, int R, hipStream_t st) {
 }
 
 hipError_t launch_topk_select(const TopkArgs &a, int R, int final, hipStream_t st) {
-  if (a.cap > SEL_MAX || a.k > 2048 || a.k < 1) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(topk_select_kernel, dim3(R), dim3(SEL_NT), 0, st, a.val, a.idx, a.cnt, a.thr,
+  if (a.k > 2048 || a.k < 1 || a.cap < a.k) return hipErrorInvalidValue;
+  int p2 = 1;
+  while (p2 < a.k) p2 <<= 1;
+  const int slots = a.cap + (final ? p2 : 0);
+  if (slots > SEL_MAX) return hipErrorInvalidValue;
+  // up to 64 KB of dynamic LDS besides the static part (gfx950: 160 KB per CU)
+  static const hipError_t attr = hipFuncSetAttribute(
+      (const void *)topk_select_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, SEL_MAX * 8);
+  if (attr != hipSuccess) return attr;
+  const size_t lds = (size_t)slots * 8;
+  hipLaunchKernelGGL(topk_select_kernel, dim3(R), dim3(SEL_NT), lds, st, a.val, a.idx, a.cnt, a.thr,
                      a.cap, a.k, final, a.table, a.tvals, a.row0);
   return hipGetLastError();
 }

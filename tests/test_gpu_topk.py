@@ -43,7 +43,8 @@ def _check_rows(orc, W, table, values, k, rows):
         assert set(clear.tolist()) <= set(a.tolist()), i
 
 
-@pytest.mark.parametrize("shape", [(700, 64, 16), (3000, 128, 50), (9000, 64, 200), (257, 24, 257)])
+@pytest.mark.parametrize("shape", [(700, 64, 16), (3000, 128, 50), (9000, 64, 200), (257, 24, 257),
+                                   (2600, 32, 2048)])
 def test_topk_table_full(orc, shape):
     V, D, k = shape
     _announce(f"topk V={V} D={D} k={k}")
