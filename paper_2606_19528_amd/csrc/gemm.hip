@@ -8,10 +8,17 @@
 //
 // Structure of one workgroup (4 or 8 waves, one BM x BN output tile):
 //  * k advances in stages of BKB bytes per row.  Global loads go through
-//    buffer resources (hardware bounds checks instead of per-load branches)
-//    into a ring of RD register sets, then into an LDS ring of NBUF buffers;
-//    a stage's loads are issued RD - 1 steps before its LDS write, which
-//    covers the latency of reads that miss L2.
+//    buffer resources (hardware bounds checks instead of per-load branches).
+//  * DMA = 1 (the bf16 128 x 128 tiles): the loads write LDS directly
+//    (buffer_load ... lds), into a ring of NBUF stages with NBUF - 1 stages
+//    in flight behind the one being read; no registers or LDS-write
+//    instructions are spent on staging.  One load moves 1 KB in lane order, so
+//    the lanes pick their source chunks to produce an XOR-swizzled layout whose
+//    fragment reads are bank-conflict free.
+//  * DMA = 0: loads go into a ring of RD register sets, then into an LDS ring
+//    of NBUF buffers; a stage's loads are issued RD - 1 steps before its LDS
+//    write, which covers the latency of reads that miss L2.  (The quantized-B
+//    path dequantizes in registers on the way into LDS, so it needs this.)
 //  * NBUF = 3: a stage is written to LDS two steps before it is consumed, so
 //    the first k-slice's MFMA fragments of the next stage can be read before
 //    the end-of-step barrier and the MFMAs of a step start without waiting on
@@ -38,6 +45,25 @@ enum { B_ROW = 0, B_KMAJ_REG = 1, B_KMAJ_TR = 2 };
 
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+typedef __attribute__((address_space(3))) void lds_void;
+
+// One direct-to-LDS load: 16 bytes per lane from voffset + soffset of the
+// resource into lds + 16 * lane (lds is the same for the whole wave; M0 holds
+// it).  Written as assembly so that the compiler does not track these LDS
+// writes: its own tracking makes some LDS reads wait for every such load in
+// flight.  Every read of a stage is ordered after its loads by the explicit
+// wait + barrier protocol of the main loop instead.  (No compiler-generated
+// code of these kernels keeps a value in M0.)
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, char *lds, uint32_t voffset,
+                                      int soffset) {
+  const uint32_t base = (uint32_t)(uintptr_t)(lds_void *)lds;
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds" ::"s"(base), "v"(voffset),
+               "s"(rs), "s"(soffset)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
 
 template <int V>
 struct IC {
@@ -54,7 +80,7 @@ __device__ __forceinline__ void static_for(F &&f) {
 }
 
 template <class E, int BM, int BN, int WM, int WN, int WK, int BMODE, int BKB, int NBUF, int RD, int FS,
-          int QB = 0, int EPI = EPI_STORE>
+          int QB = 0, int EPI = EPI_STORE, int DMA = 0>
 __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int group_m,
                                                                  SideArgs side, int nside) {
   typedef typename E::T T;
@@ -80,7 +106,15 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   constexpr int STAGE = A_BYTES + B_BYTES;
   constexpr int OWN = (NB + WK - 1) / WK;    // accumulator blocks owned per wave (k-split)
   constexpr int RED_BYTES = WK > 1 ? WM * WN * WK * OWN * 4096 : 0;
-  constexpr int LDS0 = NBUF * STAGE > RED_BYTES ? NBUF * STAGE : RED_BYTES;
+  // Direct-to-LDS stages (DMA): unpadded rows, chunks swizzled (see dma_stage).
+  constexpr int NWV = NT / 64;
+  constexpr int DA_BYTES = BM * BKB;
+  constexpr int DB_BYTES = BMODE == B_KMAJ_TR ? BKE * BN * 2 : BN * BKB;
+  constexpr int DSTAGE = DA_BYTES + DB_BYTES;
+  constexpr int DA_PW = DA_BYTES / 1024 / NWV, DB_PW = DB_BYTES / 1024 / NWV;  // loads per wave per stage
+  constexpr int IPS = DA_PW + DB_PW;
+  constexpr int RING = DMA ? NBUF * DSTAGE : NBUF * STAGE;
+  constexpr int LDS0 = RING > RED_BYTES ? RING : RED_BYTES;
   constexpr int SIDE = side_lds_bytes<E, WM * WN * WK>();
   constexpr int LDS = LDS0 > SIDE ? LDS0 : SIDE;
   constexpr uint32_t OOB = 0x80000000u;      // offset past every buffer: loads return 0
@@ -88,9 +122,12 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   static_assert(SLICES % WK == 0, "k split");
   static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile");
   static_assert(BMODE != B_KMAJ_TR || ES == 2, "transposed LDS reads are bf16");
-  static_assert(NBUF == 2 || NBUF == 3, "LDS ring depth");
+  static_assert(DMA ? (NBUF == 3 || NBUF == 4) : (NBUF == 2 || NBUF == 3), "LDS ring depth");
+  static_assert(!DMA || (QB == 0 && ES == 2 && FS == 2 && BKB == 128 && BMODE != B_KMAJ_REG &&
+                         DA_BYTES % (1024 * NWV) == 0 && DB_BYTES % (1024 * NWV) == 0),
+                "direct-to-LDS stages: bf16, 64-deep stages, whole 1 KB loads per wave");
   static_assert(RD >= 2 && RD <= 4, "register ring depth");
-  static_assert(!FS || NBUF == 2, "staged fragments use two LDS buffers");
+  static_assert(!FS || DMA || NBUF == 2, "staged fragments use two LDS buffers");
   // Quantized B (QB = 4 or 8 bits): each thread dequantizes one piece of 16
   // consecutive weights of a W row per stage.
   constexpr int QPIECES = BMODE == B_ROW ? BN * (BKE / 16) : BKE * (BN / 16);
@@ -102,6 +139,8 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
                 "quantized B: bf16, staged fragments, one 16-weight piece per thread");
 
   __shared__ __align__(16) char smem[LDS];
+  auto ring_a = [&](auto BUF) -> char * { return smem + decltype(BUF)::value * DSTAGE; };
+  auto ring_b = [&](auto BUF) -> char * { return smem + decltype(BUF)::value * DSTAGE + DA_BYTES; };
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -220,6 +259,47 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
       const int kb = b % (BKE / VEC), nb = b / (BKE / VEC);
       vb[i] = (b < KB_BLK && n0 + nb * VEC < g.N) ? (uint32_t)(kb * VEC * g.ldb * ES + nb * 16)
                                                    : OOB;
+    }
+  }
+
+  // Direct-to-LDS loads: one load instruction of a wave moves 64 x 16 bytes
+  // into 1 KB of LDS in lane order, so the LDS layout is fixed and the lanes
+  // choose which global chunk lands where.  k-contiguous operands (A; B when
+  // row-major): load q of a stage covers tile rows 8q .. 8q+7 (BKB = 128 bytes
+  // each), and row r keeps its 16-byte chunk c at chunk c ^ swz(r),
+  // swz(r) = (r & 7) ^ ((r >> 3) & 1), which puts the fragment reads of eight
+  // and of sixteen consecutive rows in distinct banks.  k-major B: load q
+  // covers k-rows 4q .. 4q+3 (BN * 2 bytes each), chunk c at c ^ 4 (r & 3).
+  const int wv = __builtin_amdgcn_readfirstlane(wave);
+  uint32_t dA[DMA ? DA_PW : 1], dA2[DMA ? DA_PW : 1], dB[DMA ? DB_PW : 1], dB2[DMA ? DB_PW : 1];
+  int dkA[DMA ? DA_PW : 1], dkB[DMA ? DB_PW : 1];
+  if constexpr (DMA) {
+#pragma unroll
+    for (int i = 0; i < DA_PW; ++i) {
+      const int q = wv + i * NWV;
+      const int r = 8 * q + (lane >> 3);
+      const int c = (lane & 7) ^ (lane >> 3) ^ (q & 1);
+      dkA[i] = c * 8;
+      dA[i] = (uint32_t)(r * g.lda * ES + c * 16);
+      dA2[i] = (uint32_t)(r * g.lda2 * ES + c * 16);
+    }
+#pragma unroll
+    for (int i = 0; i < DB_PW; ++i) {
+      const int q = wv + i * NWV;
+      if constexpr (BMODE == B_ROW) {
+        const int r = 8 * q + (lane >> 3);
+        const int c = (lane & 7) ^ (lane >> 3) ^ (q & 1);
+        dkB[i] = c * 8;
+        dB[i] = (uint32_t)(r * g.ldb * ES + c * 16);
+        dB2[i] = (uint32_t)(r * g.ldb2 * ES + c * 16);
+      } else {
+        const int r = 4 * q + (lane >> 4);
+        const int c = (lane & 15) ^ (4 * ((lane >> 4) & 3));
+        const bool ok = n0 + c * 8 < g.N;
+        dkB[i] = 0;
+        dB[i] = ok ? (uint32_t)(r * g.ldb * ES + c * 16) : OOB;
+        dB2[i] = ok ? (uint32_t)(r * g.ldb2 * ES + c * 16) : OOB;
+      }
     }
   }
 
@@ -429,6 +509,39 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
     else store_B(SET, buf);
   };
 
+  // ---- direct-to-LDS loads of stage kt into ring buffer BUF --------------------
+  auto dma_stage = [&](auto BUF, int kt) {
+    if constexpr (DMA) {
+      char *sA = ring_a(BUF);
+      char *sB = ring_b(BUF);
+      const bool lora = is_lora(kt);
+      const int k0 = stage_k0(kt);
+      const int krem = (lora ? g.r : g.K) - k0;  // valid k remaining (uniform)
+      const int soff = k0 * ES;
+      const __amdgpu_buffer_rsrc_t ra_rs = lora ? rsA2 : rsA;
+#pragma unroll
+      for (int i = 0; i < DA_PW; ++i)
+        dma16(ra_rs, sA + (wv + i * NWV) * 1024, dkA[i] < krem ? (lora ? dA2[i] : dA[i]) : (uint32_t)OOB,
+              soff);
+      if constexpr (BMODE == B_ROW) {
+        const __amdgpu_buffer_rsrc_t rb_rs = lora ? rsB2 : rsB;
+#pragma unroll
+        for (int i = 0; i < DB_PW; ++i)
+          dma16(rb_rs, sB + (wv + i * NWV) * 1024,
+                dkB[i] < krem ? (lora ? dB2[i] : dB[i]) : (uint32_t)OOB, soff);
+      } else {
+        const char *base = lora ? (const char *)g.B2 + ((int64_t)k0 * g.ldb2 + n0) * ES
+                                : (const char *)g.B + ((int64_t)k0 * g.ldb + n0) * ES;
+        const int64_t ld = lora ? g.ldb2 : g.ldb;
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+            (void *)base, (short)0, (int)(krem > 0 ? min(krem, BKE) * ld * ES : 0), 0x00020000);
+#pragma unroll
+        for (int i = 0; i < DB_PW; ++i)
+          dma16(rs, sB + (wv + i * NWV) * 1024, lora ? dB2[i] : dB[i], 0);
+      }
+    }
+  };
+
   f32x16 acc[FM][FN];
 #pragma unroll
   for (int i = 0; i < FM; ++i)
@@ -467,6 +580,30 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
       }
     }
   };
+  // Fragment reads from a direct-to-LDS stage (swizzled chunks, see dma_stage).
+  const int swz_a = (lrow & 7) ^ ((lrow >> 3) & 1);
+  const int swz_t = 4 * ((iq >> 2) & 3);
+  auto read_frags_d = [&](auto BUF, int s, Frag &f) {
+    const char *sA = ring_a(BUF);
+    const char *sB = ring_b(BUF);
+    const int sl = wk * SPW + s;
+    const int ca = ((sl * 2 + (lane >> 5)) ^ swz_a) * 16;
+#pragma unroll
+    for (int i = 0; i < FM; ++i) f.a[i] = ld16(sA + (wm * WTM + i * 32 + lrow) * BKB + ca);
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      if constexpr (BMODE == B_KMAJ_TR) {
+        const int n = wn * WTN + j * 32 + tr_n;
+        const char *p = sB + (sl * 16 + tr_k) * (BN * 2) + (((n >> 3) ^ swz_t) * 16) + (n & 7) * 2;
+        i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)p);
+        i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(p + 4 * BN * 2));
+        f.b[j] = u32x4{__builtin_bit_cast(uint2, lo).x, __builtin_bit_cast(uint2, lo).y,
+                       __builtin_bit_cast(uint2, hi).x, __builtin_bit_cast(uint2, hi).y};
+      } else {
+        f.b[j] = ld16(sB + (wn * WTN + j * 32 + lrow) * BKB + ca);
+      }
+    }
+  };
   // D = Bop * Aop^T: D rows are output columns n, D columns are rows m, so each
   // lane ends up holding runs of 4 consecutive n of one output row.
   auto mma_frags = [&](const Frag &f) {
@@ -498,7 +635,67 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   // stages past the end select out-of-range offsets (zeros, no memory traffic)
   // and stores of such stages land in an LDS buffer that is never read again.
   static_assert(!QB || FS, "quantized B runs the staged-fragment schedule");
-  if constexpr (FS) {
+  if constexpr (DMA) {
+    // Ring of NBUF stages filled by direct-to-LDS loads, fragments staged in
+    // registers one step ahead.  Step kt: wait for this wave's loads of stage
+    // kt + 1 and for its LDS reads of the previous step, barrier (stage kt + 1
+    // is then complete for every wave and nobody reads the buffer of stage kt
+    // any more), issue the loads of stage kt + NBUF into that buffer, read the
+    // fragments of stage kt + 1 while the MFMAs of stage kt run.  NBUF - 1
+    // stages stay in flight behind the one being read.  The waits are explicit
+    // (the loads write LDS behind the compiler's back as far as the barrier is
+    // concerned): vmcnt counts this wave's loads in issue order.
+    constexpr int UN = NBUF % 2 == 0 ? NBUF : 2 * NBUF;  // ring buffers and fragment sets static
+    constexpr int W_ENC = (7 << 4) | (15 << 8);           // expcnt, lgkmcnt: no wait
+    Frag F[2][SPW];
+    auto read_stage_d = [&](auto BUF, Frag(&f)[SPW]) {
+#pragma unroll
+      for (int s2 = 0; s2 < SPW; ++s2) read_frags_d(BUF, s2, f[s2]);
+    };
+    auto mma_stage = [&](const Frag(&f)[SPW]) {
+#pragma unroll
+      for (int s2 = 0; s2 < SPW; ++s2) mma_frags(f[s2]);
+    };
+    static_for<0, NBUF>([&](auto SI) { dma_stage(SI, decltype(SI)::value); });
+    {
+      constexpr int V = (NBUF - 1) * IPS;  // stage 0 landed
+      __builtin_amdgcn_s_waitcnt((V & 15) | ((V >> 4) << 14) | W_ENC);
+    }
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    read_stage_d(IC<0>(), F[0]);
+    auto step = [&](auto PH, int kt) {
+      constexpr int P = decltype(PH)::value;  // kt % UN
+      constexpr int V = (NBUF - 2) * IPS;     // stage kt + 1 landed
+      __builtin_amdgcn_s_waitcnt((V & 15) | ((V >> 4) << 14) | (7 << 4));  // and lgkmcnt(0)
+      __builtin_amdgcn_s_barrier();
+      __builtin_amdgcn_sched_barrier(0);
+      dma_stage(IC<P % NBUF>(), kt + NBUF);
+      read_stage_d(IC<(P + 1) % NBUF>(), F[(P + 1) % 2]);
+      mma_stage(F[P % 2]);
+      constexpr int NM = SPW * FM * FN;
+      constexpr int NR = SPW * (FM + FN * (BMODE == B_KMAJ_TR ? 2 : 1));
+      __builtin_amdgcn_sched_group_barrier(0x020, IPS, 0);  // the loads first
+      static_for<0, NM>([&](auto MI) {
+        constexpr int m = decltype(MI)::value;
+        constexpr int r = (m + 1) * NR / NM - m * NR / NM;
+        if constexpr (r > 0) __builtin_amdgcn_sched_group_barrier(0x100, r, 0);  // DS read
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                       // MFMA
+      });
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    int kt = 0;
+    for (; kt + UN <= nk; kt += UN) static_for<0, UN>([&](auto PH) { step(PH, kt + decltype(PH)::value); });
+    static_for<0, UN - 1>([&](auto PH) {
+      constexpr int P = decltype(PH)::value;
+      if (kt + P < nk) step(PH, kt + P);
+    });
+    // The loads of the stages past the end still write LDS: drain them before
+    // the buffers are reused.
+    __builtin_amdgcn_s_waitcnt(0 | W_ENC);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+  } else if constexpr (FS) {
     // Staged fragments: every MFMA fragment of a stage is read from LDS one
     // step ahead into the second of two register sets, so the MFMAs of a
     // step never wait on LDS and the reads of the next stage overlap them.
@@ -882,7 +1079,7 @@ static int pick_group_m(int tiles_m, int tiles_n, int BM, int BN) {
 }
 
 template <class E, int BM, int BN, int WM, int WN, int WK, int BMODE, int BKB, int NBUF, int RD, int FS,
-          int QB = 0, int EPI = EPI_STORE>
+          int QB = 0, int EPI = EPI_STORE, int DMA = 0>
 static hipError_t launch_cfg(const GemmArgs &g, const SideArgs *side, hipStream_t st) {
   const int tm = g.M > 0 ? (g.M + BM - 1) / BM : 0, tn = (g.N + BN - 1) / BN;
   SideArgs sa{};
@@ -893,7 +1090,7 @@ static hipError_t launch_cfg(const GemmArgs &g, const SideArgs *side, hipStream_
   }
   const int grid = tm * tn + nside;
   if (grid == 0) return hipSuccess;
-  hipLaunchKernelGGL((gemm_kernel<E, BM, BN, WM, WN, WK, BMODE, BKB, NBUF, RD, FS, QB, EPI>), dim3(grid),
+  hipLaunchKernelGGL((gemm_kernel<E, BM, BN, WM, WN, WK, BMODE, BKB, NBUF, RD, FS, QB, EPI, DMA>), dim3(grid),
                      dim3(64 * WM * WN * WK), 0, st, g, tm > 0 ? pick_group_m(tm, tn, BM, BN) : 1,
                      sa, nside);
   return hipGetLastError();
@@ -922,13 +1119,13 @@ static int pick_shape(int M, int N) {
 hipError_t launch_gemm_epi(const GemmArgs &g, int epi, hipStream_t st) {
   switch (epi) {
     case EPI_CE_STATS:
-      return launch_cfg<BF16, 128, 128, 2, 2, 2, B_ROW, 128, 2, 3, 2, 0, EPI_CE_STATS>(g, nullptr, st);
+      return launch_cfg<BF16, 128, 128, 2, 2, 2, B_ROW, 128, 3, 3, 2, 0, EPI_CE_STATS, 1>(g, nullptr, st);
     case EPI_CE_DZ:
-      return launch_cfg<BF16, 128, 128, 2, 2, 2, B_ROW, 128, 2, 3, 2, 0, EPI_CE_DZ>(g, nullptr, st);
+      return launch_cfg<BF16, 128, 128, 2, 2, 2, B_ROW, 128, 3, 3, 2, 0, EPI_CE_DZ, 1>(g, nullptr, st);
     case EPI_F32:
-      return launch_cfg<BF16, 128, 128, 2, 2, 2, B_KMAJ_TR, 128, 2, 3, 2, 0, EPI_F32>(g, nullptr, st);
+      return launch_cfg<BF16, 128, 128, 2, 2, 2, B_KMAJ_TR, 128, 4, 3, 2, 0, EPI_F32, 1>(g, nullptr, st);
     case EPI_TOPK:
-      return launch_cfg<BF16, 128, 128, 2, 2, 2, B_ROW, 128, 2, 3, 2, 0, EPI_TOPK>(g, nullptr, st);
+      return launch_cfg<BF16, 128, 128, 2, 2, 2, B_ROW, 128, 3, 3, 2, 0, EPI_TOPK, 1>(g, nullptr, st);
   }
   return hipErrorInvalidValue;
 }
@@ -955,8 +1152,8 @@ hipError_t launch_gemm(const GemmArgs &g, Dtype dt, bool b_kmajor, const SideArg
         return b_kmajor ? launch_cfg<BF16, 256, 128, 4, 2, 1, B_KMAJ_TR, 128, 2, 2, 0>(g, side, st)
                         : launch_cfg<BF16, 256, 128, 4, 2, 1, B_ROW, 128, 2, 2, 0>(g, side, st);
       default:
-        return b_kmajor ? launch_cfg<BF16, 128, 128, 2, 2, 2, B_KMAJ_TR, 128, 2, 3, 2>(g, side, st)
-                        : launch_cfg<BF16, 128, 128, 2, 2, 2, B_ROW, 128, 2, 3, 2>(g, side, st);
+        return b_kmajor ? launch_cfg<BF16, 128, 128, 2, 2, 2, B_KMAJ_TR, 128, 4, 3, 2, 0, EPI_STORE, 1>(g, side, st)
+                        : launch_cfg<BF16, 128, 128, 2, 2, 2, B_ROW, 128, 3, 3, 2, 0, EPI_STORE, 1>(g, side, st);
     }
   }
   return b_kmajor ? launch_cfg<F32, 128, 128, 2, 4, 1, B_KMAJ_REG, 128, 2, 2, 0>(g, side, st)
