@@ -206,7 +206,8 @@ lora_status_t lm_head_reduced_ce(const void *h, const void *W, int64_t T, int64_
  * Row i starts with i itself when no other token points the same way.  The
  * V x V similarities are never stored: a GEMM over a batch of rows and a
  * chunk of columns appends the candidates above each row's running
- * threshold, and a per-row selection keeps the k best after each chunk.
+ * threshold, and a per-row selection keeps the k best whenever a row's
+ * candidate list might not hold another chunk.
  * Similarities are fp32 (bf16 products, fp32 sums): tokens within about
  * 1e-6 of each other may come out in either order.  Requires 1 <= k <=
  * min(V, 2048) and D a multiple of 8; workspace topk_table_workspace_bytes

@@ -225,16 +225,21 @@ CeLayout ce_layout(int64_t T, int64_t D, int64_t nrows, int64_t nJ, bool want_dh
 }
 
 // Top-k table workspace: row norms, and per batch of rows a threshold, a
-// count and a candidate list of k + one column chunk per row.
+// count and a candidate list per row (TOPK_SLOTS minus the sort slots of the
+// final pass: room for k plus at least one column chunk, so that most chunks
+// need no selection).
 constexpr int64_t kTopkChunk = 4096, kTopkBatch = 16384;
 struct TopkLayout {
   size_t rn, thr, cnt, val, idx, total;
-  int64_t R, cap;
+  int64_t R, cap, lazy;
 };
 TopkLayout topk_layout(int64_t V, int64_t k) {
   TopkLayout L{};
   L.R = std::min(V, kTopkBatch);
-  L.cap = k + kTopkChunk;
+  int64_t p2 = 1;
+  while (p2 < k) p2 <<= 1;
+  L.cap = (TOPK_SLOTS - p2) & ~3;  // >= k + kTopkChunk for every k <= 2048; whole vectors of 4
+  L.lazy = L.cap - kTopkChunk;
   size_t off = 0;
   L.rn = off;
   off += round256((size_t)V * 4);
@@ -774,7 +779,7 @@ lora_status_t topk_table_build(const void *W, int64_t V, int64_t D, int64_t k, i
   TopkArgs ta{};
   ta.val = (float *)(wsb + L.val); ta.idx = (int32_t *)(wsb + L.idx);
   ta.cnt = (int *)(wsb + L.cnt); ta.thr = (float *)(wsb + L.thr);
-  ta.cap = (int)L.cap; ta.k = (int)k; ta.table = table; ta.tvals = values;
+  ta.cap = (int)L.cap; ta.k = (int)k; ta.lazy = (int)L.lazy; ta.table = table; ta.tvals = values;
   hipError_t e;
   {
     Timed t(K_TOPK_SIM, st);

@@ -133,7 +133,7 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   constexpr int QPIECES = BMODE == B_ROW ? BN * (BKE / 16) : BKE * (BN / 16);
   static_assert(QB == 0 || QB == 4 || QB == 8, "code width");
   static_assert(EPI == EPI_STORE || (ES == 2 && FS), "cross-entropy / fp32 epilogues: bf16 kernels");
-  static_assert((EPI != EPI_CE_STATS && EPI != EPI_TOPK) || (NT == 4 * BM && BM * (BN + 1) * 4 <= LDS),
+  static_assert((EPI != EPI_CE_STATS && EPI != EPI_TOPK) || (NT == 4 * BM && BM * (BN + 1) * 4 + BN * 4 <= LDS),
                 "row statistics / candidates: four threads per tile row, the fp32 tile in LDS");
   static_assert(QB == 0 || (ES == 2 && FS && BMODE != B_KMAJ_REG && QPIECES == NT),
                 "quantized B: bf16, staged fragments, one 16-weight piece per thread");
@@ -920,11 +920,13 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
     const int ncol = min(BN, g.N - n0);
     const float *zr = zt + row * (BN + 1);
     float mx = -INFINITY;
-    for (int c = sub * CPT; c < min(ncol, (sub + 1) * CPT); ++c) mx = fmaxf(mx, zr[c]);
+#pragma unroll
+    for (int c = sub * CPT; c < (sub + 1) * CPT; ++c) mx = c < ncol ? fmaxf(mx, zr[c]) : mx;
     mx = fmaxf(mx, __shfl_xor(mx, 1));
     mx = fmaxf(mx, __shfl_xor(mx, 2));
     float sm = 0.0f;
-    for (int c = sub * CPT; c < min(ncol, (sub + 1) * CPT); ++c) sm += __expf(zr[c] - mx);
+#pragma unroll
+    for (int c = sub * CPT; c < (sub + 1) * CPT; ++c) sm += c < ncol ? __expf(zr[c] - mx) : 0.0f;
     sm += __shfl_xor(sm, 1);
     sm += __shfl_xor(sm, 2);
     const int m = m0 + row;
@@ -939,10 +941,12 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   if constexpr (EPI == EPI_TOPK) {
     // Cosines c = z * rn_a[m] * rn_b[n] of this tile; every one above the
     // row's threshold is appended to the row's candidate list.  Four threads
-    // share a row: their counts give each its place after one atomic add on
-    // the row's count (the list's order is irrelevant, its content is not).
+    // share a row, each a block of BN / 4 columns: their counts give each its
+    // place after one atomic add on the row's count (the list's order is
+    // irrelevant, its content is not).  The tile's rn_b sits in LDS.
     __syncthreads();
     float *zt = (float *)smem;
+    float *rbs = zt + BM * (BN + 1);
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
       if (WK > 1 && b % WK != wk) continue;
@@ -954,17 +958,22 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
         for (int e = 0; e < 4; ++e)
           zt[row * (BN + 1) + wn * WTN + j * 32 + 8 * q + 4 * (lane >> 5) + e] = acc[i][j][4 * q + e];
     }
+    if (tid < BN) rbs[tid] = n0 + tid < g.N ? g.rn_b[n0 + tid] : 0.0f;
     __syncthreads();
     const int row = tid >> 2, sub = tid & 3;
     constexpr int CPT = BN / 4;
     const int m = m0 + row;
     if (m >= g.M) return;  // all four threads of the row leave together
     const int ncol = min(BN, g.N - n0);
-    const int c_lo = sub * CPT, c_hi = min(ncol, (sub + 1) * CPT);
+    const int c_lo = sub * CPT;
     const float *zr = zt + row * (BN + 1);
     const float ra = g.rn_a[m], th = g.tk_thr[m];
     int mine = 0;
-    for (int c = c_lo; c < c_hi; ++c) mine += zr[c] * ra * g.rn_b[n0 + c] > th;
+#pragma unroll
+    for (int c = 0; c < CPT; ++c) {
+      const int cc = c_lo + c;
+      mine += (cc < ncol) & (zr[cc] * ra * rbs[cc] > th);
+    }
     const int l0 = lane & ~3;
     const int n0c = __shfl(mine, l0), n1c = __shfl(mine, l0 + 1), n2c = __shfl(mine, l0 + 2),
               n3c = __shfl(mine, l0 + 3);
@@ -973,16 +982,17 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
     int base = 0;
     if (sub == 0 && total > 0) base = atomicAdd(g.tk_cnt + m, total);
     base = __shfl(base, l0);
-    if (total == 0) return;
+    if (mine == 0) return;
     int slot = base + before;
     float *vr = g.tk_val + (int64_t)m * g.tk_cap;
     int32_t *ir = g.tk_idx + (int64_t)m * g.tk_cap;
-    for (int c = c_lo; c < c_hi; ++c) {
-      const float v = zr[c] * ra * g.rn_b[n0 + c];
-      if (v > th) {
+    for (int c = 0; c < CPT; ++c) {
+      const int cc = c_lo + c;
+      const float v = zr[cc] * ra * rbs[cc];
+      if (cc < ncol && v > th) {
         if (slot < g.tk_cap) {  // never past the list (the sizes rule it out)
           vr[slot] = v;
-          ir[slot] = g.col0 + n0 + c;
+          ir[slot] = g.col0 + n0 + cc;
         }
         ++slot;
       }

@@ -126,12 +126,18 @@ hipError_t launch_ce_combine(const float *tmax, const float *tsum, int ntiles, i
                              const float *ztgt, float *lse, float *loss, float *total,
                              hipStream_t st);
 // Top-k similarity table: per-row candidate lists of a batch of rows.
+// Candidate slots per row of the selection: a list holds TOPK_SLOTS - p2(k)
+// entries rounded down to a multiple of 4, p2(k) the power of two at or
+// above k (at least k + 4096 for every k <= 2048).
+constexpr int TOPK_SLOTS = 8192;
 struct TopkArgs {
   float *val;
   int32_t *idx;
   int *cnt;
   float *thr;
   int cap, k;
+  int lazy;        // a non-final pass selects only rows with more candidates
+                   // than this (the list then still has room for a chunk)
   int32_t *table;  // [V][k], rows row0 .. row0 + R - 1 written by the final select
   float *tvals;    // optional [V][k]
   int64_t row0;

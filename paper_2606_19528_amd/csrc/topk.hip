@@ -4,9 +4,11 @@
 //   * the similarity GEMM runs over a batch of rows and one chunk of columns
 //     at a time; its epilogue (gemm.hip, EPI_TOPK) appends to each row's
 //     candidate list every cosine above the row's current threshold;
-//   * after each chunk, topk_select_kernel keeps each row's k best
-//     candidates (exact radix select on 64-bit keys: similarity, then the
-//     smaller token index) and raises its threshold to the k-th best;
+//   * after each chunk, topk_select_kernel keeps the k best candidates of
+//     each row whose list might not hold another chunk (exact radix select on
+//     64-bit keys: similarity, then the smaller token index) and raises its
+//     threshold to the k-th best; with lists much longer than k + one chunk
+//     a row is selected a handful of times instead of after every chunk;
 //   * after the last chunk, the same kernel sorts the k best and writes the
 //     table row.
 // The candidate set after a chunk does not depend on the order of the
@@ -49,7 +51,7 @@ __device__ __forceinline__ uint64_t make_key(float v, int32_t j) {
 }
 
 constexpr int SEL_NT = 256, SEL_NW = SEL_NT / 64;  // the histogram has one bucket per thread
-constexpr int SEL_MAX = 8192;  // candidate slots plus sort slots per row
+constexpr int SEL_MAX = TOPK_SLOTS;
 
 __device__ __forceinline__ uint64_t wave_min_u64(uint64_t v) {
 #pragma unroll
@@ -63,36 +65,76 @@ __device__ __forceinline__ uint64_t wave_min_u64(uint64_t v) {
 }
 
 // Per row (one workgroup): the k best of the row's candidates.  final = 0:
-// keep them (in the list's first k slots, in list order) and set the
-// threshold to the k-th best similarity; final = 1: sort them (best first)
-// into the table row.
+// rows with at most `lazy` candidates are left alone (their list still has
+// room for the next chunk; the threshold stays where it was, which only lets
+// more candidates in); the others keep their k best (in the list's first k
+// slots) and set the threshold to the k-th best similarity.  final = 1: sort
+// the k best (best first) into the table row.
 //
-// The k-th largest key is found by an MSB-first radix select, 8 bits a pass:
-// a histogram of the keys that share the prefix chosen so far, then one wave
-// locates the bucket holding the rank-th largest key with a suffix scan over
-// its 256 counts.  The select stops as soon as that bucket holds exactly the
-// keys still needed (usually after three or four passes, once the prefix
-// isolates one similarity value); every key at or above the prefix is then
-// among the k best.
+// Each thread holds its candidates in registers: slots 4 (t + 256 q) + e,
+// read four at a time (the list length is a multiple of 4, so a vector
+// never leaves the list).  Key 0 marks an empty slot (every real key is
+// larger).  The k-th largest key is found by an MSB-first radix select over
+// the keys minus the row's smallest, up to 8 bits a pass starting at the top
+// bit of their span: a histogram in LDS of the keys that share the prefix
+// chosen so far, then one wave locates the bucket holding the rank-th largest
+// key with a suffix scan over the 256 counts.  The select stops as soon as
+// that bucket holds exactly the keys still needed (usually after two
+// passes); every key at or above the prefix is then among the k best.  The
+// kept keys are written out wave by wave in a fixed order.
+constexpr int SEL_Q = SEL_MAX / (4 * SEL_NT);  // vectors of 4 slots per thread
 static_assert(SEL_NT == 256, "one histogram bucket per thread");
 __global__ __launch_bounds__(SEL_NT) void topk_select_kernel(float *cval, int32_t *cidx, int *cnt,
-                                                             float *thr, int cap, int k, int final,
-                                                             int32_t *table, float *tvals,
+                                                             float *thr, int cap, int k, int lazy,
+                                                             int final, int32_t *table, float *tvals,
                                                              int64_t row0) {
-  extern __shared__ uint64_t key[];  // [cap] candidates, then (final) [p2] kept keys
+  __shared__ uint64_t out[2048];  // final: the kept keys, sorted in place
   __shared__ int hist[2][256];
   __shared__ int wcount[SEL_NW];
-  __shared__ uint64_t wmin[SEL_NW];
+  __shared__ uint64_t wmin[SEL_NW], wmax[SEL_NW];
   __shared__ uint64_t s_prefix;
   __shared__ int s_rank, s_done;
   const int row = blockIdx.x, t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int n = min(cnt[row], cap);
   float *rv = cval + (int64_t)row * cap;
   int32_t *ri = cidx + (int64_t)row * cap;
-  if (!final && n <= k) return;
-  for (int i = t; i < n; i += SEL_NT) key[i] = make_key(rv[i], ri[i]);
-  uint64_t kth = 0;  // every key >= kth is among the k best (all when n <= k)
+  if (!final && n <= (lazy > k ? lazy : k)) return;  // room left for the next chunk
+  uint64_t key[SEL_Q][4];
+#pragma unroll
+  for (int q = 0; q < SEL_Q; ++q) {
+    const int b = 4 * (t + SEL_NT * q);
+    if (b < n) {
+      const float4 v = *(const float4 *)(rv + b);
+      const int4 x = *(const int4 *)(ri + b);
+      key[q][0] = make_key(v.x, x.x);
+      key[q][1] = b + 1 < n ? make_key(v.y, x.y) : 0;
+      key[q][2] = b + 2 < n ? make_key(v.z, x.z) : 0;
+      key[q][3] = b + 3 < n ? make_key(v.w, x.w) : 0;
+    } else {
+      key[q][0] = key[q][1] = key[q][2] = key[q][3] = 0;
+    }
+  }
+  uint64_t kth = 1;  // every key >= kth is among the k best (all real keys when n <= k)
   if (n > k) {
+    // The digits are taken from the key minus the row's smallest key, the
+    // first one from the top bit of the span, so the first histogram spreads
+    // over the keys' actual range (similarities share their sign and most of
+    // their exponent bits, which would put nearly every key in one bucket).
+    uint64_t lo = ~0ull, hi = 0;
+#pragma unroll
+    for (int q = 0; q < SEL_Q; ++q)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint64_t kk = key[q][e];
+        lo = (kk != 0 && kk < lo) ? kk : lo;
+        hi = kk > hi ? kk : hi;
+      }
+    lo = wave_min_u64(lo);
+    hi = ~wave_min_u64(~hi);
+    if (lane == 0) {
+      wmin[wave] = lo;
+      wmax[wave] = hi;
+    }
     hist[0][t] = 0;
     hist[1][t] = 0;
     if (t == 0) {
@@ -101,13 +143,27 @@ __global__ __launch_bounds__(SEL_NT) void topk_select_kernel(float *cval, int32_
       s_done = 0;
     }
     __syncthreads();
-    for (int shift = 56, pb = 0;; shift -= 8, pb ^= 1) {
-      const uint64_t prefix = s_prefix;
-      const uint64_t hmask = shift == 56 ? 0 : ~0ull << (shift + 8);
-      for (int i = t; i < n; i += SEL_NT) {
-        const uint64_t kk = key[i];
-        if ((kk & hmask) == prefix) atomicAdd(&hist[pb][(kk >> shift) & 0xFF], 1);
-      }
+#pragma unroll
+    for (int w = 0; w < SEL_NW; ++w) {
+      lo = wmin[w] < lo ? wmin[w] : lo;
+      hi = wmax[w] > hi ? wmax[w] : hi;
+    }
+    const int top = 63 - __clzll(hi - lo);  // keys are distinct and n >= 2, so hi > lo
+    // Pass: digit = bits [shift, shift + width) of key - lo among the keys
+    // whose bits above them equal the prefix chosen so far.
+    int width = top < 8 ? top + 1 : 8;
+    int shift = top + 1 - width;
+    for (int pb = 0;; pb ^= 1) {
+      const uint64_t prefix = s_prefix;  // chosen bits above shift + width, in place
+      const uint64_t hmask = shift + width >= 64 ? 0 : ~0ull << (shift + width);
+      const uint32_t dmask = (1u << width) - 1;
+#pragma unroll
+      for (int q = 0; q < SEL_Q; ++q)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const uint64_t r = key[q][e] - lo;
+          if (key[q][e] != 0 && (r & hmask) == prefix) atomicAdd(&hist[pb][(r >> shift) & dmask], 1);
+        }
       __syncthreads();
       if (wave == 0) {
         // lane l holds buckets 4l .. 4l+3; above = keys in higher buckets
@@ -137,21 +193,23 @@ __global__ __launch_bounds__(SEL_NT) void topk_select_kernel(float *cval, int32_
       }
       __syncthreads();
       if (s_done || shift == 0) break;
+      width = shift < 8 ? shift : 8;
+      shift -= width;
     }
-    kth = s_prefix;
+    kth = lo + s_prefix;
   }
-  // Compact the keys >= kth in list order: each wave takes a contiguous
-  // range, counts its keys by ballot, then writes them after the lower waves'.
-  const int per = ((n + SEL_NW - 1) / SEL_NW + 63) / 64 * 64;
-  const int lo = min(n, wave * per), hi = min(n, lo + per);
+  // Write the keys >= kth: each wave counts its kept keys, then writes them
+  // after the lower waves' (per vector slot q, element e, lane order).
   int c = 0;
   uint64_t mn = ~0ull;
-  for (int i0 = lo; i0 < hi; i0 += 64) {
-    const int i = i0 + lane;
-    const bool keep = i < hi && key[i] >= kth;
-    c += __popcll(__ballot(keep));
-    if (keep) mn = key[i] < mn ? key[i] : mn;
-  }
+#pragma unroll
+  for (int q = 0; q < SEL_Q; ++q)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const bool keep = key[q][e] >= kth;
+      c += __popcll(__ballot(keep));
+      mn = keep && key[q][e] < mn ? key[q][e] : mn;
+    }
   mn = wave_min_u64(mn);
   if (lane == 0) {
     wcount[wave] = c;
@@ -160,28 +218,30 @@ __global__ __launch_bounds__(SEL_NT) void topk_select_kernel(float *cval, int32_
   __syncthreads();
   int pos = 0;
   uint64_t kmin = ~0ull;
+#pragma unroll
   for (int w = 0; w < SEL_NW; ++w) {
     if (w < wave) pos += wcount[w];
     kmin = wmin[w] < kmin ? wmin[w] : kmin;
   }
   const int kept = min(n, k);
-  uint64_t *out = key + cap;
-  for (int i0 = lo; i0 < hi; i0 += 64) {
-    const int i = i0 + lane;
-    const bool keep = i < hi && key[i] >= kth;
-    const uint64_t bal = __ballot(keep);
-    if (keep) {
-      const int q = pos + __popcll(bal & ((1ull << lane) - 1));
-      const uint64_t kk = key[i];
-      if (final) {
-        out[q] = kk;
-      } else {
-        rv[q] = unordered((uint32_t)(kk >> 32));
-        ri[q] = (int32_t)(0xFFFFFFFFu - (uint32_t)kk);
+#pragma unroll
+  for (int q = 0; q < SEL_Q; ++q)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const uint64_t kk = key[q][e];
+      const bool keep = kk >= kth;
+      const uint64_t bal = __ballot(keep);
+      if (keep) {
+        const int o = pos + __popcll(bal & ((1ull << lane) - 1));
+        if (final) {
+          out[o] = kk;
+        } else {
+          rv[o] = unordered((uint32_t)(kk >> 32));
+          ri[o] = (int32_t)(0xFFFFFFFFu - (uint32_t)kk);
+        }
       }
+      pos += __popcll(bal);
     }
-    pos += __popcll(bal);
-  }
   if (!final) {
     // the k-th best similarity: the smallest kept key's value
     if (t == 0) {
@@ -236,18 +296,10 @@ hipError_t launch_topk_reset(float *thr, int *cnt, int R, hipStream_t st) {
 }
 
 hipError_t launch_topk_select(const TopkArgs &a, int R, int final, hipStream_t st) {
-  if (a.k > 2048 || a.k < 1 || a.cap < a.k) return hipErrorInvalidValue;
-  int p2 = 1;
-  while (p2 < a.k) p2 <<= 1;
-  const int slots = a.cap + (final ? p2 : 0);
-  if (slots > SEL_MAX) return hipErrorInvalidValue;
-  // up to 64 KB of dynamic LDS besides the static part (gfx950: 160 KB per CU)
-  static const hipError_t attr = hipFuncSetAttribute(
-      (const void *)topk_select_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, SEL_MAX * 8);
-  if (attr != hipSuccess) return attr;
-  const size_t lds = (size_t)slots * 8;
-  hipLaunchKernelGGL(topk_select_kernel, dim3(R), dim3(SEL_NT), lds, st, a.val, a.idx, a.cnt, a.thr,
-                     a.cap, a.k, final, a.table, a.tvals, a.row0);
+  if (a.k > 2048 || a.k < 1 || a.cap < a.k || a.lazy > a.cap || a.cap > SEL_MAX || a.cap % 4)
+    return hipErrorInvalidValue;
+  hipLaunchKernelGGL(topk_select_kernel, dim3(R), dim3(SEL_NT), 0, st, a.val, a.idx, a.cnt, a.thr,
+                     a.cap, a.k, a.lazy, final, a.table, a.tvals, a.row0);
   return hipGetLastError();
 }
 

@@ -299,10 +299,12 @@ def test_ckpt_sizes_and_rejects():
 def test_topk_table_sizes_and_rejects():
     lib = lm.lib()
     w = lib.topk_table_workspace_bytes
-    # norms + per batch of rows (at most 16384) k + 4096 candidates per row
+    # norms + per batch of rows (at most 16384) 8192 - 1024 candidate slots per
+    # row (k = 1000: the final sort takes 1024), which exceeds k + one chunk
     n = w(128256, 3072, 1000)
     R = 16384
-    assert R * (1000 + 4096) * 8 <= n <= R * (1000 + 4096) * 8 + 128256 * 4 + 2 * R * 4 + 6 * 256
+    assert R * 7168 * 8 <= n <= R * 7168 * 8 + 128256 * 4 + 2 * R * 4 + 6 * 256
+    assert w(5000, 64, 2048) >= 5000 * 6144 * 8 and 6144 >= 2048 + 4096
     assert w(1000, 64, 1001) == BAD and w(5000, 64, 2049) == BAD and w(100, 12, 5) == BAD
     t = lib.topk_table_build
     assert t(None, 1000, 64, 10, P(2), None, P(3), 1 << 30, None) == EINVAL
