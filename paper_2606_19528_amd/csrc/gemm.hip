@@ -53,13 +53,17 @@ typedef __attribute__((address_space(3))) void lds_void;
 // writes: its own tracking makes some LDS reads wait for every such load in
 // flight.  Every read of a stage is ordered after its loads by the explicit
 // wait + barrier protocol of the main loop instead.  (No compiler-generated
-// code of these kernels keeps a value in M0.)
+// code of these kernels keeps a value in M0.)  The compiler does not look
+// into the assembly for hazards, so it carries its own wait states: five
+// before the load may read SGPRs that a vector instruction wrote, one
+// between the write of M0 and the load that reads it.
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
 __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, char *lds, uint32_t voffset,
                                       int soffset) {
   const uint32_t base = (uint32_t)(uintptr_t)(lds_void *)lds;
-  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds" ::"s"(base), "v"(voffset),
+  asm volatile("s_nop 4\n\ts_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds" ::"s"(base),
+               "v"(voffset),
                "s"(rs), "s"(soffset)
                : "memory", "m0");
 }
@@ -108,8 +112,12 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   constexpr int RED_BYTES = WK > 1 ? WM * WN * WK * OWN * 4096 : 0;
   // Direct-to-LDS stages (DMA): unpadded rows, chunks swizzled (see dma_stage).
   constexpr int NWV = NT / 64;
+  // Row-major B is loaded in whole loads per wave (rows past BN read zeros);
+  // k-major B rows take 256 bytes in LDS (columns past BN read zeros).
+  constexpr int DB_ROWS = (BN + 8 * NWV - 1) / (8 * NWV) * (8 * NWV);
+  constexpr int DBRB = (BN * 2 + 255) / 256 * 256;
   constexpr int DA_BYTES = BM * BKB;
-  constexpr int DB_BYTES = BMODE == B_KMAJ_TR ? BKE * BN * 2 : BN * BKB;
+  constexpr int DB_BYTES = BMODE == B_KMAJ_TR ? BKE * DBRB : DB_ROWS * BKB;
   constexpr int DSTAGE = DA_BYTES + DB_BYTES;
   constexpr int DA_PW = DA_BYTES / 1024 / NWV, DB_PW = DB_BYTES / 1024 / NWV;  // loads per wave per stage
   constexpr int IPS = DA_PW + DB_PW;
@@ -124,7 +132,8 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   static_assert(BMODE != B_KMAJ_TR || ES == 2, "transposed LDS reads are bf16");
   static_assert(DMA ? (NBUF == 3 || NBUF == 4) : (NBUF == 2 || NBUF == 3), "LDS ring depth");
   static_assert(!DMA || (QB == 0 && ES == 2 && FS == 2 && BKB == 128 && BMODE != B_KMAJ_REG &&
-                         DA_BYTES % (1024 * NWV) == 0 && DB_BYTES % (1024 * NWV) == 0),
+                         DA_BYTES % (1024 * NWV) == 0 && DB_BYTES % (1024 * NWV) == 0 &&
+                         (BMODE != B_KMAJ_TR || DBRB == 256)),
                 "direct-to-LDS stages: bf16, 64-deep stages, whole 1 KB loads per wave");
   static_assert(RD >= 2 && RD <= 4, "register ring depth");
   static_assert(!FS || DMA || NBUF == 2, "staged fragments use two LDS buffers");
@@ -295,7 +304,7 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
       } else {
         const int r = 4 * q + (lane >> 4);
         const int c = (lane & 15) ^ (4 * ((lane >> 4) & 3));
-        const bool ok = n0 + c * 8 < g.N;
+        const bool ok = c * 8 < BN && n0 + c * 8 < g.N;
         dkB[i] = 0;
         dB[i] = ok ? (uint32_t)(r * g.ldb * ES + c * 16) : OOB;
         dB2[i] = ok ? (uint32_t)(r * g.ldb2 * ES + c * 16) : OOB;
@@ -594,9 +603,9 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
     for (int j = 0; j < FN; ++j) {
       if constexpr (BMODE == B_KMAJ_TR) {
         const int n = wn * WTN + j * 32 + tr_n;
-        const char *p = sB + (sl * 16 + tr_k) * (BN * 2) + (((n >> 3) ^ swz_t) * 16) + (n & 7) * 2;
+        const char *p = sB + (sl * 16 + tr_k) * DBRB + (((n >> 3) ^ swz_t) * 16) + (n & 7) * 2;
         i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)p);
-        i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(p + 4 * BN * 2));
+        i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(p + 4 * DBRB));
         f.b[j] = u32x4{__builtin_bit_cast(uint2, lo).x, __builtin_bit_cast(uint2, lo).y,
                        __builtin_bit_cast(uint2, hi).x, __builtin_bit_cast(uint2, hi).y};
       } else {
