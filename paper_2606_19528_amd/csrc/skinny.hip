@@ -56,22 +56,43 @@ __global__ __launch_bounds__(64 * ROW_NW) void row_skinny_kernel(RowArgs a) {
   const T *Xp = (const T *)a.X;
   const T *Vp = (const T *)a.V;
 
-  // Optional copy job (LoRA-step operands repeated once per segment).
-  if (a.bcopy_mode != BCOPY_NONE) {
-    const T *src = (const T *)a.bcopy_src;
-    T *dst = (T *)a.bcopy_dst;
-    const int64_t wg = (int64_t)blockIdx.y * gridDim.x + blockIdx.x;
-    const int64_t stride = (int64_t)gridDim.x * gridDim.y * NT;
+  // Optional copy job (LoRA-step operands repeated once per segment).  In
+  // 16-byte vectors when the repetition keeps whole vectors together: each
+  // thread loads its first CPV vectors here and stores them after the main
+  // work, so their latency hides behind the main loads instead of delaying
+  // them; further vectors, and the element-wise form, are copied at the end.
+  constexpr int CPV = 2;
+  const T *csrc = (const T *)a.bcopy_src;
+  T *cdst = (T *)a.bcopy_dst;
+  const int64_t cg = ((int64_t)blockIdx.y * gridDim.x + blockIdx.x) * NT + tid;
+  const int64_t cstride = (int64_t)gridDim.x * gridDim.y * NT;
+  const int crep = a.nsplit * r;
+  const bool cvec = (a.bcopy_mode == BCOPY_COLS && r % VEC == 0 && a.ldt % VEC == 0) ||
+                    (a.bcopy_mode == BCOPY_FLAT && a.bcopy_period % VEC == 0 && a.bcopy_elems % VEC == 0);
+  const int64_t cnv = !cvec ? 0
+                      : a.bcopy_mode == BCOPY_COLS ? (int64_t)a.bcopy_rows * (a.ldt / VEC)
+                                                   : a.bcopy_elems / VEC;
+  // vector v: destination element d, source element s (-1: zeros)
+  auto cmap = [&](int64_t v, int64_t &d, int64_t &sidx) {
     if (a.bcopy_mode == BCOPY_COLS) {
-      const int rep = a.nsplit * r;
-      const int64_t total = (int64_t)a.bcopy_rows * a.ldt;
-      for (int64_t i = wg * NT + tid; i < total; i += stride) {
-        const int64_t n = i / a.ldt;
-        const int c = (int)(i % a.ldt);
-        dst[i] = c < rep ? src[n * r + c % r] : (T)0;
-      }
+      const int64_t n = v / (a.ldt / VEC);
+      const int c0 = (int)(v % (a.ldt / VEC)) * VEC;
+      d = n * a.ldt + c0;
+      sidx = c0 < crep ? n * r + c0 % r : -1;
     } else {
-      for (int64_t i = wg * NT + tid; i < a.bcopy_elems; i += stride) dst[i] = src[i % a.bcopy_period];
+      d = v * VEC;
+      sidx = d % a.bcopy_period;
+    }
+  };
+  u32x4 cval[CPV];
+#pragma unroll
+  for (int q = 0; q < CPV; ++q) {
+    const int64_t v = cg + q * cstride;
+    cval[q] = zero16();
+    if (v < cnv) {
+      int64_t d, si;
+      cmap(v, d, si);
+      if (si >= 0) cval[q] = ld16(csrc + si);
     }
   }
 
@@ -175,6 +196,33 @@ __global__ __launch_bounds__(64 * ROW_NW) void row_skinny_kernel(RowArgs a) {
       if (tail) tail[(int64_t)(m0 + mm) * a.ldt + p * r + c] = E::from_float(a.tail_mult * s);
     } else {
       tail[(int64_t)(m0 + mm) * a.ldt + pad_lo + (c - r)] = (T)0;
+    }
+  }
+  // the copy job: held vectors, then the rest
+#pragma unroll
+  for (int q = 0; q < CPV; ++q) {
+    const int64_t v = cg + q * cstride;
+    if (v < cnv) {
+      int64_t d, si;
+      cmap(v, d, si);
+      st16(cdst + d, cval[q]);
+    }
+  }
+  for (int64_t v = cg + CPV * cstride; v < cnv; v += cstride) {
+    int64_t d, si;
+    cmap(v, d, si);
+    st16(cdst + d, si >= 0 ? ld16(csrc + si) : zero16());
+  }
+  if (a.bcopy_mode != BCOPY_NONE && !cvec) {
+    if (a.bcopy_mode == BCOPY_COLS) {
+      const int64_t total = (int64_t)a.bcopy_rows * a.ldt;
+      for (int64_t i = cg; i < total; i += cstride) {
+        const int64_t n = i / a.ldt;
+        const int c = (int)(i % a.ldt);
+        cdst[i] = c < crep ? csrc[n * r + c % r] : (T)0;
+      }
+    } else {
+      for (int64_t i = cg; i < a.bcopy_elems; i += cstride) cdst[i] = csrc[i % a.bcopy_period];
     }
   }
 }
