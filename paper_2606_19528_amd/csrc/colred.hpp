@@ -86,43 +86,61 @@ __device__ void side_item(const SideArgs &s, int item, char *smem) {
 #pragma unroll
     for (int jb = 0; jb < JB; ++jb) acc[q][jb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  auto step = [&](int tb) {
-    u32x4 xin[VEC], xt[VEC];
+  // Loads go through buffer resources based at the step's first token row
+  // (so every offset stays small whatever T is): rows past T and columns past
+  // L (or rank indices past r) read zeros without branches.  The loads of a
+  // token step are issued one step ahead of its MFMAs.
+  constexpr uint32_t OOB = 0x80000000u;
+  constexpr int ES = (int)sizeof(T);
+  struct Step {
+    u32x4 x[VEC];
+    float v[JB][VEC];
+  };
+  auto load = [&](int tb, Step &st) {
+    const int rows = min(ROWS, t_end - tb);  // <= 0 past the end: nothing is read
+    const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(Xp + (int64_t)tb * job.ldx), (short)0, rows > 0 ? rows * job.ldx * ES : 0, 0x00020000);
 #pragma unroll
-    for (int i = 0; i < VEC; ++i) {
-      const int t = tb + g * VEC + i;
-      xin[i] = (t < t_end && col < job.L) ? ld16(Xp + (int64_t)t * job.ldx + col) : zero16();
-    }
-    u32x4 vf[JB];
+    for (int i = 0; i < VEC; ++i)
+      st.x[i] = __builtin_bit_cast(
+          u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                     rx, col < job.L ? (uint32_t)(((g * VEC + i) * job.ldx + col) * ES) : OOB, 0, 0));
+    // V and its further partial sums, added in ascending order (uniform loop)
+    for (int q = 0; q < job.vparts; ++q) {
+      const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+          (void *)(job.V + (int64_t)q * job.vstride + (int64_t)tb * r), (short)0, rows > 0 ? rows * r * 4 : 0,
+          0x00020000);
 #pragma unroll
-    for (int jb = 0; jb < JB; ++jb) {
-      const int j = jg + jb * 16 + cl;
-      float f[VEC];
+      for (int jb = 0; jb < JB; ++jb) {
+        const int j = jg + jb * 16 + cl;
 #pragma unroll
-      for (int e = 0; e < VEC; ++e) {
-        const int t = tb + g * VEC + e;
-        float part[MAX_SPLIT];  // all loads issued before the first add
-        const bool ok = t < t_end && j < r;
-        const float *src = job.V + (int64_t)t * r + j;
-#pragma unroll
-        for (int q = 0; q < MAX_SPLIT; ++q) part[q] = (ok && q < job.vparts) ? src[q * job.vstride] : 0.0f;
-        float v = part[0];
-#pragma unroll
-        for (int q = 1; q < MAX_SPLIT; ++q)
-          if (q < job.vparts) v += part[q];
-        f[e] = v;
+        for (int e = 0; e < VEC; ++e) {
+          const uint32_t off = j < r ? (uint32_t)(((g * VEC + e) * r + j) * 4) : OOB;
+          const float v = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rv, off, 0, 0));
+          st.v[jb][e] = q == 0 ? v : st.v[jb][e] + v;
+        }
       }
-      vf[jb] = pack_vec(E(), f);
     }
-    transpose_block(E(), xin, xt);
+  };
+  auto compute = [&](const Step &st) {
+    u32x4 xt[VEC], vf[JB];
+#pragma unroll
+    for (int jb = 0; jb < JB; ++jb) vf[jb] = pack_vec(E(), st.v[jb]);
+    transpose_block(E(), st.x, xt);
 #pragma unroll
     for (int q = 0; q < VEC; ++q)
 #pragma unroll
       for (int jb = 0; jb < JB; ++jb) mma16(E(), acc[q][jb], xt[q], vf[jb]);
   };
-  for (int tb = wave * ROWS; tb < t_end; tb += 2 * NW * ROWS) {
-    step(tb);
-    if (tb + NW * ROWS < t_end) step(tb + NW * ROWS);
+  {
+    Step cur, nxt;
+    int tb = __builtin_amdgcn_readfirstlane(wave) * ROWS;
+    load(tb, cur);
+    for (; tb < t_end; tb += NW * ROWS) {
+      load(tb + NW * ROWS, nxt);  // past the end: zeros, no memory traffic
+      compute(cur);
+      cur = nxt;
+    }
   }
 
   // Pairwise tree over waves: in round h the upper half of the active waves
