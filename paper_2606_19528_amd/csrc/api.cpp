@@ -136,8 +136,8 @@ FwdLayout fwd_layout(int64_t T, int64_t K, int64_t N, int64_t r, lora_dtype_t dt
   FwdLayout L{};
   if (r == 0) return L;
   const Dtype d = dt == LORA_BF16 ? DT_BF16 : DT_F32;
-  L.ldt = tail_ld((int)r, d);
   L.sp = row_split(T, K, (int)r, d);
+  L.ldt = tail_ld(L.sp.nsplit * (int)r, d);
   size_t off = 0;
   L.u = off;  // partial sums of u = x A^T, [nsplit][T][r] fp32
   off += round256((size_t)L.sp.nsplit * T * r * 4);
@@ -158,9 +158,9 @@ BwdLayout bwd_layout(int64_t T, int64_t K, int64_t N, int64_t r, lora_dtype_t dt
   BwdLayout L{};
   if (r == 0) return L;
   const Dtype d = dt == LORA_BF16 ? DT_BF16 : DT_F32;
-  L.ldt = tail_ld((int)r, d);
   L.sp_u = row_split(T, K, (int)r, d);
   L.sp_du = row_split(T, N, (int)r, d);
+  L.ldt = tail_ld(L.sp_du.nsplit * (int)r, d);
   size_t off = 0;
   L.u = off;  // partial sums of u (when it is recomputed)
   off += round256((size_t)L.sp_u.nsplit * T * r * 4);
@@ -362,7 +362,7 @@ lora_status_t fwd_impl(const void *x, const void *W, const void *qc, const float
     RowArgs ra{};
     ra.X = x; ra.ldx = d_in; ra.M = (int)T; ra.L = (int)d_in;
     ra.V = A; ra.ldv = d_in; ra.vmode = V_ROW; ra.r = (int)r;
-    ra.nsplit = ns; ra.seg = L.sp.seg;
+    ra.nsplit = ns; ra.seg = L.sp.seg; ra.mb = L.sp.mb;
     ra.out_mult = 1.0f; ra.out = (ns == 1 && u_save) ? u_save : upart; ra.out_stride = T * r;
     ra.tail = wsb + L.utail; ra.ldt = L.ldt; ra.tail_mult = scale;
     // B itself serves as the LoRA-step operand when there is one partial and
@@ -458,7 +458,7 @@ lora_status_t bwd_impl(const void *x, const void *W, const void *qc, const float
     RowArgs ra{};
     ra.X = x; ra.ldx = d_in; ra.M = (int)T; ra.L = (int)d_in;
     ra.V = A; ra.ldv = d_in; ra.vmode = V_ROW; ra.r = (int)r;
-    ra.nsplit = L.sp_u.nsplit; ra.seg = L.sp_u.seg;
+    ra.nsplit = L.sp_u.nsplit; ra.seg = L.sp_u.seg; ra.mb = L.sp_u.mb;
     ra.out_mult = 1.0f; ra.out = (float *)(wsb + L.u); ra.out_stride = T * r;
     Timed t(K_LORA_DOWN, st);
     e = launch_row_skinny(ra, d, st);
@@ -473,7 +473,7 @@ lora_status_t bwd_impl(const void *x, const void *W, const void *qc, const float
     RowArgs ra{};
     ra.X = dy; ra.ldx = d_out; ra.M = (int)T; ra.L = (int)d_out;
     ra.V = B; ra.ldv = r; ra.vmode = V_KMAJ_TR; ra.r = (int)r;
-    ra.nsplit = ns; ra.seg = L.sp_du.seg;
+    ra.nsplit = ns; ra.seg = L.sp_du.seg; ra.mb = L.sp_du.mb;
     ra.out_mult = scale; ra.out = du; ra.out_stride = T * r;
     ra.tail = wsb + L.dutail; ra.ldt = L.ldt; ra.tail_mult = scale;
     if (ns > 1) {  // A repeated once per partial of du

@@ -197,16 +197,22 @@ struct RowArgs {
   void *bcopy_dst;
   int bcopy_rows;
   int64_t bcopy_period, bcopy_elems;
+  int mb;  // row tiles of 16 per workgroup: 1 (0), 2 or 4 (bf16, r <= 32)
 };
 hipError_t launch_row_skinny(const RowArgs &a, Dtype dt, hipStream_t st);
 
-// Split of a row-skinny product over its reduction axis L: enough segments to
-// give the T / 16 row blocks about one workgroup per CU, no more than fit in
-// the padded LoRA step (nsplit * r <= ldt), each segment at least one
-// 128-byte chunk per wave, and at most MAX_SPLIT segments.
+// Split of a row-skinny product over its reduction axis L, and rows per
+// workgroup.  Short T (below 2048): one 16-row tile per workgroup, enough
+// segments to give the T / 16 row blocks about one workgroup per CU, no more
+// than fit in the 64-wide padded LoRA step (nsplit * r <= tail_ld(r)).  Long
+// T (bf16, r <= 32 and a multiple of 8): up to four 16-row tiles per
+// workgroup, so each chunk of
+// the rank-r factor serves up to 64 rows, and up to 4 segments (the same
+// LoRA-step bound) for about 256 workgroups.  Always: each segment at least
+// one 128-byte chunk per wave, and at most MAX_SPLIT segments.
 constexpr int MAX_SPLIT = 8;
 struct RowSplit {
-  int nsplit, seg;
+  int nsplit, seg, mb;
 };
 RowSplit row_split(int64_t T, int64_t L, int r, Dtype dt);
 

@@ -33,7 +33,7 @@ typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr int ROW_NW = 8;  // waves per workgroup
 
-template <class E, int JB, int VMODE, int U>
+template <class E, int JB, int VMODE, int U, int MB>
 __global__ __launch_bounds__(64 * ROW_NW) void row_skinny_kernel(RowArgs a) {
   constexpr int NW = ROW_NW, NT = 64 * NW;
   typedef typename E::T T;
@@ -42,14 +42,15 @@ __global__ __launch_bounds__(64 * ROW_NW) void row_skinny_kernel(RowArgs a) {
   constexpr int R16 = JB * 16;
   constexpr int RSB = R16 * 2;              // LDS row of a staged B chunk (bf16)
   constexpr int REGION = U * CE * RSB;      // per-wave staging region
-  constexpr int RED = NW * 16 * (R16 + 1) * 4;
+  constexpr int RM = 16 * MB;                // rows per workgroup
+  constexpr int RED = NW * RM * (R16 + 1) * 4;
   constexpr int LDS = (VMODE == V_KMAJ_TR && NW * REGION > RED) ? NW * REGION : RED;
   __shared__ __align__(16) char smem[LDS];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int m0 = blockIdx.x * 16;
+  const int m0 = blockIdx.x * RM;
   const int p = blockIdx.y;  // segment of the reduction axis
-  const int row = m0 + (lane & 15);
+  const int row = m0 + (lane & 15);  // of row tile 0; tile mt adds 16 mt
   const int g = lane >> 4;
   const int M = a.M, r = a.r;
   const int k_lo = p * a.seg, k_hi = min(a.L, k_lo + a.seg);
@@ -96,13 +97,15 @@ __global__ __launch_bounds__(64 * ROW_NW) void row_skinny_kernel(RowArgs a) {
     }
   }
 
-  f32x4 acc[JB];
+  f32x4 acc[MB][JB];
 #pragma unroll
-  for (int jb = 0; jb < JB; ++jb) acc[jb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int mt = 0; mt < MB; ++mt)
+#pragma unroll
+    for (int jb = 0; jb < JB; ++jb) acc[mt][jb] = f32x4{0.f, 0.f, 0.f, 0.f};
   char *region = smem + wave * REGION;
 
   for (int kc0 = k_lo + wave * CE; kc0 < k_hi; kc0 += NW * CE * U) {
-    u32x4 xf[U][2];
+    u32x4 xf[U][MB][2];
     u32x4 vf[U][2][JB];
     // issue every global load of the U chunks first
 #pragma unroll
@@ -111,7 +114,10 @@ __global__ __launch_bounds__(64 * ROW_NW) void row_skinny_kernel(RowArgs a) {
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const int k = kc + h * 4 * VEC + g * VEC;
-        xf[u][h] = (row < M && k < k_hi) ? ld16(Xp + (int64_t)row * a.ldx + k) : zero16();
+#pragma unroll
+        for (int mt = 0; mt < MB; ++mt)
+          xf[u][mt][h] = (row + 16 * mt < M && k < k_hi) ? ld16(Xp + (int64_t)(row + 16 * mt) * a.ldx + k)
+                                                        : zero16();
         if constexpr (VMODE == V_ROW) {
 #pragma unroll
           for (int jb = 0; jb < JB; ++jb) {
@@ -167,17 +173,21 @@ __global__ __launch_bounds__(64 * ROW_NW) void row_skinny_kernel(RowArgs a) {
 #pragma unroll
       for (int h = 0; h < 2; ++h)
 #pragma unroll
-        for (int jb = 0; jb < JB; ++jb) mma16(E(), acc[jb], xf[u][h], vf[u][h][jb]);
+        for (int jb = 0; jb < JB; ++jb)
+#pragma unroll
+          for (int mt = 0; mt < MB; ++mt) mma16(E(), acc[mt][jb], xf[u][mt][h], vf[u][h][jb]);
   }
 
   // D[m][n]: m = 4 (lane / 16) + i, n = lane % 16.  Sum the waves' tiles.
   __syncthreads();
   float *red = (float *)smem;
 #pragma unroll
-  for (int jb = 0; jb < JB; ++jb)
+  for (int mt = 0; mt < MB; ++mt)
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      red[(wave * 16 + g * 4 + i) * (R16 + 1) + jb * 16 + (lane & 15)] = acc[jb][i];
+    for (int jb = 0; jb < JB; ++jb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        red[(wave * RM + mt * 16 + g * 4 + i) * (R16 + 1) + jb * 16 + (lane & 15)] = acc[mt][jb][i];
   __syncthreads();
   // Segment p owns columns p*r .. p*r + r-1 of the tail; the last segment
   // also writes its zero padding.
@@ -185,13 +195,13 @@ __global__ __launch_bounds__(64 * ROW_NW) void row_skinny_kernel(RowArgs a) {
   float *out = a.out + (int64_t)p * a.out_stride;
   const int pad_lo = a.nsplit * r;
   const int ncol = (tail && p == a.nsplit - 1) ? r + (a.ldt - pad_lo) : r;
-  for (int idx = tid; idx < 16 * ncol; idx += NT) {
+  for (int idx = tid; idx < RM * ncol; idx += NT) {
     const int mm = idx / ncol, c = idx % ncol;
     if (m0 + mm >= M) continue;
     if (c < r) {
-      float s = red[(0 * 16 + mm) * (R16 + 1) + c];
+      float s = red[(0 * RM + mm) * (R16 + 1) + c];
 #pragma unroll
-      for (int w = 1; w < NW; ++w) s += red[(w * 16 + mm) * (R16 + 1) + c];
+      for (int w = 1; w < NW; ++w) s += red[(w * RM + mm) * (R16 + 1) + c];
       out[(int64_t)(m0 + mm) * r + c] = a.out_mult * s;
       if (tail) tail[(int64_t)(m0 + mm) * a.ldt + p * r + c] = E::from_float(a.tail_mult * s);
     } else {
@@ -227,46 +237,82 @@ __global__ __launch_bounds__(64 * ROW_NW) void row_skinny_kernel(RowArgs a) {
   }
 }
 
-template <class E, int VMODE>
+template <class E, int VMODE, int MB>
 static hipError_t row_dispatch(const RowArgs &a, hipStream_t st) {
-  dim3 grid((a.M + 15) / 16, a.nsplit), block(64 * ROW_NW);
+  dim3 grid((a.M + 16 * MB - 1) / (16 * MB), a.nsplit), block(64 * ROW_NW);
   const int jb = (a.r + 15) / 16;
-#define ROWSK(J)                                                                                  \
-  case J:                                                                                         \
-    hipLaunchKernelGGL((row_skinny_kernel<E, J, VMODE, (J <= 2 ? 4 : 1)>), grid, block, 0, st, a); \
+#define ROWSK(J)                                                                                      \
+  case J:                                                                                             \
+    hipLaunchKernelGGL((row_skinny_kernel<E, J, VMODE, (J <= 2 ? 4 : 1), MB>), grid, block, 0, st, a); \
     break;
-  switch (jb) {
-    ROWSK(1) ROWSK(2) ROWSK(3) ROWSK(4) ROWSK(5) ROWSK(6) ROWSK(7) ROWSK(8)
-    default:
-      return hipErrorInvalidValue;
+  if constexpr (MB == 1) {
+    switch (jb) {
+      ROWSK(1) ROWSK(2) ROWSK(3) ROWSK(4) ROWSK(5) ROWSK(6) ROWSK(7) ROWSK(8)
+      default:
+        return hipErrorInvalidValue;
+    }
+  } else {
+    switch (jb) {  // several row tiles: ranks up to 32
+      ROWSK(1) ROWSK(2)
+      default:
+        return hipErrorInvalidValue;
+    }
   }
 #undef ROWSK
   return hipGetLastError();
+}
+
+template <class E, int VMODE>
+static hipError_t row_dispatch_mb(const RowArgs &a, hipStream_t st) {
+  switch (a.mb) {
+    case 0:
+    case 1:
+      return row_dispatch<E, VMODE, 1>(a, st);
+    case 2:
+      return row_dispatch<E, VMODE, 2>(a, st);
+    case 4:
+      return row_dispatch<E, VMODE, 4>(a, st);
+  }
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_row_skinny(const RowArgs &a, Dtype dt, hipStream_t st) {
   if (a.r < 1 || a.r > 128 || a.nsplit < 1 || a.nsplit > MAX_SPLIT || a.seg < 1) return hipErrorInvalidValue;
   if ((int64_t)(a.nsplit - 1) * a.seg >= a.L || (int64_t)a.nsplit * a.seg < a.L) return hipErrorInvalidValue;
   if (a.tail && a.nsplit * a.r > a.ldt) return hipErrorInvalidValue;
+  if (a.mb > 1 && (a.r > 32 || dt != DT_BF16)) return hipErrorInvalidValue;
   if (dt == DT_BF16) {
-    if (a.vmode == V_ROW) return row_dispatch<BF16, V_ROW>(a, st);
-    if (a.r % 8 == 0) return row_dispatch<BF16, V_KMAJ_TR>(a, st);
-    return row_dispatch<BF16, V_KMAJ_GATHER>(a, st);
+    if (a.vmode == V_ROW) return row_dispatch_mb<BF16, V_ROW>(a, st);
+    if (a.r % 8 == 0) return row_dispatch_mb<BF16, V_KMAJ_TR>(a, st);
+    return row_dispatch_mb<BF16, V_KMAJ_GATHER>(a, st);
   }
-  if (a.vmode == V_ROW) return row_dispatch<F32, V_ROW>(a, st);
-  return row_dispatch<F32, V_KMAJ_GATHER>(a, st);
+  if (a.vmode == V_ROW) return row_dispatch<F32, V_ROW, 1>(a, st);
+  return row_dispatch<F32, V_KMAJ_GATHER, 1>(a, st);
 }
 
 RowSplit row_split(int64_t T, int64_t L, int r, Dtype dt) {
-  const int64_t blocks = (T + 15) / 16;
   const int ce = dt == DT_BF16 ? 64 : 32;  // elements per 128-byte chunk
+  const int64_t max_by_l = std::max<int64_t>(1, (L + (int64_t)ROW_NW * ce - 1) / ((int64_t)ROW_NW * ce));
+  auto make = [&](int64_t s, int mb) {
+    s = std::max<int64_t>(1, std::min<int64_t>(s, max_by_l));
+    const int64_t seg = ((L + s - 1) / s + ce - 1) / ce * ce;
+    return RowSplit{(int)((L + seg - 1) / seg), (int)seg, mb};
+  };
+  if (dt == DT_BF16 && r <= 32 && r % 8 == 0 && T >= 2048) {
+    // (at most 4 partial sums: every dA / dB side item reads all of them)
+    const int64_t smax = std::min<int64_t>({(int64_t)4, std::max(1, tail_ld(r, dt) / r), max_by_l});
+    for (int mb : {4, 2}) {
+      const int64_t blocks = (T + 16 * mb - 1) / (16 * mb);
+      if (blocks * smax >= 256) return make((256 + blocks - 1) / blocks, mb);
+    }
+    const int64_t blocks = (T + 15) / 16;
+    return make(std::min<int64_t>(smax, (256 + blocks - 1) / blocks), 1);
+  }
+  const int64_t blocks = (T + 15) / 16;
   int64_t s = (256 + blocks - 1) / blocks;
   s = std::min<int64_t>(s, std::max(1, tail_ld(r, dt) / r));
   s = std::min<int64_t>(s, MAX_SPLIT);
-  s = std::min<int64_t>(s, (L + (int64_t)ROW_NW * ce - 1) / ((int64_t)ROW_NW * ce));
-  s = std::max<int64_t>(s, 1);
-  const int64_t seg = ((L + s - 1) / s + ce - 1) / ce * ce;
-  return RowSplit{(int)((L + seg - 1) / seg), (int)seg};
+  return make(s, 1);
 }
 
 }  // namespace lora

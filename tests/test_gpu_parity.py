@@ -70,6 +70,15 @@ def test_split_reduction(orc, shape, recompute, dtype):
     _case(orc, T, K, N, r, 2.0 * r, seed=41, dtype=dtype, recompute=recompute)
 
 
+# Long T: the rank-r row products take several 16-row tiles per workgroup
+# (ragged last block, rank not a multiple of 16, u rematerialised).
+@pytest.mark.parametrize("shape,recompute", [((2100, 1032, 776, 24), False), ((2100, 1032, 776, 24), True),
+                                             ((4100, 520, 1288, 8), True), ((2048, 3072, 1032, 32), False)])
+def test_long_t_row_tiles(orc, shape, recompute):
+    T, K, N, r = shape
+    _case(orc, T, K, N, r, 2.0 * r, seed=53, recompute=recompute)
+
+
 def test_split_forward_without_u_save(orc):
     # the partial sums of u stay in the workspace; y must not depend on u_save
     T, K, N, r = 256, 1800, 1032, 16
