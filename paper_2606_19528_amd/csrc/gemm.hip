@@ -1125,14 +1125,14 @@ int side_workgroups(const SideArgs &s, Dtype dt) {
 // Tile shape per problem: an estimate of the time of each candidate -- full
 // waves of tiles over the 256 CUs times the per-tile cost (relative per-CU
 // throughput measured on MI355X at T = 2048 and 4096 over the shapes of the
-// Llama and Qwen layers: 128x128 (direct-to-LDS) 0.82, 256x128 0.70,
-// 256x256 1.0).
+// Llama and Qwen layers: 128x128 and 256x128 (both direct-to-LDS) 0.82 and
+// 0.97, 256x256 (register-staged) 1.0).
 static int pick_shape(int M, int N) {
   auto cost = [&](int bm, int bn, double eff) {
     const long tiles = (long)((M + bm - 1) / bm) * ((N + bn - 1) / bn);
     return (double)((tiles + 255) / 256) * bm * bn / eff;
   };
-  const double c0 = cost(128, 128, 0.82), c1 = cost(256, 128, 0.70), c2 = cost(256, 256, 1.0);
+  const double c0 = cost(128, 128, 0.82), c1 = cost(256, 128, 0.97), c2 = cost(256, 256, 1.0);
   if (c2 <= c1 && c2 <= c0) return 2;
   return c1 < c0 ? 1 : 0;
 }
@@ -1170,8 +1170,8 @@ hipError_t launch_gemm(const GemmArgs &g, Dtype dt, bool b_kmajor, const SideArg
         return b_kmajor ? launch_cfg<BF16, 256, 256, 4, 2, 1, B_KMAJ_TR, 128, 2, 2, 0>(g, side, st)
                         : launch_cfg<BF16, 256, 256, 4, 2, 1, B_ROW, 128, 2, 2, 0>(g, side, st);
       case 1:
-        return b_kmajor ? launch_cfg<BF16, 256, 128, 4, 2, 1, B_KMAJ_TR, 128, 2, 2, 0>(g, side, st)
-                        : launch_cfg<BF16, 256, 128, 4, 2, 1, B_ROW, 128, 2, 2, 0>(g, side, st);
+        return b_kmajor ? launch_cfg<BF16, 256, 128, 4, 2, 1, B_KMAJ_TR, 128, 3, 3, 2, 0, EPI_STORE, 1>(g, side, st)
+                        : launch_cfg<BF16, 256, 128, 4, 2, 1, B_ROW, 128, 3, 3, 2, 0, EPI_STORE, 1>(g, side, st);
       default:
         return b_kmajor ? launch_cfg<BF16, 128, 128, 2, 2, 2, B_KMAJ_TR, 128, 4, 3, 2, 0, EPI_STORE, 1>(g, side, st)
                         : launch_cfg<BF16, 128, 128, 2, 2, 2, B_ROW, 128, 3, 3, 2, 0, EPI_STORE, 1>(g, side, st);
