@@ -1123,16 +1123,18 @@ int side_workgroups(const SideArgs &s, Dtype dt) {
 }
 
 // Tile shape per problem: an estimate of the time of each candidate -- full
-// waves of tiles over the 256 CUs times the per-tile cost (relative per-CU
+// waves of tiles over the 256 CUs times the per-tile cost.  Relative per-CU
 // throughput measured on MI355X at T = 2048 and 4096 over the shapes of the
-// Llama and Qwen layers: 128x128 and 256x128 (both direct-to-LDS) 0.82 and
-// 0.97, 256x256 (register-staged) 1.0).
-static int pick_shape(int M, int N) {
+// Llama and Qwen layers, for 128x128 and 256x128 (both direct-to-LDS) and
+// 256x256 (register-staged): row-major B 0.84 : 0.99 : 1.0; k-major B (the
+// transposed reads cost the small tile more) 0.76 : 1.04 : 1.0.
+static int pick_shape(int M, int N, bool b_kmajor) {
   auto cost = [&](int bm, int bn, double eff) {
     const long tiles = (long)((M + bm - 1) / bm) * ((N + bn - 1) / bn);
     return (double)((tiles + 255) / 256) * bm * bn / eff;
   };
-  const double c0 = cost(128, 128, 0.82), c1 = cost(256, 128, 0.97), c2 = cost(256, 256, 1.0);
+  const double c0 = cost(128, 128, b_kmajor ? 0.76 : 0.84), c1 = cost(256, 128, b_kmajor ? 1.04 : 0.99),
+               c2 = cost(256, 256, 1.0);
   if (c2 <= c1 && c2 <= c0) return 2;
   return c1 < c0 ? 1 : 0;
 }
@@ -1165,7 +1167,7 @@ hipError_t launch_gemm_q(const GemmArgs &g, int bits, bool b_kmajor, const SideA
 hipError_t launch_gemm(const GemmArgs &g, Dtype dt, bool b_kmajor, const SideArgs *side,
                        hipStream_t st) {
   if (dt == DT_BF16) {
-    switch (pick_shape(g.M, g.N)) {
+    switch (pick_shape(g.M, g.N, b_kmajor)) {
       case 2:
         return b_kmajor ? launch_cfg<BF16, 256, 256, 4, 2, 1, B_KMAJ_TR, 128, 2, 2, 0>(g, side, st)
                         : launch_cfg<BF16, 256, 256, 4, 2, 1, B_ROW, 128, 2, 2, 0>(g, side, st);
