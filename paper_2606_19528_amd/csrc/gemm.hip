@@ -613,6 +613,60 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
       }
     }
   };
+  // One direct-to-LDS load (q < IPS) of stage kt into ring buffer BUF.
+  auto dma_one = [&](auto BUF, int kt, auto QI) __attribute__((always_inline)) {
+    if constexpr (DMA) {
+      constexpr int q = decltype(QI)::value;
+      const bool lora = is_lora(kt);
+      const int k0 = stage_k0(kt);
+      const int krem = (lora ? g.r : g.K) - k0;
+      const int soff = k0 * ES;
+      if constexpr (q < DA_PW) {
+        const __amdgpu_buffer_rsrc_t ra_rs = lora ? rsA2 : rsA;
+        dma16(ra_rs, ring_a(BUF) + (wv + q * NWV) * 1024, dkA[q] < krem ? (lora ? dA2[q] : dA[q]) : (uint32_t)OOB,
+              soff);
+      } else {
+        constexpr int i = q - DA_PW;
+        if constexpr (BMODE == B_ROW) {
+          const __amdgpu_buffer_rsrc_t rb_rs = lora ? rsB2 : rsB;
+          dma16(rb_rs, ring_b(BUF) + (wv + i * NWV) * 1024,
+                dkB[i] < krem ? (lora ? dB2[i] : dB[i]) : (uint32_t)OOB, soff);
+        } else {
+          const char *base = lora ? (const char *)g.B2 + ((int64_t)k0 * g.ldb2 + n0) * ES
+                                  : (const char *)g.B + ((int64_t)k0 * g.ldb + n0) * ES;
+          const int64_t ld = lora ? g.ldb2 : g.ldb;
+          const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+              (void *)base, (short)0, (int)(krem > 0 ? min(krem, BKE) * ld * ES : 0), 0x00020000);
+          dma16(rs, ring_b(BUF) + (wv + i * NWV) * 1024, lora ? dB2[i] : dB[i], 0);
+        }
+      }
+    }
+  };
+  // One fragment read (ri < SPW * (FM + FN)) of a direct-to-LDS stage.
+  auto read_one_d = [&](auto BUF, auto RI, Frag *f) __attribute__((always_inline)) {
+    constexpr int ri = decltype(RI)::value;
+    constexpr int s2 = ri / (FM + FN), w = ri % (FM + FN);
+    const char *sA = ring_a(BUF);
+    const char *sB = ring_b(BUF);
+    const int sl = wk * SPW + s2;
+    if constexpr (w < FM) {
+      const int ca = ((sl * 2 + (lane >> 5)) ^ swz_a) * 16;
+      f[s2].a[w] = ld16(sA + (wm * WTM + w * 32 + lrow) * BKB + ca);
+    } else {
+      constexpr int j = w - FM;
+      if constexpr (BMODE == B_KMAJ_TR) {
+        const int n = wn * WTN + j * 32 + tr_n;
+        const char *pp = sB + (sl * 16 + tr_k) * DBRB + (((n >> 3) ^ swz_t) * 16) + (n & 7) * 2;
+        i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)pp);
+        i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(pp + 4 * DBRB));
+        f[s2].b[j] = u32x4{__builtin_bit_cast(uint2, lo).x, __builtin_bit_cast(uint2, lo).y,
+                           __builtin_bit_cast(uint2, hi).x, __builtin_bit_cast(uint2, hi).y};
+      } else {
+        const int ca = ((sl * 2 + (lane >> 5)) ^ swz_a) * 16;
+        f[s2].b[j] = ld16(sB + (wn * WTN + j * 32 + lrow) * BKB + ca);
+      }
+    }
+  };
   // D = Bop * Aop^T: D rows are output columns n, D columns are rows m, so each
   // lane ends up holding runs of 4 consecutive n of one output row.
   auto mma_frags = [&](const Frag &f) {
@@ -673,18 +727,26 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
     read_stage_d(IC<0>(), F[0]);
-    auto step = [&](auto PH, int kt) {
+    auto step = [&](auto PH, int kt) __attribute__((always_inline)) {
       constexpr int P = decltype(PH)::value;  // kt % UN
       constexpr int V = (NBUF - 2) * IPS;     // stage kt + 1 landed
       __builtin_amdgcn_s_waitcnt((V & 15) | ((V >> 4) << 14) | (7 << 4));  // and lgkmcnt(0)
       __builtin_amdgcn_s_barrier();
       __builtin_amdgcn_sched_barrier(0);
-      dma_stage(IC<P % NBUF>(), kt + NBUF);
-      read_stage_d(IC<(P + 1) % NBUF>(), F[(P + 1) % 2]);
+      // The loads of stage kt + NBUF are spread between the fragment reads of
+      // stage kt + 1 (in source order: an LDS read cannot pass the load
+      // assembly), so the load path, the LDS and the matrix cores work side by
+      // side instead of all loads queueing at the top of the step.
+      constexpr int NRO = SPW * (FM + FN);
+      static_for<0, NRO>([&](auto RI) {
+        constexpr int ri = decltype(RI)::value;
+        read_one_d(IC<(P + 1) % NBUF>(), RI, F[(P + 1) % 2]);
+        static_for<ri * IPS / NRO, (ri + 1) * IPS / NRO>(
+            [&](auto QI) { dma_one(IC<P % NBUF>(), kt + NBUF, QI); });
+      });
       mma_stage(F[P % 2]);
       constexpr int NM = SPW * FM * FN;
       constexpr int NR = SPW * (FM + FN * (BMODE == B_KMAJ_TR ? 2 : 1));
-      __builtin_amdgcn_sched_group_barrier(0x020, IPS, 0);  // the loads first
       static_for<0, NM>([&](auto MI) {
         constexpr int m = decltype(MI)::value;
         constexpr int r = (m + 1) * NR / NM - m * NR / NM;
