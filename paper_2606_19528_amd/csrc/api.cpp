@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -127,15 +128,57 @@ lora_status_t check_shapes(int64_t T, int64_t d_in, int64_t d_out, int64_t r, lo
 // Workspace layouts (offsets in bytes, 256-byte aligned).  The rank-r row
 // products are computed as `nsplit` partial sums over their reduction axis
 // (row_split); the LoRA-step operands hold one column block per partial.
+//
+// The forward's rank-r pass (u = x A^T) runs fused into the GEMM launch -- as
+// producer workgroups ahead of the tiles, each over whole rows of x -- when
+// the operands are bf16, r is a multiple of 8 up to 32 and the GEMM takes a
+// direct-to-LDS tile configuration; it then needs no partial sums and no
+// padded copy of B, and the workspace starts with the hand-over words of the
+// launch.  (The backward keeps its rank-r pass over dy as a kernel of its
+// own: the dA / dB side items that need it would have to wait in CUs the dx
+// tiles need, and fewer producers make that pass slow.)
+bool fuse_ok(int64_t T, int64_t N, int64_t r, lora_dtype_t dt) {
+  return dt == LORA_BF16 && r >= 8 && r <= 32 && r % 8 == 0 && gemm_fusable((int)T, (int)N);
+}
+// Tag of a fused launch: distinct for every call of this process, never 0.
+unsigned int next_gen() {
+  static std::atomic<unsigned int> g{0};
+  unsigned int v;
+  do {
+    v = ++g;
+  } while (v == 0);
+  return v;
+}
+// One segment over the whole reduction axis L, 16 rows per workgroup.
+RowSplit whole_rows(int64_t L, Dtype d) {
+  const int64_t ce = d == DT_BF16 ? 64 : 32;
+  return RowSplit{1, (int)((L + ce - 1) / ce * ce), 1};
+}
+
 struct FwdLayout {
-  size_t u, utail, bpad, total;
+  size_t sync, u, utail, bpad, total;
   int ldt;
+  bool fused;
   RowSplit sp;
 };
 FwdLayout fwd_layout(int64_t T, int64_t K, int64_t N, int64_t r, lora_dtype_t dt) {
   FwdLayout L{};
   if (r == 0) return L;
   const Dtype d = dt == LORA_BF16 ? DT_BF16 : DT_F32;
+  L.fused = fuse_ok(T, N, r, dt);
+  if (L.fused) {
+    L.sp = whole_rows(K, d);
+    L.ldt = tail_ld((int)r, d);
+    size_t off = 0;
+    L.sync = off;  // hand-over words
+    off += 256;
+    L.u = off;  // u = x A^T when the caller does not keep it, [T][r] fp32
+    off += round256((size_t)T * r * 4);
+    L.utail = off;  // [T][ldt]: E(s * u), zero-padded
+    off += round256((size_t)T * L.ldt * esize(dt));
+    L.total = off;
+    return L;
+  }
   L.sp = row_split(T, K, (int)r, d);
   L.ldt = tail_ld(L.sp.nsplit * (int)r, d);
   size_t off = 0;
@@ -158,7 +201,9 @@ BwdLayout bwd_layout(int64_t T, int64_t K, int64_t N, int64_t r, lora_dtype_t dt
   BwdLayout L{};
   if (r == 0) return L;
   const Dtype d = dt == LORA_BF16 ? DT_BF16 : DT_F32;
-  L.sp_u = row_split(T, K, (int)r, d);
+  // A recomputed u is summed exactly as the forward pass summed it (whole
+  // rows when the forward runs fused), so it is bitwise the saved one.
+  L.sp_u = fuse_ok(T, N, r, dt) ? whole_rows(K, d) : row_split(T, K, (int)r, d);
   L.sp_du = row_split(T, N, (int)r, d);
   L.ldt = tail_ld(L.sp_du.nsplit * (int)r, d);
   size_t off = 0;
@@ -354,6 +399,28 @@ lora_status_t fwd_impl(const void *x, const void *W, const void *qc, const float
   g.B = W; g.ldb = d_in;
   g.M = (int)T; g.N = (int)d_out; g.K = (int)d_in;
   g.C = y; g.ldc = d_out;
+  if (r > 0 && !qc && fwd_layout(T, d_in, d_out, r, dt).fused) {
+    const FwdLayout L = fwd_layout(T, d_in, d_out, r, dt);
+    char *wsb = (char *)ws;
+    FuseArgs fz{};
+    RowArgs &ra = fz.row;
+    ra.X = x; ra.ldx = d_in; ra.M = (int)T; ra.L = (int)d_in;
+    ra.V = A; ra.ldv = d_in; ra.vmode = V_ROW; ra.r = (int)r;
+    ra.nsplit = 1; ra.seg = L.sp.seg; ra.mb = 1;
+    ra.out_mult = 1.0f; ra.out = u_save ? u_save : (float *)(wsb + L.u); ra.out_stride = T * r;
+    ra.tail = wsb + L.utail; ra.ldt = L.ldt; ra.tail_mult = scale;
+    fz.nprod = (int)((T + 15) / 16);
+    fz.sync = (unsigned long long *)(wsb + L.sync);
+    fz.gen = next_gen();
+    g.A2 = wsb + L.utail; g.lda2 = L.ldt;
+    g.B2 = B; g.ldb2 = r;  // rows of r bf16: whole 16-byte vectors
+    g.r = (int)r;
+    Timed t(K_GEMM_FWD, st);
+    hipError_t e = launch_gemm_fused(g, &fz, st);
+    t.done();
+    if (e != hipSuccess) return hip_fail(e, "gemm_fwd launch");
+    return LORA_OK;
+  }
   if (r > 0) {
     const FwdLayout L = fwd_layout(T, d_in, d_out, r, dt);
     const int ns = L.sp.nsplit;

@@ -36,6 +36,7 @@
 #include <type_traits>
 
 #include "colred.hpp"
+#include "rowprod.hpp"
 #include "kernels.hpp"
 #include "launch.hpp"
 
@@ -69,6 +70,49 @@ __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, char *lds, uint
 }
 #pragma clang diagnostic pop
 
+// ---- hand-over of a fused rank-r pass (protocol in launch.hpp, FuseArgs) ------
+constexpr unsigned long long FZ_BUDGET = 20000000ull;  // 0.2 s of the 100 MHz real-time counter
+
+__device__ __forceinline__ unsigned long long fz_load(unsigned long long *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Workgroup 0, one thread, before its work: tag the launch, then open it.
+__device__ __forceinline__ void fz_arm(const FuseArgs &fz) {
+  __hip_atomic_store(fz.sync, (unsigned long long)fz.gen << 32, __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(fz.sync + 1, 0ull, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+// A producer, one thread, after every wave has released its stores: count
+// this producer once the launch is open.
+__device__ __forceinline__ void fz_produced(const FuseArgs &fz) {
+  const unsigned long long t0 = __builtin_amdgcn_s_memrealtime();
+  for (;;) {
+    if (fz_load(fz.sync + 1) == 0 && (fz_load(fz.sync) >> 32) == fz.gen) break;
+    if (__builtin_amdgcn_s_memrealtime() - t0 > FZ_BUDGET) break;
+    __builtin_amdgcn_s_sleep(4);
+  }
+  __hip_atomic_fetch_add(fz.sync, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// A consumer wave, before it reads producer data: wait until every producer
+// of this launch has counted itself.
+__device__ __forceinline__ void fz_wait(const FuseArgs &fz) {
+  const unsigned long long t0 = __builtin_amdgcn_s_memrealtime();
+  for (;;) {
+    if (fz_load(fz.sync + 1) < (unsigned long long)fz.ncons) {
+      const unsigned long long v = fz_load(fz.sync);
+      if ((v >> 32) == fz.gen && (unsigned)v >= (unsigned)fz.nprod) break;
+    }
+    if (__builtin_amdgcn_s_memrealtime() - t0 > FZ_BUDGET) break;
+    __builtin_amdgcn_s_sleep(4);
+  }
+}
+// A consumer, one thread, once it has passed.
+__device__ __forceinline__ void fz_done(const FuseArgs &fz) {
+  __hip_atomic_fetch_add(fz.sync + 1, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+constexpr int cmax(int a, int b) { return a > b ? a : b; }
+
 template <int V>
 struct IC {
   static constexpr int value = V;
@@ -86,7 +130,8 @@ __device__ __forceinline__ void static_for(F &&f) {
 template <class E, int BM, int BN, int WM, int WN, int WK, int BMODE, int BKB, int NBUF, int RD, int FS,
           int QB = 0, int EPI = EPI_STORE, int DMA = 0>
 __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int group_m,
-                                                                 SideArgs side, int nside) {
+                                                                 SideArgs side, int nside,
+                                                                 FuseArgs fz) {
   typedef typename E::T T;
   constexpr int NT = 64 * WM * WN * WK;
   constexpr int VEC = E::VEC;
@@ -124,7 +169,15 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   constexpr int RING = DMA ? NBUF * DSTAGE : NBUF * STAGE;
   constexpr int LDS0 = RING > RED_BYTES ? RING : RED_BYTES;
   constexpr int SIDE = side_lds_bytes<E, WM * WN * WK>();
-  constexpr int LDS = LDS0 > SIDE ? LDS0 : SIDE;
+  // Producer workgroups of a fused rank-r pass: u = x A^T ahead of the
+  // forward's bf16 direct-to-LDS tiles.
+  constexpr bool FUSE = DMA && QB == 0 && EPI == EPI_STORE && ES == 2 && BMODE == B_ROW;
+  constexpr int PV = V_ROW;
+  constexpr int PROD = FUSE ? cmax(cmax(row_lds_bytes<E, 1, PV, 4, 1>(), row_lds_bytes<E, 2, PV, 4, 1>()),
+                                   cmax(row_lds_bytes<E, 1, PV, 4, 2>(), row_lds_bytes<E, 2, PV, 4, 2>()))
+                            : 0;
+  constexpr int LDS1 = LDS0 > SIDE ? LDS0 : SIDE;
+  constexpr int LDS = LDS1 > PROD ? LDS1 : PROD;
   constexpr uint32_t OOB = 0x80000000u;      // offset past every buffer: loads return 0
   static_assert(WM * WN * WK == 4 || WM * WN * WK == 8, "four or eight waves");
   static_assert(SLICES % WK == 0, "k split");
@@ -165,13 +218,40 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   // The first `nside` workgroups (a multiple of 8, so the XCD of a tile
   // workgroup is unchanged) run the token-reduction side items; they start
   // first and overlap with the tiles.
-  if ((int)blockIdx.x < nside) {
-    if ((int)blockIdx.x < side_items_total<E>(side)) side_item<E, WM * WN * WK>(side, blockIdx.x, smem);
+  // With a fused rank-r pass, the `fz.nwg` producer workgroups come first.
+  const bool coh = FUSE && fz.nprod > 0;
+  const int bid = (int)blockIdx.x - (FUSE ? fz.nwg : 0);
+  if constexpr (FUSE) {
+    if (bid < 0) {
+      if ((int)blockIdx.x < fz.nprod) {
+        if (blockIdx.x == 0 && tid == 0) fz_arm(fz);
+        // Coherent stores, complete in every wave before the count: no L2
+        // write-back (which would stall every tile of the XCD) is needed.
+        auto prod = [&](auto JB, auto MB) {
+          row_item<E, decltype(JB)::value, PV, 4, decltype(MB)::value, true>(fz.row, blockIdx.x, 0, fz.nprod, 1,
+                                                                             smem);
+        };
+        if (fz.row.r <= 16) {
+          if (fz.row.mb == 2) prod(IC<1>(), IC<2>());
+          else prod(IC<1>(), IC<1>());
+        } else {
+          if (fz.row.mb == 2) prod(IC<2>(), IC<2>());
+          else prod(IC<2>(), IC<1>());
+        }
+        __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
+        __syncthreads();
+        if (tid == 0) fz_produced(fz);
+      }
+      return;
+    }
+  }
+  if (bid < nside) {
+    if (bid < side_items_total<E>(side)) side_item<E, WM * WN * WK>(side, bid, smem);
     return;
   }
   int t;
   {
-    const int id = (int)blockIdx.x - nside;
+    const int id = bid - nside;
     const int xcd = id & 7, local = id >> 3;
     const int base = ntiles >> 3, rem = ntiles & 7;
     t = xcd * base + (xcd < rem ? xcd : rem) + local;
@@ -529,15 +609,17 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
       const int soff = k0 * ES;
       const __amdgpu_buffer_rsrc_t ra_rs = lora ? rsA2 : rsA;
 #pragma unroll
-      for (int i = 0; i < DA_PW; ++i)
-        dma16(ra_rs, sA + (wv + i * NWV) * 1024, dkA[i] < krem ? (lora ? dA2[i] : dA[i]) : (uint32_t)OOB,
-              soff);
+      for (int i = 0; i < DA_PW; ++i) {
+        const uint32_t vo = dkA[i] < krem ? (lora ? dA2[i] : dA[i]) : (uint32_t)OOB;
+        dma16(ra_rs, sA + (wv + i * NWV) * 1024, vo, soff);
+      }
       if constexpr (BMODE == B_ROW) {
         const __amdgpu_buffer_rsrc_t rb_rs = lora ? rsB2 : rsB;
 #pragma unroll
-        for (int i = 0; i < DB_PW; ++i)
-          dma16(rb_rs, sB + (wv + i * NWV) * 1024,
-                dkB[i] < krem ? (lora ? dB2[i] : dB[i]) : (uint32_t)OOB, soff);
+        for (int i = 0; i < DB_PW; ++i) {
+          const uint32_t vo = dkB[i] < krem ? (lora ? dB2[i] : dB[i]) : (uint32_t)OOB;
+          dma16(rb_rs, sB + (wv + i * NWV) * 1024, vo, soff);
+        }
       } else {
         const char *base = lora ? (const char *)g.B2 + ((int64_t)k0 * g.ldb2 + n0) * ES
                                 : (const char *)g.B + ((int64_t)k0 * g.ldb + n0) * ES;
@@ -545,8 +627,9 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
         const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
             (void *)base, (short)0, (int)(krem > 0 ? min(krem, BKE) * ld * ES : 0), 0x00020000);
 #pragma unroll
-        for (int i = 0; i < DB_PW; ++i)
+        for (int i = 0; i < DB_PW; ++i) {
           dma16(rs, sB + (wv + i * NWV) * 1024, lora ? dB2[i] : dB[i], 0);
+        }
       }
     }
   };
@@ -623,14 +706,14 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
       const int soff = k0 * ES;
       if constexpr (q < DA_PW) {
         const __amdgpu_buffer_rsrc_t ra_rs = lora ? rsA2 : rsA;
-        dma16(ra_rs, ring_a(BUF) + (wv + q * NWV) * 1024, dkA[q] < krem ? (lora ? dA2[q] : dA[q]) : (uint32_t)OOB,
-              soff);
+        const uint32_t vo = dkA[q] < krem ? (lora ? dA2[q] : dA[q]) : (uint32_t)OOB;
+        dma16(ra_rs, ring_a(BUF) + (wv + q * NWV) * 1024, vo, soff);
       } else {
         constexpr int i = q - DA_PW;
         if constexpr (BMODE == B_ROW) {
           const __amdgpu_buffer_rsrc_t rb_rs = lora ? rsB2 : rsB;
-          dma16(rb_rs, ring_b(BUF) + (wv + i * NWV) * 1024,
-                dkB[i] < krem ? (lora ? dB2[i] : dB[i]) : (uint32_t)OOB, soff);
+          const uint32_t vo = dkB[i] < krem ? (lora ? dB2[i] : dB[i]) : (uint32_t)OOB;
+          dma16(rb_rs, ring_b(BUF) + (wv + i * NWV) * 1024, vo, soff);
         } else {
           const char *base = lora ? (const char *)g.B2 + ((int64_t)k0 * g.ldb2 + n0) * ES
                                   : (const char *)g.B + ((int64_t)k0 * g.ldb + n0) * ES;
@@ -719,6 +802,10 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
 #pragma unroll
       for (int s2 = 0; s2 < SPW; ++s2) mma_frags(f[s2]);
     };
+    // A fused launch's LoRA-step operands come from its producers: wait for
+    // them before the first load of a LoRA stage (here when the prologue
+    // already issues one, else in the step that does).
+    if (coh && nk_main < NBUF) fz_wait(fz);
     static_for<0, NBUF>([&](auto SI) { dma_stage(SI, decltype(SI)::value); });
     {
       constexpr int V = (NBUF - 1) * IPS;  // stage 0 landed
@@ -732,6 +819,10 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
       constexpr int V = (NBUF - 2) * IPS;     // stage kt + 1 landed
       __builtin_amdgcn_s_waitcnt((V & 15) | ((V >> 4) << 14) | (7 << 4));  // and lgkmcnt(0)
       __builtin_amdgcn_s_barrier();
+      __builtin_amdgcn_sched_barrier(0);
+      // A fused launch's LoRA stage holds its producers' output: wait for them
+      // before the step that issues its loads.
+      if (FUSE && coh && kt + NBUF == nk_main) fz_wait(fz);
       __builtin_amdgcn_sched_barrier(0);
       // The loads of stage kt + NBUF are spread between the fragment reads of
       // stage kt + 1 (in source order: an LDS read cannot pass the load
@@ -766,6 +857,7 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
     __builtin_amdgcn_s_waitcnt(0 | W_ENC);
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
+    if (coh && tid == 0) fz_done(fz);
   } else if constexpr (FS) {
     // Staged fragments: every MFMA fragment of a stage is read from LDS one
     // step ahead into the second of two register sets, so the MFMAs of a
@@ -1161,7 +1253,7 @@ static int pick_group_m(int tiles_m, int tiles_n, int BM, int BN) {
 
 template <class E, int BM, int BN, int WM, int WN, int WK, int BMODE, int BKB, int NBUF, int RD, int FS,
           int QB = 0, int EPI = EPI_STORE, int DMA = 0>
-static hipError_t launch_cfg(const GemmArgs &g, const SideArgs *side, hipStream_t st) {
+static hipError_t launch_cfg(const GemmArgs &g, const SideArgs *side, hipStream_t st, FuseArgs *fz = nullptr) {
   const int tm = g.M > 0 ? (g.M + BM - 1) / BM : 0, tn = (g.N + BN - 1) / BN;
   SideArgs sa{};
   int nside = 0;
@@ -1169,11 +1261,24 @@ static hipError_t launch_cfg(const GemmArgs &g, const SideArgs *side, hipStream_
     sa = *side;
     nside = side_workgroups(sa, std::is_same<E, BF16>::value ? DT_BF16 : DT_F32);
   }
-  const int grid = tm * tn + nside;
+  FuseArgs fa{};
+  if (fz && fz->nprod > 0) {
+    // 16 rows per producer while they fit beside the tiles on the 256 CUs (a
+    // tile needs the producers' rows only in its last steps), else 32.
+    const int free = 256 - tm * tn - nside;
+    const int64_t T = fz->row.M;
+    const int mb = ((T + 15) / 16 + 7) / 8 * 8 <= free ? 1 : 2;
+    fz->row.mb = mb;
+    fz->nprod = (int)((T + 16 * mb - 1) / (16 * mb));
+    fz->ncons = tm * tn;  // consumers: the tiles
+    fz->nwg = (fz->nprod + 7) / 8 * 8;
+    fa = *fz;
+  }
+  const int grid = tm * tn + nside + fa.nwg;
   if (grid == 0) return hipSuccess;
   hipLaunchKernelGGL((gemm_kernel<E, BM, BN, WM, WN, WK, BMODE, BKB, NBUF, RD, FS, QB, EPI, DMA>), dim3(grid),
                      dim3(64 * WM * WN * WK), 0, st, g, tm > 0 ? pick_group_m(tm, tn, BM, BN) : 1,
-                     sa, nside);
+                     sa, nside, fa);
   return hipGetLastError();
 }
 
@@ -1223,6 +1328,21 @@ hipError_t launch_gemm_q(const GemmArgs &g, int bits, bool b_kmajor, const SideA
   if (bits == 8)
     return b_kmajor ? launch_cfg<BF16, 128, 128, 2, 2, 2, B_KMAJ_TR, 128, 2, 3, 2, 8>(g, side, st)
                     : launch_cfg<BF16, 128, 128, 2, 2, 2, B_ROW, 128, 2, 3, 2, 8>(g, side, st);
+  return hipErrorInvalidValue;
+}
+
+bool gemm_fusable(int M, int N) { return pick_shape(M, N, false) != 2; }
+
+hipError_t launch_gemm_fused(const GemmArgs &g, FuseArgs *fz, hipStream_t st) {
+  if (!fz || fz->nprod <= 0 || fz->row.vmode != V_ROW || fz->row.nsplit != 1 || fz->row.r < 1 ||
+      fz->row.r > 32 || g.r < 1 || !fz->sync || fz->gen == 0)
+    return hipErrorInvalidValue;
+  switch (pick_shape(g.M, g.N, false)) {
+    case 1:
+      return launch_cfg<BF16, 256, 128, 4, 2, 1, B_ROW, 128, 3, 3, 2, 0, EPI_STORE, 1>(g, nullptr, st, fz);
+    case 0:
+      return launch_cfg<BF16, 128, 128, 2, 2, 2, B_ROW, 128, 3, 3, 2, 0, EPI_STORE, 1>(g, nullptr, st, fz);
+  }
   return hipErrorInvalidValue;
 }
 

@@ -36,6 +36,7 @@ struct SideArgs {
   int T, r;
 };
 
+
 // C[M, N] = sum_k Aop[m][k] Bop[n][k]  (+ LoRA step), rounded to the element type.
 //   Aop[m][k] = A[m*lda + k]                         m < M, k < K
 //   Bop[n][k] = B[n*ldb + k]   (b_kmajor = false)    n < N
@@ -200,6 +201,46 @@ struct RowArgs {
   int mb;  // row tiles of 16 per workgroup: 1 (0), 2 or 4 (bf16, r <= 32)
 };
 hipError_t launch_row_skinny(const RowArgs &a, Dtype dt, hipStream_t st);
+
+// Fused rank-r pass of the forward: the first `nwg` workgroups of the GEMM
+// launch (a multiple of 8, so the tiles keep their XCD mapping) are
+// producers, one per 16 * row.mb rows, that compute u = x A^T over the whole
+// reduction axis (row: nsplit = 1, V_ROW) -- u and the LoRA-step operand
+// E(s u) -- ahead of the tiles, which need them only in their last (LoRA)
+// step.  They hand over through two 8-byte words of the workspace (8-byte
+// aligned; nothing else may use them during the launch):
+//   sync[0] = (gen << 32) | producers counted, sync[1] = tiles that passed.
+// Workgroup 0 arms the launch before its work (sync[0] = gen << 32, then,
+// released after it, sync[1] = 0).  A producer stores its rows coherently at
+// device scope (write-through, no L2 write-back that would stall the tiles of
+// its XCD), waits until every wave's stores have completed, and counts itself
+// in sync[0] once it sees the launch armed: sync[1] == 0, then the tag in
+// sync[0].  A tile, in the step that issues its LoRA stage, waits until
+// sync[1] < ncons and then sync[0] holds the tag and all producers, reads the
+// producers' rows with ordinary loads, and counts itself in sync[1] after its
+// main loop.  The reads see the producers' data: no L2 holds an older copy of
+// those rows (the L2s are invalidated when a launch starts, and nothing in
+// the launch reads the rows before the wait), so every read fetches the rows
+// as the producers stored them.  A stale state left by an earlier launch with
+// the same tag (a replayed graph) has sync[1] == ncons, so it never passes
+// for armed; a workspace with arbitrary contents holds the tag only by a
+// 2^-32 chance.  Every wait gives up after about 0.2 s, so a broken hand-over
+// yields wrong results, never a hang.
+struct FuseArgs {
+  RowArgs row;
+  int nprod;                 // producers (row blocks); 0: no fusion
+  int nwg;                   // workgroups reserved for them
+  unsigned long long *sync;  // sync[0], sync[1]
+  unsigned int gen;          // this launch's tag, never 0
+  int ncons;                 // consumers: the tiles (set by launch_gemm_fused)
+};
+
+// Whether the bf16 forward GEMM (row-major B) of this shape runs a tile
+// configuration that takes producer workgroups.
+bool gemm_fusable(int M, int N);
+// The bf16 forward GEMM with producers at the front (fz->nprod > 0; chooses
+// fz->row.mb and sets fz->nprod, fz->nwg and fz->ncons).
+hipError_t launch_gemm_fused(const GemmArgs &g, FuseArgs *fz, hipStream_t st);
 
 // Split of a row-skinny product over its reduction axis L, and rows per
 // workgroup.  Short T (below 2048): one 16-row tile per workgroup, enough
