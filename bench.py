@@ -279,13 +279,15 @@ def bench_topk(dev, V=128256, D=3072, k=1000):
             "table_bytes": V * k * 4}
 
 
-def kernel_flops(workload):
-    """Algorithmic flops of one launch of each GEMM kernel, per linear shape."""
+def kernel_flops(workload, fused_fwd=False):
+    """Algorithmic flops of one launch of each GEMM kernel, per linear shape.
+    With `fused_fwd` the forward launch also computes u = x A^T (its producer
+    workgroups), 2TKr more."""
     T = workload.tokens
     per = {}
     for lin in workload.linears:
         K, N, r = lin.d_in, lin.d_out, lin.rank
-        per.setdefault("gemm_fwd", []).append(2.0 * T * N * (K + r))
+        per.setdefault("gemm_fwd", []).append(2.0 * T * N * (K + r) + (2.0 * T * K * r if fused_fwd else 0.0))
         per.setdefault("gemm_bwd_dx", []).append(2.0 * T * K * (N + r))
     if workload.head is not None:
         per["gemm_frozen_dx"] = [2.0 * T * workload.head.d_in * workload.head.d_out]
@@ -397,7 +399,9 @@ def main():
             per_kernel[name] = (tot, n)
     lm.profiler_reset()
     dom = max(per_kernel, key=lambda k: per_kernel[k][0])
-    kf = kernel_flops(w)
+    # the forward's rank-r pass runs inside its GEMM launch when no
+    # separate lora_down launch was recorded
+    kf = kernel_flops(w, fused_fwd="lora_down" not in per_kernel)
     launch_flops = sum(kf[dom]) / len(kf[dom]) if dom in kf else None
     tot, n = per_kernel[dom]
     avg_ms = tot / n
