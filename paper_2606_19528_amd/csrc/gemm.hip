@@ -1293,7 +1293,7 @@ int side_workgroups(const SideArgs &s, Dtype dt) {
 // waves of tiles over the 256 CUs times the per-tile cost.  Relative per-CU
 // throughput measured on MI355X at T = 2048 and 4096 over the shapes of the
 // Llama and Qwen layers, for 128x128 and 256x128 (both direct-to-LDS) and
-// 256x256 (register-staged): row-major B 0.84 : 0.99 : 1.0; k-major B (the
+// 256x256 (register-staged): row-major B 0.84 : 0.99 : 0.95; k-major B (the
 // transposed reads cost the small tile more) 0.76 : 1.04 : 1.0.
 static int pick_shape(int M, int N, bool b_kmajor) {
   auto cost = [&](int bm, int bn, double eff) {
@@ -1301,7 +1301,7 @@ static int pick_shape(int M, int N, bool b_kmajor) {
     return (double)((tiles + 255) / 256) * bm * bn / eff;
   };
   const double c0 = cost(128, 128, b_kmajor ? 0.76 : 0.84), c1 = cost(256, 128, b_kmajor ? 1.04 : 0.99),
-               c2 = cost(256, 256, 1.0);
+               c2 = cost(256, 256, b_kmajor ? 1.0 : 0.95);
   if (c2 <= c1 && c2 <= c0) return 2;
   return c1 < c0 ? 1 : 0;
 }
@@ -1331,7 +1331,15 @@ hipError_t launch_gemm_q(const GemmArgs &g, int bits, bool b_kmajor, const SideA
   return hipErrorInvalidValue;
 }
 
-bool gemm_fusable(int M, int N) { return pick_shape(M, N, false) != 2; }
+// Producers only pay off on CUs the tiles leave idle: fused when the tile
+// shape is direct-to-LDS and 32-row producers fit beside the tiles.
+bool gemm_fusable(int M, int N) {
+  const int cfg = pick_shape(M, N, false);
+  if (cfg == 2) return false;
+  const long bm = cfg == 1 ? 256 : 128;
+  const long tiles = ((M + bm - 1) / bm) * ((N + 127) / 128);
+  return tiles + ((M + 31) / 32 + 7) / 8 * 8 <= 256;
+}
 
 hipError_t launch_gemm_fused(const GemmArgs &g, FuseArgs *fz, hipStream_t st) {
   if (!fz || fz->nprod <= 0 || fz->row.vmode != V_ROW || fz->row.nsplit != 1 || fz->row.r < 1 ||

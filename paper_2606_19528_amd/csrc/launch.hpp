@@ -236,7 +236,7 @@ struct FuseArgs {
 };
 
 // Whether the bf16 forward GEMM (row-major B) of this shape runs a tile
-// configuration that takes producer workgroups.
+// configuration that takes producer workgroups, and leaves the CUs for them.
 bool gemm_fusable(int M, int N);
 // The bf16 forward GEMM with producers at the front (fz->nprod > 0; chooses
 // fz->row.mb and sets fz->nprod, fz->nwg and fz->ncons).
