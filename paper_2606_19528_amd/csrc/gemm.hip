@@ -46,29 +46,6 @@ enum { B_ROW = 0, B_KMAJ_REG = 1, B_KMAJ_TR = 2 };
 
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-typedef __attribute__((address_space(3))) void lds_void;
-
-// One direct-to-LDS load: 16 bytes per lane from voffset + soffset of the
-// resource into lds + 16 * lane (lds is the same for the whole wave; M0 holds
-// it).  Written as assembly so that the compiler does not track these LDS
-// writes: its own tracking makes some LDS reads wait for every such load in
-// flight.  Every read of a stage is ordered after its loads by the explicit
-// wait + barrier protocol of the main loop instead.  (No compiler-generated
-// code of these kernels keeps a value in M0.)  The compiler does not look
-// into the assembly for hazards, so it carries its own wait states: five
-// before the load may read SGPRs that a vector instruction wrote, one
-// between the write of M0 and the load that reads it.
-#pragma clang diagnostic push
-#pragma clang diagnostic ignored "-Winline-asm"
-__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, char *lds, uint32_t voffset,
-                                      int soffset) {
-  const uint32_t base = (uint32_t)(uintptr_t)(lds_void *)lds;
-  asm volatile("s_nop 4\n\ts_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds" ::"s"(base),
-               "v"(voffset),
-               "s"(rs), "s"(soffset)
-               : "memory", "m0");
-}
-#pragma clang diagnostic pop
 
 // ---- hand-over of a fused rank-r pass (protocol in launch.hpp, FuseArgs) ------
 constexpr unsigned long long FZ_BUDGET = 20000000ull;  // 0.2 s of the 100 MHz real-time counter

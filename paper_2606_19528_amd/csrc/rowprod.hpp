@@ -3,10 +3,20 @@
 // fused GEMM launch (gemm.hip):
 //   P_p[m][j] = sum_{k in segment p} X[m][k] V(j, k)
 // for the 16 * MB rows of row block `bx` and reduction segment `by` (see
-// RowArgs in launch.hpp).  Eight waves take interleaved 128-byte chunks of the
-// segment (up to four chunks in flight per wave), accumulate 16 x r tiles on
-// 16x16 matrix cores, and the eight partial tiles are summed in LDS in a
-// fixed order.  At r >= 16 vector FMAs would not keep up with HBM.
+// RowArgs in launch.hpp).  The eight waves accumulate 16 x r tiles on 16x16
+// matrix cores over their share of the segment, and the eight partial tiles
+// are summed in LDS in a fixed order.  At r >= 16 vector FMAs would not keep
+// up with HBM.
+//
+// bf16 with r <= 32 (row-major V, or k-major V with r a multiple of 8): both
+// operands stream through LDS.  A stage is 256 k of the item's rows and of V;
+// direct-to-LDS loads fill a ring of stages (512-byte row pieces, two rows per
+// load; k-major V as its contiguous [256 k][r] block), and wave w reads k-slice
+// w (32 k) of every stage.  Fetching the V fragments straight from global
+// memory (16 rows x 64 bytes per load, the same lines for every workgroup)
+// cost a third of the kernel's time; read from LDS they cost almost nothing.
+// Other cases: eight waves take interleaved 128-byte chunks of the segment (up
+// to four chunks in flight per wave) and load their fragments directly.
 //
 // k-major V (B in the backward pass): each wave copies the V rows of its chunk
 // into a private LDS region and reads them back with ds_read_b64_tr_b16,
@@ -30,12 +40,29 @@ typedef __attribute__((address_space(3))) rp_i16x4 rp_lds_i16x4;
 
 constexpr int ROW_NW = 8;  // waves per workgroup
 
+// Streamed through LDS (see above)?
+template <class E, int JB, int VMODE>
+constexpr bool row_streamed() {
+  return sizeof(typename E::T) == 2 && JB <= 2 && (VMODE == V_ROW || VMODE == V_KMAJ_TR);
+}
+constexpr int ROW_KS = 256;  // k per stage of the streamed form
+// Stage bytes and ring depth of the streamed form: 512-byte pieces of the 16 MB
+// rows and of 16 JB rows of V (a k-major V block of 256 x r bf16 fits in them).
+template <int JB, int MB>
+constexpr int row_stage_bytes() { return (16 * MB + 16 * JB) * ROW_KS * 2; }
+template <int JB, int MB>
+constexpr int row_nbuf() { return row_stage_bytes<JB, MB>() <= 32768 ? 4 : 3; }
+
 // LDS bytes of one item.
 template <class E, int JB, int VMODE, int U, int MB>
 constexpr int row_lds_bytes() {
   constexpr int CE = 128 / (int)sizeof(typename E::T);
   constexpr int REGION = U * CE * JB * 16 * 2;
   constexpr int RED = ROW_NW * 16 * MB * (JB * 16 + 1) * 4;
+  if constexpr (row_streamed<E, JB, VMODE>()) {
+    constexpr int RING = row_nbuf<JB, MB>() * row_stage_bytes<JB, MB>();
+    return RING > RED ? RING : RED;
+  }
   return (VMODE == V_KMAJ_TR && ROW_NW * REGION > RED) ? ROW_NW * REGION : RED;
 }
 
@@ -107,6 +134,95 @@ __device__ __forceinline__ void row_item(const RowArgs &a, int bx, int by, int g
   for (int mt = 0; mt < MB; ++mt)
 #pragma unroll
     for (int jb = 0; jb < JB; ++jb) acc[mt][jb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  if constexpr (row_streamed<E, JB, VMODE>()) {
+    // Stage layout: rows 0 .. 16 MB - 1 of the item, then V (row-major: 16 JB
+    // rows; k-major: the [256][r] block), 512 bytes per row.  Row-major
+    // pieces keep their 16-byte chunk c at c ^ (row & 15), so the fragment
+    // reads of 16 rows at one k hit distinct banks.
+    constexpr int KS = ROW_KS, PB = KS * 2;
+    constexpr int XB = 16 * MB * PB;
+    constexpr int STAGE = row_stage_bytes<JB, MB>(), NBUF = row_nbuf<JB, MB>();
+    constexpr int LPW = MB + JB;  // loads per wave per stage
+    constexpr uint32_t OOB = 0x80000000u;
+    const int wv = __builtin_amdgcn_readfirstlane(wave);
+    const int klen = k_hi - k_lo, nst = (klen + KS - 1) / KS;
+    const int nrows = max(0, min(M - m0, 16 * MB));
+    // (the values are uniform; readfirstlane keeps the resources in SGPRs)
+    auto rsrc = [](const void *base, int64_t bytes) {
+      const uint64_t b = (uint64_t)(uintptr_t)base;
+      const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)b);
+      const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+      const int n = __builtin_amdgcn_readfirstlane((int)bytes);
+      return __builtin_amdgcn_make_buffer_rsrc((void *)(uintptr_t)(((uint64_t)hi << 32) | lo), (short)0, n,
+                                               0x00020000);
+    };
+    const __amdgpu_buffer_rsrc_t rsX = rsrc(Xp + (int64_t)m0 * a.ldx + k_lo, (int64_t)nrows * a.ldx * 2);
+    const __amdgpu_buffer_rsrc_t rsV = VMODE == V_ROW ? rsrc(Vp + k_lo, (int64_t)r * a.ldv * 2)
+                                                      : rsrc(Vp + (int64_t)k_lo * r, (int64_t)klen * r * 2);
+    // Load q of this wave covers stage bytes [1024 (wv + 8 q), + 1024): the
+    // item's rows for q < MB, V after.  kq: k (within a stage) of the lane's
+    // first element, or its k-row for k-major V.
+    uint32_t offq[LPW];
+    int kq[LPW];
+#pragma unroll
+    for (int q = 0; q < LPW; ++q) {
+      const int ii = wv + 8 * (q < MB ? q : q - MB);
+      if (q < MB || VMODE == V_ROW) {
+        const int rr = 2 * ii + (lane >> 5);
+        const int c = (lane & 31) ^ (rr & 15);
+        kq[q] = c * 8;
+        offq[q] = (uint32_t)(rr * (q < MB ? a.ldx : a.ldv) * 2 + c * 16);
+      } else {
+        const int byte = ii * 1024 + lane * 16;
+        kq[q] = byte / (2 * r) < KS ? byte / (2 * r) : KS + klen;  // past the block: never loaded
+        offq[q] = (uint32_t)byte;
+      }
+    }
+    auto issue = [&](int st) __attribute__((always_inline)) {
+      char *buf = smem + (st % NBUF) * STAGE;
+      const int k0 = st * KS;
+#pragma unroll
+      for (int q = 0; q < LPW; ++q) {
+        const uint32_t vo = k0 + kq[q] < klen ? offq[q] : OOB;
+        if (q < MB) dma16(rsX, buf + (wv + 8 * q) * 1024, vo, k0 * 2);
+        else dma16(rsV, buf + XB + (wv + 8 * (q - MB)) * 1024, vo, VMODE == V_ROW ? k0 * 2 : k0 * r * 2);
+      }
+    };
+#pragma unroll
+    for (int st = 0; st < NBUF - 1; ++st) issue(st);
+    const int pos = (4 * wv + (lane >> 4)) ^ (lane & 15);  // k-slice wv of a stage
+    for (int s = 0; s < nst; ++s) {
+      constexpr int V = (NBUF - 2) * LPW;  // this wave's loads of stage s landed, LDS reads done
+      __builtin_amdgcn_s_waitcnt((V & 15) | ((V >> 4) << 14) | (7 << 4));
+      __builtin_amdgcn_s_barrier();
+      __builtin_amdgcn_sched_barrier(0);
+      issue(s + NBUF - 1);  // into the buffer of stage s - 1, which nobody reads any more
+      const char *buf = smem + (s % NBUF) * STAGE;
+      u32x4 xa[MB], vb[JB];
+#pragma unroll
+      for (int mt = 0; mt < MB; ++mt) xa[mt] = ld16(buf + (mt * 16 + (lane & 15)) * PB + pos * 16);
+#pragma unroll
+      for (int jb = 0; jb < JB; ++jb) {
+        if constexpr (VMODE == V_ROW) {
+          vb[jb] = ld16(buf + XB + (jb * 16 + (lane & 15)) * PB + pos * 16);
+        } else {
+          // four consecutive k of one column per lane (as in the other form)
+          const int iq = lane & 15;
+          const char *pp = buf + XB + (32 * wv + 8 * g + (iq >> 2)) * (2 * r) + (jb * 16 + 4 * (iq & 3)) * 2;
+          rp_i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((rp_lds_i16x4 *)pp);
+          rp_i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((rp_lds_i16x4 *)(pp + 4 * (2 * r)));
+          vb[jb] = u32x4{__builtin_bit_cast(uint2, lo).x, __builtin_bit_cast(uint2, lo).y,
+                         __builtin_bit_cast(uint2, hi).x, __builtin_bit_cast(uint2, hi).y};
+        }
+      }
+#pragma unroll
+      for (int jb = 0; jb < JB; ++jb)
+#pragma unroll
+        for (int mt = 0; mt < MB; ++mt) mma16(E(), acc[mt][jb], xa[mt], vb[jb]);
+    }
+    __builtin_amdgcn_s_waitcnt((7 << 4));  // the loads past the end (zeros) too
+  } else {
   char *region = smem + wave * REGION;
 
   for (int kc0 = k_lo + wave * CE; kc0 < k_hi; kc0 += NW * CE * U) {
@@ -181,6 +297,7 @@ __device__ __forceinline__ void row_item(const RowArgs &a, int bx, int by, int g
         for (int jb = 0; jb < JB; ++jb)
 #pragma unroll
           for (int mt = 0; mt < MB; ++mt) mma16(E(), acc[mt][jb], xf[u][mt][h], vf[u][h][jb]);
+  }
   }
 
   // D[m][n]: m = 4 (lane / 16) + i, n = lane % 16.  Sum the waves' tiles.
