@@ -70,10 +70,12 @@ def test_split_reduction(orc, shape, recompute, dtype):
     _case(orc, T, K, N, r, 2.0 * r, seed=41, dtype=dtype, recompute=recompute)
 
 
-# Long T: the rank-r row products take several 16-row tiles per workgroup
-# (ragged last block, rank not a multiple of 16, u rematerialised).
+# Long T: the rank-r row products take several 16-row tiles per workgroup, or
+# whole rows, or two segments of 16-row blocks (ragged last block, rank not a
+# multiple of 16, u rematerialised, reduction axes on both sides of 4096).
 @pytest.mark.parametrize("shape,recompute", [((2100, 1032, 776, 24), False), ((2100, 1032, 776, 24), True),
-                                             ((4100, 520, 1288, 8), True), ((2048, 3072, 1032, 32), False)])
+                                             ((4100, 520, 1288, 8), True), ((2048, 3072, 1032, 32), False),
+                                             ((4100, 4200, 264, 32), True), ((4100, 264, 4200, 32), False)])
 def test_long_t_row_tiles(orc, shape, recompute):
     T, K, N, r = shape
     _case(orc, T, K, N, r, 2.0 * r, seed=53, recompute=recompute)
