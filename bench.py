@@ -279,16 +279,18 @@ def bench_topk(dev, V=128256, D=3072, k=1000):
             "table_bytes": V * k * 4}
 
 
-def kernel_flops(workload, fused_fwd=False):
+def kernel_flops(workload, fused_fwd=False, fused_bwd=False):
     """Algorithmic flops of one launch of each GEMM kernel, per linear shape.
     With `fused_fwd` the forward launch also computes u = x A^T (its producer
-    workgroups), 2TKr more."""
+    workgroups), 2TKr more; with `fused_bwd` the dx launch also computes
+    du = s dy B, 2TNr more.  (The dA / dB side items that share the dx launch
+    are not counted in either case.)"""
     T = workload.tokens
     per = {}
     for lin in workload.linears:
         K, N, r = lin.d_in, lin.d_out, lin.rank
         per.setdefault("gemm_fwd", []).append(2.0 * T * N * (K + r) + (2.0 * T * K * r if fused_fwd else 0.0))
-        per.setdefault("gemm_bwd_dx", []).append(2.0 * T * K * (N + r))
+        per.setdefault("gemm_bwd_dx", []).append(2.0 * T * K * (N + r) + (2.0 * T * N * r if fused_bwd else 0.0))
     if workload.head is not None:
         per["gemm_frozen_dx"] = [2.0 * T * workload.head.d_in * workload.head.d_out]
     return per
@@ -401,7 +403,7 @@ def main():
     dom = max(per_kernel, key=lambda k: per_kernel[k][0])
     # the forward's rank-r pass runs inside its GEMM launch when no
     # separate lora_down launch was recorded
-    kf = kernel_flops(w, fused_fwd="lora_down" not in per_kernel)
+    kf = kernel_flops(w, fused_fwd="lora_down" not in per_kernel, fused_bwd="lora_dy_b" not in per_kernel)
     launch_flops = sum(kf[dom]) / len(kf[dom]) if dom in kf else None
     tot, n = per_kernel[dom]
     avg_ms = tot / n

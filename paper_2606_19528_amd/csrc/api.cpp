@@ -129,16 +129,16 @@ lora_status_t check_shapes(int64_t T, int64_t d_in, int64_t d_out, int64_t r, lo
 // products are computed as `nsplit` partial sums over their reduction axis
 // (row_split); the LoRA-step operands hold one column block per partial.
 //
-// The forward's rank-r pass (u = x A^T) runs fused into the GEMM launch -- as
-// producer workgroups ahead of the tiles, each over whole rows of x -- when
-// the operands are bf16, r is a multiple of 8 up to 32 and the GEMM takes a
-// direct-to-LDS tile configuration; it then needs no partial sums and no
-// padded copy of B, and the workspace starts with the hand-over words of the
-// launch.  (The backward keeps its rank-r pass over dy as a kernel of its
-// own: the dA / dB side items that need it would have to wait in CUs the dx
-// tiles need, and fewer producers make that pass slow.)
-bool fuse_ok(int64_t T, int64_t N, int64_t r, lora_dtype_t dt) {
-  return dt == LORA_BF16 && r >= 8 && r <= 32 && r % 8 == 0 && gemm_fusable((int)T, (int)N);
+// The rank-r pass of either direction (forward u = x A^T, backward
+// du = s dy B) runs fused into its GEMM launch -- as producer workgroups
+// ahead of the tiles, each over whole rows -- when the operands are bf16, r
+// is a multiple of 8 up to 32 and the GEMM takes a direct-to-LDS tile
+// configuration that leaves the producers room beside the tiles; it then
+// needs no partial sums and no padded copy of B (A), and the workspace starts
+// with the hand-over words of the launch.  In the backward the producers then
+// run the dA / dB side items, so those take no CUs of their own.
+bool fuse_ok(int64_t T, int64_t N, int64_t r, lora_dtype_t dt, bool b_kmajor = false) {
+  return dt == LORA_BF16 && r >= 8 && r <= 32 && r % 8 == 0 && gemm_fusable((int)T, (int)N, b_kmajor);
 }
 // Tag of a fused launch: distinct for every call of this process, never 0.
 unsigned int next_gen() {
@@ -193,8 +193,9 @@ FwdLayout fwd_layout(int64_t T, int64_t K, int64_t N, int64_t r, lora_dtype_t dt
 }
 
 struct BwdLayout {
-  size_t u, du, dutail, acat, total;
+  size_t sync, u, du, dutail, acat, total;
   int ldt;
+  bool fused;
   RowSplit sp_u, sp_du;
 };
 BwdLayout bwd_layout(int64_t T, int64_t K, int64_t N, int64_t r, lora_dtype_t dt) {
@@ -204,9 +205,12 @@ BwdLayout bwd_layout(int64_t T, int64_t K, int64_t N, int64_t r, lora_dtype_t dt
   // A recomputed u is summed exactly as the forward pass summed it (whole
   // rows when the forward runs fused), so it is bitwise the saved one.
   L.sp_u = fuse_ok(T, N, r, dt) ? whole_rows(K, d) : row_split(T, K, (int)r, d);
-  L.sp_du = row_split(T, N, (int)r, d);
+  L.fused = fuse_ok(T, K, r, dt, true);
+  L.sp_du = L.fused ? whole_rows(N, d) : row_split(T, N, (int)r, d);
   L.ldt = tail_ld(L.sp_du.nsplit * (int)r, d);
   size_t off = 0;
+  L.sync = off;  // hand-over words of a fused launch
+  off += L.fused ? 256 : 0;
   L.u = off;  // partial sums of u (when it is recomputed)
   off += round256((size_t)L.sp_u.nsplit * T * r * 4);
   L.du = off;  // partial sums of du = s dy B
@@ -416,7 +420,7 @@ lora_status_t fwd_impl(const void *x, const void *W, const void *qc, const float
     g.B2 = B; g.ldb2 = r;  // rows of r bf16: whole 16-byte vectors
     g.r = (int)r;
     Timed t(K_GEMM_FWD, st);
-    hipError_t e = launch_gemm_fused(g, &fz, st);
+    hipError_t e = launch_gemm_fused(g, &fz, nullptr, st);
     t.done();
     if (e != hipSuccess) return hip_fail(e, "gemm_fwd launch");
     return LORA_OK;
@@ -536,6 +540,32 @@ lora_status_t bwd_impl(const void *x, const void *W, const void *qc, const float
   }
   const int ns = L.sp_du.nsplit;
   float *du = (float *)(wsb + L.du);
+  if (L.fused && !qc && dx) {
+    // du = s dy B by the producer workgroups of the dx launch, which then run
+    // the dA / dB side items.
+    FuseArgs fz{};
+    RowArgs &ra = fz.row;
+    ra.X = dy; ra.ldx = d_out; ra.M = (int)T; ra.L = (int)d_out;
+    ra.V = B; ra.ldv = r; ra.vmode = V_KMAJ_TR; ra.r = (int)r;
+    ra.nsplit = 1; ra.seg = L.sp_du.seg; ra.mb = 1;
+    ra.out_mult = scale; ra.out = du; ra.out_stride = T * r;
+    ra.tail = wsb + L.dutail; ra.ldt = L.ldt; ra.tail_mult = scale;
+    fz.nprod = (int)((T + 15) / 16);
+    fz.sync = (unsigned long long *)(wsb + L.sync);
+    fz.gen = next_gen();
+    SideArgs sd{};
+    sd.T = (int)T; sd.r = (int)r; sd.njobs = 2;
+    sd.job[0] = ColJob{x, d_in, (int)d_in, du, dA, 1, 1.0f, 1, T * r};
+    sd.job[1] = ColJob{dy, d_out, (int)d_out, u, dB, 0, scale, u_parts, T * r};
+    g.A2 = wsb + L.dutail; g.lda2 = L.ldt;
+    g.B2 = A; g.ldb2 = d_in;
+    g.r = (int)r;
+    Timed t(K_GEMM_BWD_DX, st);
+    e = launch_gemm_fused(g, &fz, &sd, st);
+    t.done();
+    if (e != hipSuccess) return hip_fail(e, "gemm_bwd_dx launch");
+    return LORA_OK;
+  }
   {
     RowArgs ra{};
     ra.X = dy; ra.ldx = d_out; ra.M = (int)T; ra.L = (int)d_out;

@@ -9,7 +9,8 @@
 // Structure of one workgroup (4 or 8 waves, one BM x BN output tile):
 //  * k advances in stages of BKB bytes per row.  Global loads go through
 //    buffer resources (hardware bounds checks instead of per-load branches).
-//  * DMA = 1 (the bf16 128 x 128 tiles): the loads write LDS directly
+//  * DMA = 1 or 2 (the bf16 128 x 128 and 256 x 128 tiles; 2 with producer
+//    workgroups of a fused rank-r pass in front): the loads write LDS directly
 //    (buffer_load ... lds), into a ring of NBUF stages with NBUF - 1 stages
 //    in flight behind the one being read; no registers or LDS-write
 //    instructions are spent on staging.  One load moves 1 KB in lane order, so
@@ -83,6 +84,19 @@ __device__ __forceinline__ void fz_wait(const FuseArgs &fz) {
     __builtin_amdgcn_s_sleep(4);
   }
 }
+// A producer that then runs side items, one thread, after counting itself:
+// wait until every producer of this launch has counted itself.  Its own count
+// followed this launch's arming, so the count it reads is this launch's and
+// no condition on the tiles' count is needed.
+__device__ __forceinline__ void fz_wait_producers(const FuseArgs &fz) {
+  const unsigned long long t0 = __builtin_amdgcn_s_memrealtime();
+  for (;;) {
+    const unsigned long long v = fz_load(fz.sync);
+    if ((v >> 32) == fz.gen && (unsigned)v >= (unsigned)fz.nprod) break;
+    if (__builtin_amdgcn_s_memrealtime() - t0 > FZ_BUDGET) break;
+    __builtin_amdgcn_s_sleep(4);
+  }
+}
 // A consumer, one thread, once it has passed.
 __device__ __forceinline__ void fz_done(const FuseArgs &fz) {
   __hip_atomic_fetch_add(fz.sync + 1, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -146,10 +160,15 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   constexpr int RING = DMA ? NBUF * DSTAGE : NBUF * STAGE;
   constexpr int LDS0 = RING > RED_BYTES ? RING : RED_BYTES;
   constexpr int SIDE = side_lds_bytes<E, WM * WN * WK>();
-  // Producer workgroups of a fused rank-r pass: u = x A^T ahead of the
-  // forward's bf16 direct-to-LDS tiles.
-  constexpr bool FUSE = DMA && QB == 0 && EPI == EPI_STORE && ES == 2 && BMODE == B_ROW;
-  constexpr int PV = V_ROW;
+  // Producer workgroups of a fused rank-r pass ahead of the bf16
+  // direct-to-LDS tiles: u = x A^T (forward, row-major A) or du = s dy B
+  // (backward, k-major B).
+  // (DMA = 2: a separate instance, so launches without producers carry none
+  // of their code or registers.)
+  constexpr bool FUSE = DMA == 2;
+  static_assert(!FUSE || (QB == 0 && EPI == EPI_STORE && ES == 2 && (BMODE == B_ROW || BMODE == B_KMAJ_TR)),
+                "producers: bf16 direct-to-LDS tiles that store C");
+  constexpr int PV = BMODE == B_ROW ? V_ROW : V_KMAJ_TR;
   constexpr int PROD = FUSE ? cmax(cmax(row_lds_bytes<E, 1, PV, 4, 1>(), row_lds_bytes<E, 2, PV, 4, 1>()),
                                    cmax(row_lds_bytes<E, 1, PV, 4, 2>(), row_lds_bytes<E, 2, PV, 4, 2>()))
                             : 0;
@@ -218,6 +237,17 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
         __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
         __syncthreads();
         if (tid == 0) fz_produced(fz);
+        // Backward: the producers then run the dA / dB side items (dA needs
+        // all of du), on CUs the tiles leave to them.
+        const int nitems = BMODE == B_KMAJ_TR ? side_items_total<E>(side) : 0;
+        if constexpr (BMODE == B_KMAJ_TR) if (nitems > 0) {
+          if (tid == 0) fz_wait_producers(fz);
+          __syncthreads();
+          for (int it = blockIdx.x; it < nitems; it += fz.nprod) {
+            side_item<E, WM * WN * WK>(side, it, smem);
+            __syncthreads();
+          }
+        }
       }
       return;
     }
@@ -1240,9 +1270,11 @@ static hipError_t launch_cfg(const GemmArgs &g, const SideArgs *side, hipStream_
   }
   FuseArgs fa{};
   if (fz && fz->nprod > 0) {
+    // Side items of a fused launch run on the producer workgroups.
+    nside = 0;
     // 16 rows per producer while they fit beside the tiles on the 256 CUs (a
     // tile needs the producers' rows only in its last steps), else 32.
-    const int free = 256 - tm * tn - nside;
+    const int free = 256 - tm * tn;
     const int64_t T = fz->row.M;
     const int mb = ((T + 15) / 16 + 7) / 8 * 8 <= free ? 1 : 2;
     fz->row.mb = mb;
@@ -1310,23 +1342,34 @@ hipError_t launch_gemm_q(const GemmArgs &g, int bits, bool b_kmajor, const SideA
 
 // Producers only pay off on CUs the tiles leave idle: fused when the tile
 // shape is direct-to-LDS and 32-row producers fit beside the tiles.
-bool gemm_fusable(int M, int N) {
-  const int cfg = pick_shape(M, N, false);
+bool gemm_fusable(int M, int N, bool b_kmajor) {
+  const int cfg = pick_shape(M, N, b_kmajor);
   if (cfg == 2) return false;
   const long bm = cfg == 1 ? 256 : 128;
   const long tiles = ((M + bm - 1) / bm) * ((N + 127) / 128);
   return tiles + ((M + 31) / 32 + 7) / 8 * 8 <= 256;
 }
 
-hipError_t launch_gemm_fused(const GemmArgs &g, FuseArgs *fz, hipStream_t st) {
-  if (!fz || fz->nprod <= 0 || fz->row.vmode != V_ROW || fz->row.nsplit != 1 || fz->row.r < 1 ||
-      fz->row.r > 32 || g.r < 1 || !fz->sync || fz->gen == 0)
+hipError_t launch_gemm_fused(const GemmArgs &g, FuseArgs *fz, const SideArgs *side, hipStream_t st) {
+  const bool kmaj = fz && fz->row.vmode == V_KMAJ_TR;
+  if (!fz || fz->nprod <= 0 || (fz->row.vmode != V_ROW && !kmaj) || fz->row.nsplit != 1 || fz->row.r < 1 ||
+      fz->row.r > 32 || (kmaj && fz->row.r % 8) || g.r < 1 || g.M < 1 || !fz->sync || fz->gen == 0 ||
+      (side && !kmaj))
     return hipErrorInvalidValue;
+  if (kmaj) {
+    switch (pick_shape(g.M, g.N, true)) {
+      case 1:
+        return launch_cfg<BF16, 256, 128, 4, 2, 1, B_KMAJ_TR, 128, 3, 3, 2, 0, EPI_STORE, 2>(g, side, st, fz);
+      case 0:
+        return launch_cfg<BF16, 128, 128, 2, 2, 2, B_KMAJ_TR, 128, 4, 3, 2, 0, EPI_STORE, 2>(g, side, st, fz);
+    }
+    return hipErrorInvalidValue;
+  }
   switch (pick_shape(g.M, g.N, false)) {
     case 1:
-      return launch_cfg<BF16, 256, 128, 4, 2, 1, B_ROW, 128, 3, 3, 2, 0, EPI_STORE, 1>(g, nullptr, st, fz);
+      return launch_cfg<BF16, 256, 128, 4, 2, 1, B_ROW, 128, 3, 3, 2, 0, EPI_STORE, 2>(g, nullptr, st, fz);
     case 0:
-      return launch_cfg<BF16, 128, 128, 2, 2, 2, B_ROW, 128, 3, 3, 2, 0, EPI_STORE, 1>(g, nullptr, st, fz);
+      return launch_cfg<BF16, 128, 128, 2, 2, 2, B_ROW, 128, 3, 3, 2, 0, EPI_STORE, 2>(g, nullptr, st, fz);
   }
   return hipErrorInvalidValue;
 }

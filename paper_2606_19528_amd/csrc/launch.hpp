@@ -202,13 +202,16 @@ struct RowArgs {
 };
 hipError_t launch_row_skinny(const RowArgs &a, Dtype dt, hipStream_t st);
 
-// Fused rank-r pass of the forward: the first `nwg` workgroups of the GEMM
-// launch (a multiple of 8, so the tiles keep their XCD mapping) are
-// producers, one per 16 * row.mb rows, that compute u = x A^T over the whole
-// reduction axis (row: nsplit = 1, V_ROW) -- u and the LoRA-step operand
-// E(s u) -- ahead of the tiles, which need them only in their last (LoRA)
-// step.  They hand over through two 8-byte words of the workspace (8-byte
-// aligned; nothing else may use them during the launch):
+// Fused rank-r pass: the first `nwg` workgroups of the GEMM launch (a
+// multiple of 8, so the tiles keep their XCD mapping) are producers, one per
+// 16 * row.mb rows, that compute the rank-r product over the whole reduction
+// axis (row: nsplit = 1) -- forward: u = x A^T (V_ROW) and the LoRA-step
+// operand E(s u); backward: du = s dy B (V_KMAJ_TR) and E(du) -- ahead of the
+// tiles, which need them only in their last (LoRA) step.  In the backward the
+// producers then run the dA / dB side items: each waits, after counting
+// itself, until every producer has counted (dA = du^T x needs all of du).
+// They hand over through two 8-byte words of the workspace (8-byte aligned;
+// nothing else may use them during the launch):
 //   sync[0] = (gen << 32) | producers counted, sync[1] = tiles that passed.
 // Workgroup 0 arms the launch before its work (sync[0] = gen << 32, then,
 // released after it, sync[1] = 0).  A producer stores its rows coherently at
@@ -235,12 +238,15 @@ struct FuseArgs {
   int ncons;                 // consumers: the tiles (set by launch_gemm_fused)
 };
 
-// Whether the bf16 forward GEMM (row-major B) of this shape runs a tile
-// configuration that takes producer workgroups, and leaves the CUs for them.
-bool gemm_fusable(int M, int N);
-// The bf16 forward GEMM with producers at the front (fz->nprod > 0; chooses
-// fz->row.mb and sets fz->nprod, fz->nwg and fz->ncons).
-hipError_t launch_gemm_fused(const GemmArgs &g, FuseArgs *fz, hipStream_t st);
+// Whether the bf16 GEMM of this shape (forward: row-major B; backward:
+// k-major B) runs a tile configuration that takes producer workgroups, and
+// leaves the CUs for them.
+bool gemm_fusable(int M, int N, bool b_kmajor);
+// The bf16 GEMM with producers at the front (fz->nprod > 0; chooses
+// fz->row.mb and sets fz->nprod, fz->nwg and fz->ncons).  fz->row.vmode
+// selects the forward (V_ROW, side must be null) or the backward (V_KMAJ_TR,
+// side items run by the producers); dx rows are required (g.M >= 1).
+hipError_t launch_gemm_fused(const GemmArgs &g, FuseArgs *fz, const SideArgs *side, hipStream_t st);
 
 // Split of a row-skinny product over its reduction axis L, and rows per
 // workgroup.  Short T (below 2048): one 16-row tile per workgroup, enough
