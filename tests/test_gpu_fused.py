@@ -1,6 +1,7 @@
-"""GPU tests of the forward's fused rank-r pass: producer workgroups in the
-GEMM launch compute u = x A^T and hand it to the tiles through tagged counters
-in the workspace.
+"""GPU tests of the fused rank-r passes: producer workgroups in the GEMM
+launch compute u = x A^T (forward) or du = s dy B (backward, then the dA / dB
+side items) and hand them to the tiles through tagged counters in the
+workspace.
 
 The hand-over must hold when the workspace is reused by calls with other
 inputs and shapes, when it starts out with arbitrary bytes, and when the same
@@ -119,3 +120,22 @@ def test_graph_replay(orc):
         torch.cuda.synchronize()
         ref = oracle_lora(orc, inp, s)
         compare({k: v.cpu() for k, v in o.items()}, ref, torch.bfloat16, label=f"replay {it}")
+
+
+@pytest.mark.parametrize("shape,recompute", [((48, 2056, 1032, 8), False), ((48, 2056, 1032, 8), True),
+                                             ((200, 1032, 2056, 24), False)])
+def test_backward_side_items_on_producers(orc, shape, recompute):
+    """Fused backward: the producers of du then run the dA / dB side items,
+    here many more items than producers (3 or 13 producers, 26 items; ragged
+    column blocks, rank not a multiple of 16)."""
+    T, K, N, r = shape
+    s = 2.0
+    _announce(f"fused bwd side items T={T} K={K} N={N} r={r} recompute={recompute}")
+    inp = lora_inputs(T, K, N, r, seed=95)
+    d = {k: v.cuda() for k, v in inp.items()}
+    ws = _ws(T, K, N, r)
+    o = _buffers(T, K, N, r)
+    _step(d, o, s, ws, ws, recompute=recompute)
+    torch.cuda.synchronize()
+    ref = oracle_lora(orc, inp, s)
+    compare({k: v.cpu() for k, v in o.items()}, ref, torch.bfloat16, label="side items on producers")
