@@ -12,8 +12,11 @@
 // coalesced), transposes the VEC x VEC block in registers so a lane holds VEC
 // consecutive tokens of one column -- the matrix-core operand whose reduction
 // axis is the token axis -- and accumulates a (16*VEC) x 32 tile, two token
-// steps in flight.  The waves take interleaved token steps; their tiles are
-// summed in LDS by a fixed pairwise tree, so the result is deterministic.
+// steps in flight.  Eight (virtual) waves take interleaved token steps; their
+// tiles are summed by a fixed pairwise tree, so the result is deterministic
+// and the same whether the launch has eight waves per workgroup or four (a
+// wave then runs virtual waves w and w + 4 and adds the two tiles first, the
+// tree's first round).
 #pragma once
 
 #include "kernels.hpp"
@@ -22,6 +25,18 @@
 namespace lora {
 
 constexpr int SIDE_JB = 2;  // rank indices per item: 32
+
+template <int V>
+struct SideIC {
+  static constexpr int value = V;
+};
+template <int B, int E, class F>
+__device__ __forceinline__ void static_for_side(F &&f) {
+  if constexpr (B < E) {
+    f(SideIC<B>());
+    static_for_side<B + 1, E>(f);
+  }
+}
 
 template <class E>
 struct SideShape {
@@ -80,11 +95,15 @@ __device__ void side_item(const SideArgs &s, int item, char *smem) {
   const int col = c0 + cl * VEC;
   const T *Xp = (const T *)job.X;
 
-  f32x4 acc[VEC][JB];
+  constexpr int VW = 8, PER = VW / NW;  // virtual waves, per real wave
+  static_assert(NW * PER == VW, "four or eight waves");
+  f32x4 acc[PER][VEC][JB];
 #pragma unroll
-  for (int q = 0; q < VEC; ++q)
+  for (int p = 0; p < PER; ++p)
 #pragma unroll
-    for (int jb = 0; jb < JB; ++jb) acc[q][jb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int q = 0; q < VEC; ++q)
+#pragma unroll
+      for (int jb = 0; jb < JB; ++jb) acc[p][q][jb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   // Loads go through buffer resources based at the step's first token row
   // (so every offset stays small whatever T is): rows past T and columns past
@@ -122,7 +141,7 @@ __device__ void side_item(const SideArgs &s, int item, char *smem) {
       }
     }
   };
-  auto compute = [&](const Step &st) {
+  auto compute = [&](const Step &st, f32x4(&a)[VEC][JB]) {
     u32x4 xt[VEC], vf[JB];
 #pragma unroll
     for (int jb = 0; jb < JB; ++jb) vf[jb] = pack_vec(E(), st.v[jb]);
@@ -130,22 +149,35 @@ __device__ void side_item(const SideArgs &s, int item, char *smem) {
 #pragma unroll
     for (int q = 0; q < VEC; ++q)
 #pragma unroll
-      for (int jb = 0; jb < JB; ++jb) mma16(E(), acc[q][jb], xt[q], vf[jb]);
+      for (int jb = 0; jb < JB; ++jb) mma16(E(), a[q][jb], xt[q], vf[jb]);
   };
   {
+    // Step n of this wave: virtual wave w + NW (n % PER), its (n / PER)-th
+    // token step.  Each virtual wave runs its own steps in ascending order,
+    // exactly as a wave of an eight-wave workgroup would.
+    const int w0 = __builtin_amdgcn_readfirstlane(wave);
+    auto tb_of = [&](int n) { return (w0 + NW * (n % PER) + VW * (n / PER)) * ROWS; };
     Step cur, nxt;
-    int tb = __builtin_amdgcn_readfirstlane(wave) * ROWS;
-    load(tb, cur);
-    for (; tb < t_end; tb += NW * ROWS) {
-      load(tb + NW * ROWS, nxt);  // past the end: zeros, no memory traffic
-      compute(cur);
-      cur = nxt;
+    load(tb_of(0), cur);
+    for (int n = 0; tb_of(n) < t_end; n += PER) {
+      static_for_side<0, PER>([&](auto P) {
+        constexpr int p = decltype(P)::value;
+        load(tb_of(n + p + 1), nxt);  // past the end: zeros, no memory traffic
+        if (tb_of(n + p) < t_end) compute(cur, acc[p]);
+        cur = nxt;
+      });
     }
+#pragma unroll
+    for (int p = 1; p < PER; ++p)
+#pragma unroll
+      for (int q = 0; q < VEC; ++q)
+#pragma unroll
+        for (int jb = 0; jb < JB; ++jb) acc[0][q][jb] += acc[p][q][jb];
   }
 
   // Pairwise tree over waves: in round h the upper half of the active waves
   // writes, the lower half adds (wave w receives wave w + h).
-  // acc[q][jb] element i: local column (4g + i) * VEC + q, rank index 16 jb + cl.
+  // acc[0][q][jb] element i: local column (4g + i) * VEC + q, rank index 16 jb + cl.
   float *red = (float *)smem;
 #pragma unroll
   for (int h = NW / 2; h >= 1; h /= 2) {
@@ -157,7 +189,7 @@ __device__ void side_item(const SideArgs &s, int item, char *smem) {
 #pragma unroll
         for (int jb = 0; jb < JB; ++jb)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) slot[((4 * g + i) * VEC + q) * RS + jb * 16 + cl] = acc[q][jb][i];
+          for (int i = 0; i < 4; ++i) slot[((4 * g + i) * VEC + q) * RS + jb * 16 + cl] = acc[0][q][jb][i];
     }
     __syncthreads();
     if (wave < h) {
@@ -167,7 +199,7 @@ __device__ void side_item(const SideArgs &s, int item, char *smem) {
 #pragma unroll
         for (int jb = 0; jb < JB; ++jb)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) acc[q][jb][i] += slot[((4 * g + i) * VEC + q) * RS + jb * 16 + cl];
+          for (int i = 0; i < 4; ++i) acc[0][q][jb][i] += slot[((4 * g + i) * VEC + q) * RS + jb * 16 + cl];
     }
   }
   // Wave 0 holds the item's tile: scale and store it.
@@ -182,7 +214,7 @@ __device__ void side_item(const SideArgs &s, int item, char *smem) {
           const int l = c0 + (4 * g + i) * VEC + q;
           const int j = jb * 16 + cl;
           if (l < job.L && j < jn) {
-            const float v = job.scale * acc[q][jb][i];
+            const float v = job.scale * acc[0][q][jb][i];
             if (job.transpose_out)
               job.out[(int64_t)(jg + j) * job.L + l] = v;
             else

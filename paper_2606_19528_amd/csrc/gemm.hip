@@ -150,7 +150,7 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   constexpr int NWV = NT / 64;
   // Row-major B is loaded in whole loads per wave (rows past BN read zeros);
   // k-major B rows take 256 bytes in LDS (columns past BN read zeros).
-  constexpr int DB_ROWS = (BN + 8 * NWV - 1) / (8 * NWV) * (8 * NWV);
+  constexpr int DB_ROWS = (BN + (1024 / BKB) * NWV - 1) / ((1024 / BKB) * NWV) * ((1024 / BKB) * NWV);
   constexpr int DBRB = (BN * 2 + 255) / 256 * 256;
   constexpr int DA_BYTES = BM * BKB;
   constexpr int DB_BYTES = BMODE == B_KMAJ_TR ? BKE * DBRB : DB_ROWS * BKB;
@@ -180,10 +180,10 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile");
   static_assert(BMODE != B_KMAJ_TR || ES == 2, "transposed LDS reads are bf16");
   static_assert(DMA ? (NBUF == 3 || NBUF == 4) : (NBUF == 2 || NBUF == 3), "LDS ring depth");
-  static_assert(!DMA || (QB == 0 && ES == 2 && FS == 2 && BKB == 128 && BMODE != B_KMAJ_REG &&
+  static_assert(!DMA || (QB == 0 && ES == 2 && FS == 2 && (BKB == 128 || BKB == 64) && BMODE != B_KMAJ_REG &&
                          DA_BYTES % (1024 * NWV) == 0 && DB_BYTES % (1024 * NWV) == 0 &&
-                         (BMODE != B_KMAJ_TR || DBRB == 256)),
-                "direct-to-LDS stages: bf16, 64-deep stages, whole 1 KB loads per wave");
+                         (BMODE != B_KMAJ_TR || DBRB == 256 || DBRB == 512)),
+                "direct-to-LDS stages: bf16, 64- or 32-deep stages, whole 1 KB loads per wave");
   static_assert(RD >= 2 && RD <= 4, "register ring depth");
   static_assert(!FS || DMA || NBUF == 2, "staged fragments use two LDS buffers");
   // Quantized B (QB = 4 or 8 bits): each thread dequantizes one piece of 16
@@ -361,11 +361,15 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   // Direct-to-LDS loads: one load instruction of a wave moves 64 x 16 bytes
   // into 1 KB of LDS in lane order, so the LDS layout is fixed and the lanes
   // choose which global chunk lands where.  k-contiguous operands (A; B when
-  // row-major): load q of a stage covers tile rows 8q .. 8q+7 (BKB = 128 bytes
-  // each), and row r keeps its 16-byte chunk c at chunk c ^ swz(r),
-  // swz(r) = (r & 7) ^ ((r >> 3) & 1), which puts the fragment reads of eight
-  // and of sixteen consecutive rows in distinct banks.  k-major B: load q
-  // covers k-rows 4q .. 4q+3 (BN * 2 bytes each), chunk c at c ^ 4 (r & 3).
+  // row-major): load q of a stage covers tile rows RPK q .. RPK q + RPK - 1
+  // (RPK = 8 rows of BKB = 128 bytes, or 16 rows of 64 bytes), and row r keeps
+  // its 16-byte chunk c at chunk c ^ swz(r): swz(r) = (r & 7) ^ ((r >> 3) & 1)
+  // for 128-byte rows, (r >> 2) & 3 for 64-byte rows, which puts the fragment
+  // reads of sixteen consecutive rows in distinct banks.  k-major B: load q
+  // covers k-rows KPK q .. KPK q + KPK - 1 (DBRB = 256 or 512 bytes each, KPK
+  // = 4 or 2), chunk c at c ^ 4 (r & 3).
+  constexpr int RPK = 1024 / BKB, KPK = 1024 / DBRB;
+  auto swz_row = [](int r) { return CPR == 8 ? (r & 7) ^ ((r >> 3) & 1) : (r >> 2) & 3; };
   const int wv = __builtin_amdgcn_readfirstlane(wave);
   uint32_t dA[DMA ? DA_PW : 1], dA2[DMA ? DA_PW : 1], dB[DMA ? DB_PW : 1], dB2[DMA ? DB_PW : 1];
   int dkA[DMA ? DA_PW : 1], dkB[DMA ? DB_PW : 1];
@@ -373,8 +377,8 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
 #pragma unroll
     for (int i = 0; i < DA_PW; ++i) {
       const int q = wv + i * NWV;
-      const int r = 8 * q + (lane >> 3);
-      const int c = (lane & 7) ^ (lane >> 3) ^ (q & 1);
+      const int r = RPK * q + lane / CPR;
+      const int c = (lane % CPR) ^ swz_row(r);
       dkA[i] = c * 8;
       dA[i] = (uint32_t)(r * g.lda * ES + c * 16);
       dA2[i] = (uint32_t)(r * g.lda2 * ES + c * 16);
@@ -383,14 +387,15 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
     for (int i = 0; i < DB_PW; ++i) {
       const int q = wv + i * NWV;
       if constexpr (BMODE == B_ROW) {
-        const int r = 8 * q + (lane >> 3);
-        const int c = (lane & 7) ^ (lane >> 3) ^ (q & 1);
+        const int r = RPK * q + lane / CPR;
+        const int c = (lane % CPR) ^ swz_row(r);
         dkB[i] = c * 8;
         dB[i] = (uint32_t)(r * g.ldb * ES + c * 16);
         dB2[i] = (uint32_t)(r * g.ldb2 * ES + c * 16);
       } else {
-        const int r = 4 * q + (lane >> 4);
-        const int c = (lane & 15) ^ (4 * ((lane >> 4) & 3));
+        constexpr int CPK = DBRB / 16;  // chunks per k-row
+        const int r = KPK * q + lane / CPK;
+        const int c = (lane % CPK) ^ (4 * (r & 3));
         const bool ok = c * 8 < BN && n0 + c * 8 < g.N;
         dkB[i] = 0;
         dB[i] = ok ? (uint32_t)(r * g.ldb * ES + c * 16) : OOB;
@@ -680,7 +685,7 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
     }
   };
   // Fragment reads from a direct-to-LDS stage (swizzled chunks, see dma_stage).
-  const int swz_a = (lrow & 7) ^ ((lrow >> 3) & 1);
+  const int swz_a = CPR == 8 ? (lrow & 7) ^ ((lrow >> 3) & 1) : (lrow >> 2) & 3;  // swz_row of the lane's rows
   const int swz_t = 4 * ((iq >> 2) & 3);
   auto read_frags_d = [&](auto BUF, int s, Frag &f) {
     const char *sA = ring_a(BUF);
@@ -1301,16 +1306,17 @@ int side_workgroups(const SideArgs &s, Dtype dt) {
 // Tile shape per problem: an estimate of the time of each candidate -- full
 // waves of tiles over the 256 CUs times the per-tile cost.  Relative per-CU
 // throughput measured on MI355X at T = 2048 and 4096 over the shapes of the
-// Llama and Qwen layers, for 128x128 and 256x128 (both direct-to-LDS) and
-// 256x256 (register-staged): row-major B 0.84 : 0.99 : 0.95; k-major B (the
-// transposed reads cost the small tile more) 0.76 : 1.04 : 1.0.
+// Llama and Qwen layers, for 128x128, 256x128 (8 waves, 64-deep stages) and
+// 256x256 (4 waves of 128x128, 32-deep stages), all direct-to-LDS: row-major
+// B 0.84 : 0.99 : 1.02; k-major B (the transposed reads cost the small tile
+// more) 0.76 : 1.04 : 1.11.
 static int pick_shape(int M, int N, bool b_kmajor) {
   auto cost = [&](int bm, int bn, double eff) {
     const long tiles = (long)((M + bm - 1) / bm) * ((N + bn - 1) / bn);
     return (double)((tiles + 255) / 256) * bm * bn / eff;
   };
   const double c0 = cost(128, 128, b_kmajor ? 0.76 : 0.84), c1 = cost(256, 128, b_kmajor ? 1.04 : 0.99),
-               c2 = cost(256, 256, b_kmajor ? 1.0 : 0.95);
+               c2 = cost(256, 256, b_kmajor ? 1.11 : 1.02);
   if (c2 <= c1 && c2 <= c0) return 2;
   return c1 < c0 ? 1 : 0;
 }
@@ -1379,8 +1385,8 @@ hipError_t launch_gemm(const GemmArgs &g, Dtype dt, bool b_kmajor, const SideArg
   if (dt == DT_BF16) {
     switch (pick_shape(g.M, g.N, b_kmajor)) {
       case 2:
-        return b_kmajor ? launch_cfg<BF16, 256, 256, 4, 2, 1, B_KMAJ_TR, 128, 2, 2, 0>(g, side, st)
-                        : launch_cfg<BF16, 256, 256, 4, 2, 1, B_ROW, 128, 2, 2, 0>(g, side, st);
+        return b_kmajor ? launch_cfg<BF16, 256, 256, 2, 2, 1, B_KMAJ_TR, 64, 3, 3, 2, 0, EPI_STORE, 1>(g, side, st)
+                        : launch_cfg<BF16, 256, 256, 2, 2, 1, B_ROW, 64, 4, 3, 2, 0, EPI_STORE, 1>(g, side, st);
       case 1:
         return b_kmajor ? launch_cfg<BF16, 256, 128, 4, 2, 1, B_KMAJ_TR, 128, 3, 3, 2, 0, EPI_STORE, 1>(g, side, st)
                         : launch_cfg<BF16, 256, 128, 4, 2, 1, B_ROW, 128, 3, 3, 2, 0, EPI_STORE, 1>(g, side, st);
