@@ -368,8 +368,17 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   // reads of sixteen consecutive rows in distinct banks.  k-major B: load q
   // covers k-rows KPK q .. KPK q + KPK - 1 (DBRB = 256 or 512 bytes each, KPK
   // = 4 or 2), chunk c at c ^ 4 (r & 3).
-  constexpr int RPK = 1024 / BKB, KPK = 1024 / DBRB;
-  auto swz_row = [](int r) { return CPR == 8 ? (r & 7) ^ ((r >> 3) & 1) : (r >> 2) & 3; };
+  // (Written out per layout: the general forms cost the fused kernels
+  // registers, and spills, that these do not.)
+  auto chunk_row = [&](int q, int &r, int &c) __attribute__((always_inline)) {
+    if constexpr (CPR == 8) {
+      r = 8 * q + (lane >> 3);
+      c = (lane & 7) ^ (lane >> 3) ^ (q & 1);
+    } else {
+      r = 16 * q + (lane >> 2);
+      c = (lane & 3) ^ ((lane >> 4) & 3);
+    }
+  };
   const int wv = __builtin_amdgcn_readfirstlane(wave);
   uint32_t dA[DMA ? DA_PW : 1], dA2[DMA ? DA_PW : 1], dB[DMA ? DB_PW : 1], dB2[DMA ? DB_PW : 1];
   int dkA[DMA ? DA_PW : 1], dkB[DMA ? DB_PW : 1];
@@ -377,8 +386,8 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
 #pragma unroll
     for (int i = 0; i < DA_PW; ++i) {
       const int q = wv + i * NWV;
-      const int r = RPK * q + lane / CPR;
-      const int c = (lane % CPR) ^ swz_row(r);
+      int r, c;
+      chunk_row(q, r, c);
       dkA[i] = c * 8;
       dA[i] = (uint32_t)(r * g.lda * ES + c * 16);
       dA2[i] = (uint32_t)(r * g.lda2 * ES + c * 16);
@@ -387,15 +396,14 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
     for (int i = 0; i < DB_PW; ++i) {
       const int q = wv + i * NWV;
       if constexpr (BMODE == B_ROW) {
-        const int r = RPK * q + lane / CPR;
-        const int c = (lane % CPR) ^ swz_row(r);
+        int r, c;
+        chunk_row(q, r, c);
         dkB[i] = c * 8;
         dB[i] = (uint32_t)(r * g.ldb * ES + c * 16);
         dB2[i] = (uint32_t)(r * g.ldb2 * ES + c * 16);
       } else {
-        constexpr int CPK = DBRB / 16;  // chunks per k-row
-        const int r = KPK * q + lane / CPK;
-        const int c = (lane % CPK) ^ (4 * (r & 3));
+        const int r = DBRB == 256 ? 4 * q + (lane >> 4) : 2 * q + (lane >> 5);
+        const int c = DBRB == 256 ? (lane & 15) ^ (4 * ((lane >> 4) & 3)) : (lane & 31) ^ (4 * (r & 3));
         const bool ok = c * 8 < BN && n0 + c * 8 < g.N;
         dkB[i] = 0;
         dB[i] = ok ? (uint32_t)(r * g.ldb * ES + c * 16) : OOB;
@@ -685,7 +693,7 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
     }
   };
   // Fragment reads from a direct-to-LDS stage (swizzled chunks, see dma_stage).
-  const int swz_a = CPR == 8 ? (lrow & 7) ^ ((lrow >> 3) & 1) : (lrow >> 2) & 3;  // swz_row of the lane's rows
+  const int swz_a = CPR == 8 ? (lrow & 7) ^ ((lrow >> 3) & 1) : (lrow >> 2) & 3;  // the lane's rows' swizzle
   const int swz_t = 4 * ((iq >> 2) & 3);
   auto read_frags_d = [&](auto BUF, int s, Frag &f) {
     const char *sA = ring_a(BUF);
