@@ -81,6 +81,17 @@ def test_long_t_row_tiles(orc, shape, recompute):
     _case(orc, T, K, N, r, 2.0 * r, seed=53, recompute=recompute)
 
 
+# The widest tiles (256 x 256, 32-deep stages) are picked only where they fill
+# the machine in fewer waves: these shapes select them for the forward
+# (d_out = 8192) and for dx (d_in = 8192), with a reduction axis that is not a
+# multiple of the stage depth.  Sampled rows of y and dx; dA and dB in full.
+@pytest.mark.parametrize("shape", [(4096, 264, 8192, 16), (4096, 8192, 264, 24)])
+def test_wide_tiles(orc, shape):
+    T, K, N, r = shape
+    rows = list(range(0, T, 61)) + [T - 1]
+    _case(orc, T, K, N, r, 2.0 * r, seed=59, rows=rows)
+
+
 def test_split_forward_without_u_save(orc):
     # the partial sums of u stay in the workspace; y must not depend on u_save
     T, K, N, r = 256, 1800, 1032, 16
