@@ -1317,14 +1317,17 @@ int side_workgroups(const SideArgs &s, Dtype dt) {
 // Llama and Qwen layers, for 128x128, 256x128 (8 waves, 64-deep stages) and
 // 256x256 (4 waves of 128x128, 32-deep stages), all direct-to-LDS: row-major
 // B 0.84 : 0.99 : 1.02; k-major B (the transposed reads cost the small tile
-// more) 0.76 : 1.04 : 1.11.
+// more) 0.76 : 1.04 : 1.11.  128x64 (0.56 row-major, 0.47 k-major) only where
+// 128x128 tiles would leave most CUs idle (the Qwen k/v forward, 2048 -> 256).
+// Returns 0: 128x128, 1: 256x128, 2: 256x256, 3: 128x64.
 static int pick_shape(int M, int N, bool b_kmajor) {
   auto cost = [&](int bm, int bn, double eff) {
     const long tiles = (long)((M + bm - 1) / bm) * ((N + bn - 1) / bn);
     return (double)((tiles + 255) / 256) * bm * bn / eff;
   };
   const double c0 = cost(128, 128, b_kmajor ? 0.76 : 0.84), c1 = cost(256, 128, b_kmajor ? 1.04 : 0.99),
-               c2 = cost(256, 256, b_kmajor ? 1.11 : 1.02);
+               c2 = cost(256, 256, b_kmajor ? 1.11 : 1.02), c3 = cost(128, 64, b_kmajor ? 0.47 : 0.56);
+  if (c3 < c0 && c3 < c1 && c3 < c2) return 3;
   if (c2 <= c1 && c2 <= c0) return 2;
   return c1 < c0 ? 1 : 0;
 }
@@ -1359,8 +1362,8 @@ hipError_t launch_gemm_q(const GemmArgs &g, int bits, bool b_kmajor, const SideA
 bool gemm_fusable(int M, int N, bool b_kmajor) {
   const int cfg = pick_shape(M, N, b_kmajor);
   if (cfg == 2) return false;
-  const long bm = cfg == 1 ? 256 : 128;
-  const long tiles = ((M + bm - 1) / bm) * ((N + 127) / 128);
+  const long bm = cfg == 1 ? 256 : 128, bn = cfg == 3 ? 64 : 128;
+  const long tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
   return tiles + ((M + 31) / 32 + 7) / 8 * 8 <= 256;
 }
 
@@ -1376,6 +1379,8 @@ hipError_t launch_gemm_fused(const GemmArgs &g, FuseArgs *fz, const SideArgs *si
         return launch_cfg<BF16, 256, 128, 4, 2, 1, B_KMAJ_TR, 128, 3, 3, 2, 0, EPI_STORE, 2>(g, side, st, fz);
       case 0:
         return launch_cfg<BF16, 128, 128, 2, 2, 2, B_KMAJ_TR, 128, 4, 3, 2, 0, EPI_STORE, 2>(g, side, st, fz);
+      case 3:
+        return launch_cfg<BF16, 128, 64, 2, 2, 2, B_KMAJ_TR, 128, 4, 3, 2, 0, EPI_STORE, 2>(g, side, st, fz);
     }
     return hipErrorInvalidValue;
   }
@@ -1384,6 +1389,8 @@ hipError_t launch_gemm_fused(const GemmArgs &g, FuseArgs *fz, const SideArgs *si
       return launch_cfg<BF16, 256, 128, 4, 2, 1, B_ROW, 128, 3, 3, 2, 0, EPI_STORE, 2>(g, nullptr, st, fz);
     case 0:
       return launch_cfg<BF16, 128, 128, 2, 2, 2, B_ROW, 128, 3, 3, 2, 0, EPI_STORE, 2>(g, nullptr, st, fz);
+    case 3:
+      return launch_cfg<BF16, 128, 64, 2, 2, 2, B_ROW, 128, 3, 3, 2, 0, EPI_STORE, 2>(g, nullptr, st, fz);
   }
   return hipErrorInvalidValue;
 }
@@ -1398,6 +1405,9 @@ hipError_t launch_gemm(const GemmArgs &g, Dtype dt, bool b_kmajor, const SideArg
       case 1:
         return b_kmajor ? launch_cfg<BF16, 256, 128, 4, 2, 1, B_KMAJ_TR, 128, 3, 3, 2, 0, EPI_STORE, 1>(g, side, st)
                         : launch_cfg<BF16, 256, 128, 4, 2, 1, B_ROW, 128, 3, 3, 2, 0, EPI_STORE, 1>(g, side, st);
+      case 3:
+        return b_kmajor ? launch_cfg<BF16, 128, 64, 2, 2, 2, B_KMAJ_TR, 128, 4, 3, 2, 0, EPI_STORE, 1>(g, side, st)
+                        : launch_cfg<BF16, 128, 64, 2, 2, 2, B_ROW, 128, 3, 3, 2, 0, EPI_STORE, 1>(g, side, st);
       default:
         return b_kmajor ? launch_cfg<BF16, 128, 128, 2, 2, 2, B_KMAJ_TR, 128, 4, 3, 2, 0, EPI_STORE, 1>(g, side, st)
                         : launch_cfg<BF16, 128, 128, 2, 2, 2, B_ROW, 128, 3, 3, 2, 0, EPI_STORE, 1>(g, side, st);
