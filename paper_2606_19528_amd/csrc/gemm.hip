@@ -323,6 +323,12 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
         (void *)((const char *)g.B2 + (int64_t)n0 * g.ldb2 * ES), (short)0,
         g.r > 0 ? (int)(nrows * g.ldb2 * ES) : 0, 0x00020000);
   }
+  // k-major B whole (columns of the tile from n0), for the loads of full main
+  // stages: their k-rows all lie below K, the stage start goes in soffset.
+  __amdgpu_buffer_rsrc_t rsBk;
+  if constexpr (BMODE == B_KMAJ_TR)
+    rsBk = __builtin_amdgcn_make_buffer_rsrc((void *)((const char *)g.B + (int64_t)n0 * ES), (short)0,
+                                             (int)((int64_t)g.K * g.ldb * ES), 0x00020000);
   uint32_t va[A_PER], va2[A_PER], vb[BMODE == B_KMAJ_REG ? KB_PER : B_PER], vb2[B_PER];
   int kca[A_PER], kcb[B_PER];
 #pragma unroll
@@ -716,9 +722,21 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
       }
     }
   };
-  // One direct-to-LDS load (q < IPS) of stage kt into ring buffer BUF.
-  auto dma_one = [&](auto BUF, int kt, auto QI) __attribute__((always_inline)) {
-    if constexpr (DMA) {
+  // One direct-to-LDS load (q < IPS) of stage kt into ring buffer BUF.  With
+  // MASK = 0 the stage is a full main stage (every k below K, no LoRA step),
+  // so the lanes' precomputed offsets need no per-load selection.
+  auto dma_one = [&](auto BUF, int kt, auto QI, auto MASK) __attribute__((always_inline)) {
+    if constexpr (DMA && !decltype(MASK)::value) {
+      constexpr int q = decltype(QI)::value;
+      const int k0 = stage_k0(kt);
+      if constexpr (q < DA_PW) {
+        dma16(rsA, ring_a(BUF) + (wv + q * NWV) * 1024, dA[q], k0 * ES);
+      } else {
+        constexpr int i = q - DA_PW;
+        if constexpr (BMODE == B_ROW) dma16(rsB, ring_b(BUF) + (wv + i * NWV) * 1024, dB[i], k0 * ES);
+        else dma16(rsBk, ring_b(BUF) + (wv + i * NWV) * 1024, dB[i], (int)((int64_t)k0 * g.ldb * ES));
+      }
+    } else if constexpr (DMA) {
       constexpr int q = decltype(QI)::value;
       const bool lora = is_lora(kt);
       const int k0 = stage_k0(kt);
@@ -834,7 +852,7 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
     read_stage_d(IC<0>(), F[0]);
-    auto step = [&](auto PH, int kt) __attribute__((always_inline)) {
+    auto step = [&](auto PH, int kt, auto MASK) __attribute__((always_inline)) {
       constexpr int P = decltype(PH)::value;  // kt % UN
       constexpr int V = (NBUF - 2) * IPS;     // stage kt + 1 landed
       __builtin_amdgcn_s_waitcnt((V & 15) | ((V >> 4) << 14) | (7 << 4));  // and lgkmcnt(0)
@@ -853,7 +871,7 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
         constexpr int ri = decltype(RI)::value;
         read_one_d(IC<(P + 1) % NBUF>(), RI, F[(P + 1) % 2]);
         static_for<ri * IPS / NRO, (ri + 1) * IPS / NRO>(
-            [&](auto QI) { dma_one(IC<P % NBUF>(), kt + NBUF, QI); });
+            [&](auto QI) { dma_one(IC<P % NBUF>(), kt + NBUF, QI, MASK); });
       });
       mma_stage(F[P % 2]);
       constexpr int NM = SPW * FM * FN;
@@ -866,11 +884,23 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
       });
       __builtin_amdgcn_sched_barrier(0);
     };
+    // Steps whose loads fill a full main stage (stage kt + NBUF below the K
+    // tail) run unmasked; the K tail, the LoRA stages and the stages past the
+    // end (zeros) run masked.
+    // (Launches with producers, and the 256 x 128 tile with k-major B, keep
+    // one loop: the second copy of the steps costs them registers and spills.)
+    constexpr bool SPLIT = !FUSE && !(BM == 256 && BN == 128 && BMODE == B_KMAJ_TR);
+    const bool whole_ok = BMODE != B_KMAJ_TR || (int64_t)g.K * g.ldb * ES < (int64_t)1 << 31;
+    const int nb = QB || !whole_ok ? 0 : g.K / BKE - NBUF;
     int kt = 0;
-    for (; kt + UN <= nk; kt += UN) static_for<0, UN>([&](auto PH) { step(PH, kt + decltype(PH)::value); });
+    if constexpr (SPLIT)
+      for (; kt + UN <= nb; kt += UN)
+        static_for<0, UN>([&](auto PH) { step(PH, kt + decltype(PH)::value, IC<0>()); });
+    for (; kt + UN <= nk; kt += UN)
+      static_for<0, UN>([&](auto PH) { step(PH, kt + decltype(PH)::value, IC<1>()); });
     static_for<0, UN - 1>([&](auto PH) {
       constexpr int P = decltype(PH)::value;
-      if (kt + P < nk) step(PH, kt + P);
+      if (kt + P < nk) step(PH, kt + P, IC<1>());
     });
     // The loads of the stages past the end still write LDS: drain them before
     // the buffers are reused.
