@@ -1349,14 +1349,21 @@ int side_workgroups(const SideArgs &s, Dtype dt) {
 // B 0.84 : 0.99 : 1.02; k-major B (the transposed reads cost the small tile
 // more) 0.76 : 1.04 : 1.11.  128x64 (0.56 row-major, 0.47 k-major) only where
 // 128x128 tiles would leave most CUs idle (the Qwen k/v forward, 2048 -> 256).
-// Returns 0: 128x128, 1: 256x128, 2: 256x256, 3: 128x64.
-static int pick_shape(int M, int N, bool b_kmajor) {
+// 256x192 (4 waves of 128x96, 32-deep stages; 0.88 row-major, 0.91 k-major)
+// where it alone fills the 256 CUs in one wave: a 4096 x 3072 output, 5-8 %
+// faster there than three waves of 128x128 or 192 tiles of 256x256.  Not for
+// launches with token-reduction side items: with every CU holding a tile,
+// those run after the tiles instead of beside them (+7 % on such launches).
+// Returns 0: 128x128, 1: 256x128, 2: 256x256, 3: 128x64, 4: 256x192.
+static int pick_shape(int M, int N, bool b_kmajor, bool with_side) {
   auto cost = [&](int bm, int bn, double eff) {
     const long tiles = (long)((M + bm - 1) / bm) * ((N + bn - 1) / bn);
     return (double)((tiles + 255) / 256) * bm * bn / eff;
   };
   const double c0 = cost(128, 128, b_kmajor ? 0.76 : 0.84), c1 = cost(256, 128, b_kmajor ? 1.04 : 0.99),
-               c2 = cost(256, 256, b_kmajor ? 1.11 : 1.02), c3 = cost(128, 64, b_kmajor ? 0.47 : 0.56);
+               c2 = cost(256, 256, b_kmajor ? 1.11 : 1.02), c3 = cost(128, 64, b_kmajor ? 0.47 : 0.56),
+               c4 = cost(256, 192, b_kmajor ? 0.91 : 0.88);
+  if (!with_side && c4 < c0 && c4 < c1 && c4 < c2 && c4 < c3) return 4;
   if (c3 < c0 && c3 < c1 && c3 < c2) return 3;
   if (c2 <= c1 && c2 <= c0) return 2;
   return c1 < c0 ? 1 : 0;
@@ -1390,8 +1397,8 @@ hipError_t launch_gemm_q(const GemmArgs &g, int bits, bool b_kmajor, const SideA
 // Producers only pay off on CUs the tiles leave idle: fused when the tile
 // shape is direct-to-LDS and 32-row producers fit beside the tiles.
 bool gemm_fusable(int M, int N, bool b_kmajor) {
-  const int cfg = pick_shape(M, N, b_kmajor);
-  if (cfg == 2) return false;
+  const int cfg = pick_shape(M, N, b_kmajor, b_kmajor);
+  if (cfg == 2 || cfg == 4) return false;
   const long bm = cfg == 1 ? 256 : 128, bn = cfg == 3 ? 64 : 128;
   const long tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
   return tiles + ((M + 31) / 32 + 7) / 8 * 8 <= 256;
@@ -1404,7 +1411,7 @@ hipError_t launch_gemm_fused(const GemmArgs &g, FuseArgs *fz, const SideArgs *si
       (side && !kmaj))
     return hipErrorInvalidValue;
   if (kmaj) {
-    switch (pick_shape(g.M, g.N, true)) {
+    switch (pick_shape(g.M, g.N, true, true)) {
       case 1:
         return launch_cfg<BF16, 256, 128, 4, 2, 1, B_KMAJ_TR, 128, 3, 3, 2, 0, EPI_STORE, 2>(g, side, st, fz);
       case 0:
@@ -1414,7 +1421,7 @@ hipError_t launch_gemm_fused(const GemmArgs &g, FuseArgs *fz, const SideArgs *si
     }
     return hipErrorInvalidValue;
   }
-  switch (pick_shape(g.M, g.N, false)) {
+  switch (pick_shape(g.M, g.N, false, false)) {
     case 1:
       return launch_cfg<BF16, 256, 128, 4, 2, 1, B_ROW, 128, 3, 3, 2, 0, EPI_STORE, 2>(g, nullptr, st, fz);
     case 0:
@@ -1428,10 +1435,13 @@ hipError_t launch_gemm_fused(const GemmArgs &g, FuseArgs *fz, const SideArgs *si
 hipError_t launch_gemm(const GemmArgs &g, Dtype dt, bool b_kmajor, const SideArgs *side,
                        hipStream_t st) {
   if (dt == DT_BF16) {
-    switch (pick_shape(g.M, g.N, b_kmajor)) {
+    switch (pick_shape(g.M, g.N, b_kmajor, side != nullptr)) {
       case 2:
         return b_kmajor ? launch_cfg<BF16, 256, 256, 2, 2, 1, B_KMAJ_TR, 64, 3, 3, 2, 0, EPI_STORE, 1>(g, side, st)
                         : launch_cfg<BF16, 256, 256, 2, 2, 1, B_ROW, 64, 4, 3, 2, 0, EPI_STORE, 1>(g, side, st);
+      case 4:
+        return b_kmajor ? launch_cfg<BF16, 256, 192, 2, 2, 1, B_KMAJ_TR, 64, 3, 3, 2, 0, EPI_STORE, 1>(g, side, st)
+                        : launch_cfg<BF16, 256, 192, 2, 2, 1, B_ROW, 64, 4, 3, 2, 0, EPI_STORE, 1>(g, side, st);
       case 1:
         return b_kmajor ? launch_cfg<BF16, 256, 128, 4, 2, 1, B_KMAJ_TR, 128, 3, 3, 2, 0, EPI_STORE, 1>(g, side, st)
                         : launch_cfg<BF16, 256, 128, 4, 2, 1, B_ROW, 128, 3, 3, 2, 0, EPI_STORE, 1>(g, side, st);

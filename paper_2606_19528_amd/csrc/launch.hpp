@@ -239,8 +239,8 @@ struct FuseArgs {
 };
 
 // Whether the bf16 GEMM of this shape (forward: row-major B; backward:
-// k-major B) runs a tile configuration that takes producer workgroups, and
-// leaves the CUs for them.
+// k-major B, carrying the dA / dB side items) runs a tile configuration that
+// takes producer workgroups, and leaves the CUs for them.
 bool gemm_fusable(int M, int N, bool b_kmajor);
 // The bf16 GEMM with producers at the front (fz->nprod > 0; chooses
 // fz->row.mb and sets fz->nprod, fz->nwg and fz->ncons).  fz->row.vmode

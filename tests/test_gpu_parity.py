@@ -92,6 +92,16 @@ def test_wide_tiles(orc, shape):
     _case(orc, T, K, N, r, 2.0 * r, seed=59, rows=rows)
 
 
+# 256 x 192 tiles fill the 256 CUs in one wave where the output is about
+# 4096 x 3072: T = 4000 and d_in = d_out = 3000 select them for the forward and
+# for dx, with ragged row and column tiles and both reduction axes not a
+# multiple of the stage depth.  Sampled rows of y and dx; dA and dB in full.
+def test_one_wave_tiles(orc):
+    T, K, N, r = 4000, 3000, 3000, 16
+    rows = list(range(0, T, 53)) + [T - 1]
+    _case(orc, T, K, N, r, 2.0 * r, seed=61, rows=rows)
+
+
 def test_split_forward_without_u_save(orc):
     # the partial sums of u stay in the workspace; y must not depend on u_save
     T, K, N, r = 256, 1800, 1032, 16
@@ -172,6 +182,21 @@ def test_frozen_dx_small(orc, shape, dtype):
     torch.cuda.synchronize()
     ref = orc.frozen_dx(inp["dy"], inp["W"])
     assert relerr(dx.cpu().to(torch.float64).numpy(), ref) <= TOL[dtype]
+
+
+# 256 x 192 tiles with k-major B (frozen dx carries no side items): ragged row
+# and column tiles, reduction axis not a multiple of the stage depth.
+def test_frozen_dx_one_wave_tiles(orc):
+    T, K, N = 4000, 3000, 1032
+    _announce(f"frozen T={T} K={K} N={N}")
+    inp = frozen_inputs(T, K, N, seed=5)
+    dy, W = inp["dy"].cuda(), inp["W"].cuda()
+    dx = torch.empty(T, K, dtype=torch.bfloat16, device="cuda")
+    lm.frozen_linear_bwd_dx(dy, W, dx)
+    torch.cuda.synchronize()
+    rows = list(range(0, T, 37)) + [T - 1]
+    ref = orc.frozen_dx(inp["dy"][rows], inp["W"])
+    assert relerr(dx[rows].cpu().to(torch.float64).numpy(), ref) <= TOL[torch.bfloat16]
 
 
 # --- full-size workloads (sampled rows of y and dx) --------------------------------
