@@ -25,8 +25,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 import paper_2606_19528_amd as lm  # noqa: E402
-from workloads import (WORKLOADS, frozen_inputs, head_inputs, linear_seed, lora_inputs,  # noqa: E402
-                       quant_weight)
+from workloads import (ORDER, WORKLOADS, frozen_inputs, head_inputs, linear_seed,  # noqa: E402
+                       lora_inputs, quant_weight)
 
 METRIC = "LoRA linear fwd+bwd TFLOP/s (% bf16 MFMA peak) + peak device workspace bytes"
 PEAK_BF16_TFLOPS = 2516.6   # 256 CU x 4096 dense bf16 flop/clk x 2.4 GHz
@@ -153,6 +153,42 @@ def time_steps(fn, steps, warmup):
     return e0.elapsed_time(e1) / steps
 
 
+def percentiles(v):
+    """median, p10, p90 of a list of step times (ms)."""
+    t = torch.tensor(sorted(v), dtype=torch.float64)
+    q = torch.quantile(t, torch.tensor([0.5, 0.1, 0.9], dtype=torch.float64))
+    return {"median_ms": round(float(q[0]), 5), "p10_ms": round(float(q[1]), 5),
+            "p90_ms": round(float(q[2]), 5)}
+
+
+def event_steps(fn, steps, flush=None):
+    """Run `steps` steps with an event between consecutive steps; with `flush`
+    (a device buffer) every step is preceded, outside its own event pair, by a
+    write of the whole buffer, which evicts the 256 MB last-level cache (the
+    cold-cache protocol).  Returns (total ms from first to last event, list of
+    per-step ms)."""
+    n = steps + 1 if flush is None else 2 * steps
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+    torch.cuda.synchronize()
+    if flush is None:
+        ev[0].record()
+        for i in range(steps):
+            fn()
+            ev[i + 1].record()
+    else:
+        for i in range(steps):
+            flush.fill_(i & 0xFF)
+            ev[2 * i].record()
+            fn()
+            ev[2 * i + 1].record()
+    torch.cuda.synchronize()
+    if flush is None:
+        per = [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]
+        return ev[0].elapsed_time(ev[steps]), per
+    per = [ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(steps)]
+    return sum(per), per
+
+
 def per_kernel_ms(fn, steps):
     lm.profiler_reset()
     lm.profiler_enable(True)
@@ -166,6 +202,65 @@ def per_kernel_ms(fn, steps):
         if n:
             out[name] = (tot, n)
     lm.profiler_reset()
+    return out
+
+
+def algorithmic(workload):
+    """Algorithmic work of one step per library kernel, from the plan of each
+    linear (which GEMM launches carry the rank-r producers, which products run
+    as separate row-skinny launches).  GEMM launches: flops (the dx launch also
+    does the dA / dB token reductions, 2Tr(K+N)).  Row-skinny launches: the
+    bytes they must move (inputs once, fp32 outputs once) and their flops.
+      forward   gemm_fwd     2TN(K+r) (+ 2TKr when u = x A^T runs inside it)
+                lora_down    2TK + 2rK + 4Tr bytes, 2TKr flops (otherwise)
+      backward  gemm_bwd_dx  2TK(N+r) + 2Tr(K+N) (+ 2TNr when du = s dy B runs inside it)
+                lora_dy_b    2TN + 2Nr + 4Tr bytes, 2TNr flops (otherwise)
+      head      gemm_frozen_dx  2TKN"""
+    T = workload.tokens
+    flops, nbytes = {}, {}
+
+    def add(d, k, v):
+        d[k] = d.get(k, 0.0) + v
+
+    for lin in workload.linears:
+        K, N, r = lin.d_in, lin.d_out, lin.rank
+        p = lm.lora_linear_plan(T, K, N, r)
+        L = workload.layers
+        add(flops, "gemm_fwd", L * (2.0 * T * N * (K + r) + (2.0 * T * K * r if p["fwd_fused"] else 0.0)))
+        if not p["fwd_fused"]:
+            add(flops, "lora_down", L * 2.0 * T * K * r)
+            add(nbytes, "lora_down", L * (2.0 * T * K + 2.0 * r * K + 4.0 * T * r))
+        add(flops, "gemm_bwd_dx", L * (2.0 * T * K * (N + r) + 2.0 * T * r * (K + N)
+                                       + (2.0 * T * N * r if p["bwd_fused"] else 0.0)))
+        if not p["bwd_fused"]:
+            add(flops, "lora_dy_b", L * 2.0 * T * N * r)
+            add(nbytes, "lora_dy_b", L * (2.0 * T * N + 2.0 * N * r + 4.0 * T * r))
+    if workload.head is not None:
+        add(flops, "gemm_frozen_dx", 2.0 * T * workload.head.d_in * workload.head.d_out)
+    return flops, nbytes
+
+
+def kernel_table(workload, per_kernel, steps):
+    """Per library kernel: time per step, launches, average launch, and the
+    roofline position (TFLOP/s against the dense bf16 peak for the GEMMs, GB/s
+    of algorithmic bytes against HBM for the row-skinny kernels)."""
+    flops, nbytes = algorithmic(workload)
+    out = {}
+    for name, (tot, n) in per_kernel.items():
+        ms = tot / steps
+        e = {"ms_per_step": round(ms, 5), "launches_per_step": round(n / steps, 3),
+             "avg_launch_us": round(tot / n * 1e3, 3)}
+        if name in nbytes:
+            gbs = nbytes[name] / (ms * 1e-3) / 1e9
+            e.update({"bound": "hbm", "achieved": round(gbs, 1), "unit": "GB/s",
+                      "frac": round(gbs / PEAK_HBM_GBS, 4),
+                      "bytes_per_launch": round(nbytes[name] / (n / steps))})
+        elif name in flops:
+            tf = flops[name] / (ms * 1e-3) / 1e12
+            e.update({"bound": "mfma", "achieved": round(tf, 2), "unit": "TFLOP/s",
+                      "frac": round(tf / PEAK_BF16_TFLOPS, 4),
+                      "flops_per_launch": round(flops[name] / (n / steps))})
+        out[name] = e
     return out
 
 
@@ -279,71 +374,141 @@ def bench_topk(dev, V=128256, D=3072, k=1000):
             "table_bytes": V * k * 4}
 
 
-def kernel_flops(workload, fused_fwd=False, fused_bwd=False):
-    """Algorithmic flops of one launch of each GEMM kernel, per linear shape.
-    With `fused_fwd` the forward launch also computes u = x A^T (its producer
-    workgroups), 2TKr more; with `fused_bwd` the dx launch also computes
-    du = s dy B, 2TNr more.  (The dA / dB side items that share the dx launch
-    are not counted in either case.)"""
-    T = workload.tokens
-    per = {}
-    for lin in workload.linears:
-        K, N, r = lin.d_in, lin.d_out, lin.rank
-        per.setdefault("gemm_fwd", []).append(2.0 * T * N * (K + r) + (2.0 * T * K * r if fused_fwd else 0.0))
-        per.setdefault("gemm_bwd_dx", []).append(2.0 * T * K * (N + r) + (2.0 * T * N * r if fused_bwd else 0.0))
-    if workload.head is not None:
-        per["gemm_frozen_dx"] = [2.0 * T * workload.head.d_in * workload.head.d_out]
-    return per
+def cpu_info():
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        aff = len(os.sched_getaffinity(0))
+    except AttributeError:
+        aff = os.cpu_count()
+    return model, os.cpu_count(), aff
 
 
-def cpu_baseline(workload, layers, target_s=12.0):
-    """The fp64 oracle (as it stands) timed on the host on a bounded sample:
-    the full fwd+bwd of the workload's first linear over its first Ts tokens,
-    Ts chosen so one pass takes about `target_s` seconds; when all tokens take
-    less than that, the full pass is repeated until the sample does."""
+def cpu_baseline(workload, layers, head, target_s=10.0):
+    """The fp64 oracle (as it stands) timed on the host on a bounded sample of
+    the same workload: the full fwd + bwd of the first decoder layer's linears
+    over their first Ts tokens (Ts chosen so the sample takes about
+    `target_s`), plus the frozen head's dx on 64 sampled rows when the
+    workload has one.  Every oracle function is linear in the token count, so
+    the whole step is extrapolated as layers x (T / Ts) x the layer sample plus
+    (T / 64) x the head sample, and labelled as such.  A 1-thread time of the
+    first linear over a shorter token sample is reported beside it."""
     import oracle
+    from workloads import sample_rows
 
     orc = oracle.load()
-    L = layers[0]
-    K, N, r, s = L.lin.d_in, L.lin.d_out, L.lin.rank, L.lin.scale
-    cpu = {k: getattr(L, k).cpu() for k in ("x", "W", "A", "B", "dy")}
+    threads = orc.threads()
+    T = workload.tokens
+    first = layers[:len(workload.linears)]
+    cpu = [{k: getattr(L, k).cpu() for k in ("x", "W", "A", "B", "dy")} for L in first]
 
-    def run(Ts, reps=1):
-        inp = {k: (v[:Ts] if k in ("x", "dy") else v) for k, v in cpu.items()}
+    def run_linear(i, Ts):
+        L, c = first[i], cpu[i]
+        s = L.lin.scale
+        x, dy = c["x"][:Ts], c["dy"][:Ts]
+        U = orc.u(x, c["A"])
+        orc.y(x, c["W"], U, c["B"], s)
+        _, dU = orc.grad_u(dy, c["B"], s)
+        orc.dx(dy, c["W"], dU, c["A"])
+        orc.da(dU, x)
+        orc.db(dy, U, s)
+
+    def run_layer(Ts):
         t0 = time.perf_counter()
-        for _ in range(reps):
-            U = orc.u(inp["x"], inp["A"])
-            orc.y(inp["x"], inp["W"], U, inp["B"], s)
-            _, dU = orc.grad_u(inp["dy"], inp["B"], s)
-            orc.dx(inp["dy"], inp["W"], dU, inp["A"])
-            orc.da(dU, inp["x"])
-            orc.db(inp["dy"], U, s)
+        for i in range(len(first)):
+            run_linear(i, Ts)
         return time.perf_counter() - t0
 
-    def flops(Ts):
-        return 4.0 * Ts * K * N + 6.0 * Ts * r * (K + N)
+    def layer_flops(Ts):
+        return sum(4.0 * Ts * L.lin.d_in * L.lin.d_out + 6.0 * Ts * L.lin.rank * (L.lin.d_in + L.lin.d_out)
+                   for L in first)
 
-    Ts = 8
-    t = run(Ts)
-    Ts = int(max(8, min(L.T, Ts * target_s / max(t, 1e-3))))
-    t = run(Ts)
-    reps = 1
-    if Ts == L.T and t < target_s / 2:
-        reps = int(target_s / max(t, 1e-3))
-        t = run(Ts, reps)
-    return {"value": flops(Ts) * reps / t / 1e12, "unit": "TFLOP/s", "cores": orc.threads(),
-            "kind": "oracle",
-            "sample": f"full fwd+bwd of {L.lin.name} ({K}->{N}, r={r}) over the first {Ts} of "
-                      f"{L.T} tokens, {reps} pass(es), {t:.1f} s, fp64 C loops (OpenMP)"}
+    head_s, head_flops = 0.0, 0.0
+    if head is not None:
+        rows = sample_rows(T, 64)
+        dyh, Wh = head[0].cpu()[rows], head[1].cpu()
+        t0 = time.perf_counter()
+        orc.frozen_dx(dyh, Wh)
+        head_s = time.perf_counter() - t0
+        head_flops = 2.0 * len(rows) * Wh.shape[0] * Wh.shape[1]
+    Ts = min(T, 16)
+    t = run_layer(Ts)
+    budget = max(1.0, target_s - head_s)
+    Ts = int(max(16, min(T, Ts * budget / max(t, 1e-3))))
+    t = run_layer(Ts)
+    value = (layer_flops(Ts) + head_flops) / (t + head_s) / 1e12
+    step_s = workload.layers * t * T / Ts + (head_s * T / len(rows) if head is not None else 0.0)
+    # 1 thread, first linear, shorter token sample
+    orc.set_threads(1)
+    try:
+        L0 = first[0].lin
+        # about 2 s at one thread: the layer sample's rate divided by the threads
+        f0 = 4.0 * L0.d_in * L0.d_out + 6.0 * L0.rank * (L0.d_in + L0.d_out)
+        T1 = max(8, min(T, int(2.0 * layer_flops(Ts) / max(t, 1e-3) / threads / f0)))
+        t0 = time.perf_counter()
+        run_linear(0, T1)
+        t1 = time.perf_counter() - t0
+    finally:
+        orc.set_threads(threads)
+    f1 = 4.0 * T1 * L0.d_in * L0.d_out + 6.0 * T1 * L0.rank * (L0.d_in + L0.d_out)
+    model, ncpu, aff = cpu_info()
+    what = (f"full fwd+bwd of the first layer's {len(first)} linear(s) over their first {Ts} of {T} tokens "
+            f"({t:.1f} s)")
+    if head is not None:
+        what += f", plus the frozen head dx on 64 sampled rows ({head_s:.1f} s)"
+    return {"value": value, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": what + "; fp64 C loops (OpenMP)",
+            "cpu_model": model, "nproc": ncpu, "affinity_cpus": aff,
+            "extrapolated_step_s": round(step_s, 1),
+            "extrapolated_note": f"extrapolated: {workload.layers} layer(s) x T/{Ts} x the layer sample"
+                                 + (" + T/64 x the head sample" if head is not None else "")
+                                 + " (every oracle sum is linear in the token count)",
+            "one_thread": {"value": f1 / t1 / 1e12, "unit": "TFLOP/s",
+                           "sample": f"{L0.name} ({L0.d_in}->{L0.d_out}, r={L0.rank}) over {T1} tokens, "
+                                     f"{t1:.1f} s"}}
+
+
+def bench_workload(w, dev, steps, warmup, flush):
+    """Warm and cold per-step times of one workload (the breakdown beside the
+    headline): median / p10 / p90 and TFLOP/s on the median."""
+    layers, head, ws, ws_bytes = build(w, dev)
+    fn = lambda: step(layers, head, ws)  # noqa: E731
+    for _ in range(warmup):
+        fn()
+    _, warm = event_steps(fn, steps)
+    _, cold = event_steps(fn, steps, flush=flush)
+    flops = w.flops_per_step()
+    wm, cm = percentiles(warm), percentiles(cold)
+    out = {"warm": wm, "cold": cm,
+           "tflops_warm_median": round(flops / (wm["median_ms"] * 1e-3) / 1e12, 2),
+           "tflops_cold_median": round(flops / (cm["median_ms"] * 1e-3) / 1e12, 2),
+           "frac_bf16_peak_warm": round(flops / (wm["median_ms"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+           "steps": steps, "workspace_bytes": int(ws_bytes)}
+    pk = per_kernel_ms(fn, steps)
+    out["kernels"] = kernel_table(w, pk, steps)
+    del layers, head, ws
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return out
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="llama_q_proj", choices=sorted(WORKLOADS))
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llama_stack", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the per-workload breakdown of the smaller workloads")
+    ap.add_argument("--no-cold", action="store_true", help="skip the cold-cache pass")
     ap.add_argument("--no-topk", action="store_true",
                     help="skip the secondary measurement of the top-k similarity table build")
     ap.add_argument("--no-ckpt", action="store_true",
@@ -369,53 +534,42 @@ def main():
     torch.cuda.synchronize()
     base_mem = torch.cuda.memory_allocated()
     torch.cuda.reset_peak_memory_stats()
+    fn = lambda: step(layers, head, ws)  # noqa: E731
 
     for _ in range(args.warmup):
-        step(layers, head, ws)
+        fn()
     torch.cuda.synchronize()
     log(f"[bench] warmup {args.warmup} done")
 
-    # Timed region: plain steps.
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    e0.record()
-    for _ in range(args.steps):
-        step(layers, head, ws)
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / args.steps
+    # Timed region: exactly K steps between two synchronisations, an event
+    # between consecutive steps (per-step spread).
+    total_ms, per = event_steps(fn, args.steps)
+    ms = total_ms / args.steps
     log(f"[bench] {args.steps} steps: {ms:.4f} ms/step")
     extra_peak = torch.cuda.max_memory_allocated() - base_mem
+    total_peak = torch.cuda.max_memory_allocated()
+    if lm.handover_giveups():
+        raise RuntimeError("a fused hand-over wait gave up during the timed steps")
+
+    timing = {"warm": percentiles(per)}
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    if not args.no_cold:
+        _, cold = event_steps(fn, args.steps, flush=flush)
+        timing["cold"] = percentiles(cold)
+        log(f"[bench] cold-cache median {timing['cold']['median_ms']:.4f} ms/step")
 
     # Same steps again with the library's HIP-event hook around every kernel.
-    lm.profiler_reset()
-    lm.profiler_enable(True)
-    for _ in range(args.steps):
-        step(layers, head, ws)
-    torch.cuda.synchronize()
-    lm.profiler_enable(False)
-    per_kernel = {}
-    for name in lm.kernel_names():
-        tot, n = lm.profiler_read(name)
-        if n:
-            per_kernel[name] = (tot, n)
-    lm.profiler_reset()
-    dom = max(per_kernel, key=lambda k: per_kernel[k][0])
-    # the forward's rank-r pass runs inside its GEMM launch when no
-    # separate lora_down launch was recorded
-    kf = kernel_flops(w, fused_fwd="lora_down" not in per_kernel, fused_bwd="lora_dy_b" not in per_kernel)
-    launch_flops = sum(kf[dom]) / len(kf[dom]) if dom in kf else None
-    tot, n = per_kernel[dom]
-    avg_ms = tot / n
-    roofline = None
-    if launch_flops is not None:
-        achieved = launch_flops / (avg_ms * 1e-3) / 1e12
-        traffic = stored_traffic(w.key).get(dom)
-        roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
-                    "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                    "traffic": traffic, "kernel": dom, "avg_launch_us": round(avg_ms * 1e3, 3)}
-    log("[bench] per-kernel (ms total, launches): " +
-        ", ".join(f"{k}={v[0]:.3f}/{v[1]}" for k, v in per_kernel.items()))
+    per_kernel = per_kernel_ms(fn, args.steps)
+    kernels = kernel_table(w, per_kernel, args.steps)
+    gemms = {k: v for k, v in kernels.items() if v.get("bound") == "mfma"}
+    dom = max(gemms, key=lambda k: gemms[k]["ms_per_step"])
+    kd = kernels[dom]
+    traffic = stored_traffic(w.key).get(dom)
+    roofline = {"bound": "mfma", "achieved": kd["achieved"], "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": kd["frac"], "traffic": traffic, "kernel": dom,
+                "avg_launch_us": kd["avg_launch_us"], "flops_per_launch": kd["flops_per_launch"]}
+    log("[bench] per-kernel: " + ", ".join(f"{k}={v['ms_per_step']:.3f} ms ({v.get('frac')})"
+                                           for k, v in kernels.items()))
 
     flops = w.flops_per_step()
     value = flops / (ms * 1e-3) / 1e12
@@ -430,11 +584,16 @@ def main():
                    "head": None if w.head is None else [w.head.d_in, w.head.d_out],
                    "parallelism": "single GPU"},
         "frac_bf16_peak": round(value / PEAK_BF16_TFLOPS, 4),
+        "timing": timing,
+        "timing_note": "value and ms_per_step: K back-to-back steps (warm: a step's inputs may sit "
+                       "in the 256 MB last-level cache from the step before); cold: each step after "
+                       "a 512 MiB write that evicts that cache",
         "peak_workspace_bytes": int(ws_bytes),
         "peak_extra_device_bytes_during_steps": int(extra_peak),
+        "total_device_bytes_peak": int(total_peak),
         "frozen_weight_bytes": int(w.frozen_weight_bytes()),
         "roofline": roofline,
-        "kernels_ms_per_step": {k: round(v[0] / args.steps, 5) for k, v in per_kernel.items()},
+        "kernels": kernels,
     }
     if not args.no_quant:
         # Quantized frozen base (INT4 linears, INT8 head) dequantized inside the
@@ -453,6 +612,24 @@ def main():
             "unit": "TFLOP/s", "frozen_weight_bytes": int(wbytes),
             "kernels_ms_per_step": {k: round(v[0] / args.steps, 5) for k, v in pk.items()}}
         log(f"[bench] quantized base: {msq:.4f} ms/step")
+        del qs, qh
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("[bench] cpu baseline (oracle) ...")
+        cpu = cpu_baseline(w, layers, head)
+    del layers, head, ws
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    if not args.no_configs:
+        cfgs = {}
+        for key in ORDER:
+            if key == w.key:
+                continue
+            n = {"single_256": 200, "llama_q_proj": 200}.get(key, 50)
+            cfgs[key] = bench_workload(WORKLOADS[key], dev, n, 5, flush)
+            log(f"[bench] {key}: {cfgs[key]['warm']['median_ms']:.4f} ms/step warm, "
+                f"{cfgs[key]['cold']['median_ms']:.4f} cold")
+        out["configs"] = cfgs
     if not args.no_topk:
         out["topk_table"] = bench_topk(dev)
         log(f"[bench] top-k table: {out['topk_table']}")
@@ -470,9 +647,10 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         out["calib_copy_bytes"] = n * 4
-    if not args.no_cpu_baseline:
-        log("[bench] cpu baseline (oracle) ...")
-        out["cpu_baseline"] = cpu_baseline(w, layers)
+    if lm.handover_giveups():
+        raise RuntimeError("a fused hand-over wait gave up during the benchmark")
+    if cpu is not None:
+        out["cpu_baseline"] = cpu
     print(json.dumps(out), flush=True)
 
 

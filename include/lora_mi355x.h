@@ -26,9 +26,10 @@
  * the fp32 accumulator.
  *
  * Ownership: every pointer is a device pointer owned by the caller.  The
- * library never allocates device memory and keeps no pointer after a call
- * returns.  Scratch space comes from the caller's workspace `ws` of
- * `ws_bytes` bytes (size it with lora_linear_workspace_bytes); its contents
+ * library never allocates device memory (apart from the counter noted
+ * below) and keeps no pointer after a call returns.  Scratch space comes
+ * from the caller's workspace `ws` of `ws_bytes` bytes (size it with
+ * lora_linear_workspace_bytes); its contents
  * on entry are ignored and on return are unspecified.
  *
  * Streams: all work is enqueued on `hip_stream` (a hipStream_t; NULL = the
@@ -50,9 +51,16 @@
  * lora_last_error() returns a short text for the calling thread's last error.
  * No entry point prints, aborts or throws.
  *
- * Determinism: no atomics on any path; every reduction (over tokens, over the
- * split feature axis of the rank-r products, across waves) adds its parts in
- * a fixed order, so identical inputs give bitwise identical outputs.
+ * Determinism: every reduction (over tokens, over the split feature axis of
+ * the rank-r products, across waves) adds its parts in a fixed order, so
+ * identical inputs give bitwise identical outputs.  Atomics appear only where
+ * they cannot change a result: the counters of the fused hand-over (they
+ * order work; see lora_handover_giveups), and, in the top-k table build, the
+ * reservation of candidate-list slots, whose order is normalised by the
+ * selection (ties go to the smaller index).
+ *
+ * Device memory held by the library itself: one 4-byte counter per device
+ * (lora_handover_giveups); everything else is the caller's.
  */
 #ifndef LORA_MI355X_H
 #define LORA_MI355X_H
@@ -253,6 +261,37 @@ lora_status_t lora_ckpt_forward(const lora_node_t *nodes, int n, int64_t T, cons
 lora_status_t lora_ckpt_backward(const lora_node_t *nodes, int n, int64_t T, const void *g_n,
                                  void *dx0, const void *host_stash, size_t host_bytes, void *ws,
                                  size_t ws_bytes, void *compute_stream, void *copy_stream);
+
+/* ---- Plan and hand-over diagnostics -----------------------------------------
+ * Which kernel configuration lora_linear_fwd / lora_linear_bwd run for these
+ * sizes (host logic only, no GPU work): the output tile of the forward GEMM
+ * (y, T x d_out) and of the dx GEMM (T x d_in); whether the rank-r pass runs
+ * as producer workgroups inside that GEMM launch ("fused"); and otherwise
+ * over how many partial sums of its reduction axis u = x A^T and
+ * du = s dy B are computed.  Errors as for the entry points' size checks. */
+typedef struct {
+  int fwd_tile_m, fwd_tile_n, fwd_fused, fwd_u_parts;
+  int bwd_tile_m, bwd_tile_n, bwd_fused, bwd_du_parts;
+} lora_plan_t;
+lora_status_t lora_linear_plan(int64_t T, int64_t d_in, int64_t d_out, int64_t r, lora_dtype_t dt,
+                               lora_plan_t *plan);
+
+/* A fused launch hands the rank-r rows from its producer workgroups to its
+ * tiles through counters in the workspace; a wait for them gives up after a
+ * bounded time (0.2 s) instead of hanging, and a launch whose wait gave up
+ * may have used incomplete rows.  Every wave whose wait gave up adds one to
+ * a counter of the current device; this call synchronises the device,
+ * stores the count in *count and, if `reset`, sets it back to 0.  A caller
+ * that needs certainty checks that the count stays 0.  Errors: LORA_EINVAL
+ * (NULL), LORA_EHIP. */
+lora_status_t lora_handover_giveups(uint64_t *count, int reset);
+
+/* Test hook: with hold = 1, every tile's hand-over wait in the fused
+ * launches enqueued afterwards (from any thread) gives up after its 0.2 s
+ * budget instead of seeing the producers' count, so those launches' results
+ * are invalid and lora_handover_giveups counts them; hold = 0 (the default)
+ * restores normal operation.  Errors: LORA_EINVAL for other values. */
+lora_status_t lora_debug_set_handover(int hold);
 
 /* Static text for a status code. */
 const char *lora_status_str(lora_status_t status);

@@ -70,6 +70,8 @@ def _declare(lib: ctypes.CDLL) -> ctypes.CDLL:
         getattr(lib, name).restype = None
     lib.oracle_threads.argtypes = []
     lib.oracle_threads.restype = ctypes.c_int
+    lib.oracle_set_threads.argtypes = [ctypes.c_int]
+    lib.oracle_set_threads.restype = None
     return lib
 
 
@@ -111,6 +113,10 @@ class Oracle:
 
     def threads(self) -> int:
         return int(self.lib.oracle_threads())
+
+    def set_threads(self, n: int) -> None:
+        """OpenMP threads of the following calls (timing only)."""
+        self.lib.oracle_set_threads(int(n))
 
     # --- one definition per call -------------------------------------------------
     def u(self, X, A):

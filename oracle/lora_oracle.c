@@ -275,6 +275,10 @@ void oracle_topk_table(const double *W, int64_t V, int64_t D, int64_t k, const i
 #ifdef _OPENMP
 #include <omp.h>
 int oracle_threads(void) { return omp_get_max_threads(); }
+/* Thread count of the following parallel loops (timing only; the results do
+ * not depend on it). */
+void oracle_set_threads(int n) { omp_set_num_threads(n > 0 ? n : 1); }
 #else
 int oracle_threads(void) { return 1; }
+void oracle_set_threads(int n) { (void)n; }
 #endif

@@ -8,4 +8,4 @@ from .lora import (LORA_BF16, LORA_F32, LORA_OP_BWD, LORA_OP_FROZEN_DX, LORA_OP_
                    lora_ckpt_backward, lora_ckpt_forward, lora_ckpt_sizes,
                    lora_linear_workspace_bytes, lm_head_build_vocab, lm_head_reduced_ce,
                    lm_head_workspace_bytes, profiler_enable, profiler_read, profiler_reset,
-                   topk_table_build)
+                   topk_table_build, lora_linear_plan, handover_giveups, debug_set_handover)

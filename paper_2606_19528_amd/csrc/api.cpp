@@ -149,6 +149,10 @@ unsigned int next_gen() {
   } while (v == 0);
   return v;
 }
+// Test hook (lora_debug_set_handover): 1 makes every tile's hand-over wait
+// of the following fused launches give up.
+std::atomic<int> g_fz_hold{0};
+void handover_params(FuseArgs &fz) { fz.hold = g_fz_hold.load(); }
 // One segment over the whole reduction axis L, 16 rows per workgroup.
 RowSplit whole_rows(int64_t L, Dtype d) {
   const int64_t ce = d == DT_BF16 ? 64 : 32;
@@ -416,6 +420,7 @@ lora_status_t fwd_impl(const void *x, const void *W, const void *qc, const float
     fz.nprod = (int)((T + 15) / 16);
     fz.sync = (unsigned long long *)(wsb + L.sync);
     fz.gen = next_gen();
+    handover_params(fz);
     g.A2 = wsb + L.utail; g.lda2 = L.ldt;
     g.B2 = B; g.ldb2 = r;  // rows of r bf16: whole 16-byte vectors
     g.r = (int)r;
@@ -553,10 +558,11 @@ lora_status_t bwd_impl(const void *x, const void *W, const void *qc, const float
     fz.nprod = (int)((T + 15) / 16);
     fz.sync = (unsigned long long *)(wsb + L.sync);
     fz.gen = next_gen();
+    handover_params(fz);
     SideArgs sd{};
-    sd.T = (int)T; sd.r = (int)r; sd.njobs = 2;
-    sd.job[0] = ColJob{x, d_in, (int)d_in, du, dA, 1, 1.0f, 1, T * r};
-    sd.job[1] = ColJob{dy, d_out, (int)d_out, u, dB, 0, scale, u_parts, T * r};
+    sd.T = (int)T; sd.r = (int)r; sd.njobs = 2; sd.scale1 = scale; sd.vstride = T * r;
+    sd.job[0] = ColJob{x, du, dA, (int)d_in, 1};
+    sd.job[1] = ColJob{dy, u, dB, (int)d_out, u_parts};
     g.A2 = wsb + L.dutail; g.lda2 = L.ldt;
     g.B2 = A; g.ldb2 = d_in;
     g.r = (int)r;
@@ -583,9 +589,9 @@ lora_status_t bwd_impl(const void *x, const void *W, const void *qc, const float
     if (e != hipSuccess) return hip_fail(e, "lora_dy_b launch");
   }
   SideArgs sd{};
-  sd.T = (int)T; sd.r = (int)r; sd.njobs = 2;
-  sd.job[0] = ColJob{x, d_in, (int)d_in, du, dA, 1, 1.0f, ns, T * r};
-  sd.job[1] = ColJob{dy, d_out, (int)d_out, u, dB, 0, scale, u_parts, T * r};
+  sd.T = (int)T; sd.r = (int)r; sd.njobs = 2; sd.scale1 = scale; sd.vstride = T * r;
+  sd.job[0] = ColJob{x, du, dA, (int)d_in, ns};
+  sd.job[1] = ColJob{dy, u, dB, (int)d_out, u_parts};
   g.A2 = wsb + L.dutail; g.lda2 = L.ldt;
   g.B2 = ns > 1 ? (const void *)(wsb + L.acat) : A; g.ldb2 = d_in;
   g.r = (int)(ns * r);
@@ -909,6 +915,42 @@ lora_status_t topk_table_build(const void *W, int64_t V, int64_t D, int64_t k, i
       if (e != hipSuccess) return hip_fail(e, "topk_select launch");
     }
   }
+  return LORA_OK;
+}
+
+lora_status_t lora_linear_plan(int64_t T, int64_t d_in, int64_t d_out, int64_t r, lora_dtype_t dt,
+                               lora_plan_t *plan) {
+  if (!plan) return fail(LORA_EINVAL, "plan is NULL");
+  lora_status_t s = check_shapes(T, d_in, d_out, r, dt);
+  if (s != LORA_OK) return s;
+  const Dtype d = dt == LORA_BF16 ? DT_BF16 : DT_F32;
+  lora_plan_t p{};
+  gemm_tile_shape((int)T, (int)d_out, false, false, d, &p.fwd_tile_m, &p.fwd_tile_n);
+  gemm_tile_shape((int)T, (int)d_in, true, r > 0, d, &p.bwd_tile_m, &p.bwd_tile_n);
+  if (r > 0) {
+    const FwdLayout F = fwd_layout(T, d_in, d_out, r, dt);
+    const BwdLayout B = bwd_layout(T, d_in, d_out, r, dt);
+    p.fwd_fused = F.fused;
+    p.fwd_u_parts = F.sp.nsplit;
+    p.bwd_fused = B.fused;
+    p.bwd_du_parts = B.sp_du.nsplit;
+  }
+  *plan = p;
+  return LORA_OK;
+}
+
+lora_status_t lora_handover_giveups(uint64_t *count, int reset) {
+  if (!count) return fail(LORA_EINVAL, "count is NULL");
+  unsigned c = 0;
+  hipError_t e = handover_giveups(&c, reset != 0);
+  if (e != hipSuccess) return hip_fail(e, "reading the hand-over give-up count");
+  *count = c;
+  return LORA_OK;
+}
+
+lora_status_t lora_debug_set_handover(int hold) {
+  if (hold != 0 && hold != 1) return fail(LORA_EINVAL, "hold must be 0 or 1");
+  g_fz_hold.store(hold);
   return LORA_OK;
 }
 

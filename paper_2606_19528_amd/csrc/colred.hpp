@@ -51,17 +51,10 @@ constexpr int side_lds_bytes() {
   return (NW / 2) * SideShape<E>::COLS * (SIDE_JB * 16 + 1) * 4;
 }
 
-template <class E>
-__device__ __forceinline__ int side_items_of(const ColJob &job, const SideArgs &s) {
-  const int ncb = (job.L + SideShape<E>::COLS - 1) / SideShape<E>::COLS;
-  return ncb * ((s.r + 31) / 32);
-}
-
+// Work items: job 0's, then job 1's (counted on the host: side_count).
 template <class E>
 __device__ __forceinline__ int side_items_total(const SideArgs &s) {
-  int n = 0;
-  for (int i = 0; i < s.njobs; ++i) n += side_items_of<E>(s.job[i], s);
-  return n;
+  return s.ntot;
 }
 
 template <class E, int NW>
@@ -74,14 +67,19 @@ __device__ void side_item(const SideArgs &s, int item, char *smem) {
   constexpr int RS = JB * 16 + 1;  // padded LDS row (floats)
 
   int ji = 0;
-  {
-    const int n0 = side_items_of<E>(s.job[0], s);
-    if (item >= n0) {
-      ji = 1;
-      item -= n0;
-    }
+  if (item >= s.n0) {
+    ji = 1;
+    item -= s.n0;
   }
-  const ColJob &job = s.job[ji];
+  // The job's fields, each chosen by a select between the two constant
+  // indices (indexing the argument array with the run-time ji made the
+  // compiler copy the arguments to scratch memory).
+  const void *jX = ji ? s.job[1].X : s.job[0].X;
+  const float *jV = ji ? s.job[1].V : s.job[0].V;
+  float *jout = ji ? s.job[1].out : s.job[0].out;
+  const int jL = ji ? s.job[1].L : s.job[0].L;
+  const int jvparts = ji ? s.job[1].vparts : s.job[0].vparts;
+  const float jscale = ji ? s.scale1 : 1.0f;
   const int r = s.r;
   const int ngz = (r + 31) / 32;
   const int z = item % ngz;
@@ -93,7 +91,7 @@ __device__ void side_item(const SideArgs &s, int item, char *smem) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, cl = lane & 15;
   const int col = c0 + cl * VEC;
-  const T *Xp = (const T *)job.X;
+  const T *Xp = (const T *)jX;
 
   constexpr int VW = 8, PER = VW / NW;  // virtual waves, per real wave
   static_assert(NW * PER == VW, "four or eight waves");
@@ -118,16 +116,16 @@ __device__ void side_item(const SideArgs &s, int item, char *smem) {
   auto load = [&](int tb, Step &st) {
     const int rows = min(ROWS, t_end - tb);  // <= 0 past the end: nothing is read
     const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
-        (void *)(Xp + (int64_t)tb * job.ldx), (short)0, rows > 0 ? rows * job.ldx * ES : 0, 0x00020000);
+        (void *)(Xp + (int64_t)tb * jL), (short)0, rows > 0 ? rows * jL * ES : 0, 0x00020000);
 #pragma unroll
     for (int i = 0; i < VEC; ++i)
       st.x[i] = __builtin_bit_cast(
           u32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                     rx, col < job.L ? (uint32_t)(((g * VEC + i) * job.ldx + col) * ES) : OOB, 0, 0));
+                     rx, col < jL ? (uint32_t)(((g * VEC + i) * jL + col) * ES) : OOB, 0, 0));
     // V and its further partial sums, added in ascending order (uniform loop)
-    for (int q = 0; q < job.vparts; ++q) {
+    for (int q = 0; q < jvparts; ++q) {
       const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
-          (void *)(job.V + (int64_t)q * job.vstride + (int64_t)tb * r), (short)0, rows > 0 ? rows * r * 4 : 0,
+          (void *)(jV + (int64_t)q * s.vstride + (int64_t)tb * r), (short)0, rows > 0 ? rows * r * 4 : 0,
           0x00020000);
 #pragma unroll
       for (int jb = 0; jb < JB; ++jb) {
@@ -213,12 +211,12 @@ __device__ void side_item(const SideArgs &s, int item, char *smem) {
         for (int i = 0; i < 4; ++i) {
           const int l = c0 + (4 * g + i) * VEC + q;
           const int j = jb * 16 + cl;
-          if (l < job.L && j < jn) {
-            const float v = job.scale * acc[0][q][jb][i];
-            if (job.transpose_out)
-              job.out[(int64_t)(jg + j) * job.L + l] = v;
+          if (l < jL && j < jn) {
+            const float v = jscale * acc[0][q][jb][i];
+            if (ji == 0)
+              jout[(int64_t)(jg + j) * jL + l] = v;
             else
-              job.out[(int64_t)l * r + jg + j] = v;
+              jout[(int64_t)l * r + jg + j] = v;
           }
         }
   }

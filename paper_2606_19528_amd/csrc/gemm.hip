@@ -51,55 +51,100 @@ typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 // ---- hand-over of a fused rank-r pass (protocol in launch.hpp, FuseArgs) ------
 constexpr unsigned long long FZ_BUDGET = 20000000ull;  // 0.2 s of the 100 MHz real-time counter
 
+// Waits that gave up (their condition not met within FZ_BUDGET), summed over
+// every launch on this device; read and cleared from the host
+// (handover_giveups).  A give-up means the launch may have computed with
+// incomplete producer rows.
+__device__ unsigned int g_fz_giveups;
+
+// A wait that gives up marks its wave by raising the wave's scheduling
+// priority (s_setprio), a flag that costs no register while the tile's
+// main loop still runs; fz_report counts marked waves once their work is
+// done.  (Every other form of recording at the point of the give-up --
+// a store, an atomic, an extra live value -- made the fused kernels spill.)
+constexpr int FZ_MARK = 3;
+__device__ __forceinline__ void fz_mark() { __builtin_amdgcn_s_setprio(FZ_MARK); }
+// The wave's user priority: bits 4:3 of the STATUS hardware register.
+__device__ __forceinline__ int fz_prio() {
+  return __builtin_amdgcn_s_getreg((1 << 11) | (3 << 6) | 2);  // size 2, offset 3, STATUS
+}
+// After a wave's last use of producer data: count it if a wait of it gave up,
+// and drop the mark.
+__device__ __forceinline__ void fz_report() {
+  if (fz_prio() == FZ_MARK) {
+    if ((threadIdx.x & 63) == 0)
+      __hip_atomic_fetch_add(&g_fz_giveups, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __builtin_amdgcn_s_setprio(0);
+  }
+}
+
 __device__ __forceinline__ unsigned long long fz_load(unsigned long long *p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 // Workgroup 0, one thread, before its work: tag the launch, then open it.
-__device__ __forceinline__ void fz_arm(const FuseArgs &fz) {
-  __hip_atomic_store(fz.sync, (unsigned long long)fz.gen << 32, __ATOMIC_RELAXED,
-                     __HIP_MEMORY_SCOPE_AGENT);
-  __hip_atomic_store(fz.sync + 1, 0ull, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+__device__ __forceinline__ void fz_arm(unsigned long long *sync, unsigned gen) {
+  __hip_atomic_store(sync, (unsigned long long)gen << 32, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(sync + 1, 0ull, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
 }
-// A producer, one thread, after every wave has released its stores: count
+// A producer, one thread, after every wave's stores have completed: count
 // this producer once the launch is open.
-__device__ __forceinline__ void fz_produced(const FuseArgs &fz) {
+__device__ __forceinline__ void fz_produced(unsigned long long *sync, unsigned gen) {
   const unsigned long long t0 = __builtin_amdgcn_s_memrealtime();
   for (;;) {
-    if (fz_load(fz.sync + 1) == 0 && (fz_load(fz.sync) >> 32) == fz.gen) break;
-    if (__builtin_amdgcn_s_memrealtime() - t0 > FZ_BUDGET) break;
+    if (fz_load(sync + 1) == 0 && (fz_load(sync) >> 32) == gen) break;
+    if (__builtin_amdgcn_s_memrealtime() - t0 > FZ_BUDGET) {
+      fz_mark();
+      break;
+    }
     __builtin_amdgcn_s_sleep(4);
   }
-  __hip_atomic_fetch_add(fz.sync, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_fetch_add(sync, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 // A consumer wave, before it reads producer data: wait until every producer
-// of this launch has counted itself.
-__device__ __forceinline__ void fz_wait(const FuseArgs &fz) {
+// of this launch has counted itself (ncons 0: never -- a test's way of
+// forcing every wait to give up).
+__device__ __forceinline__ void fz_wait(unsigned long long *sync, unsigned gen, int nprod, int ncons) {
   const unsigned long long t0 = __builtin_amdgcn_s_memrealtime();
   for (;;) {
-    if (fz_load(fz.sync + 1) < (unsigned long long)fz.ncons) {
-      const unsigned long long v = fz_load(fz.sync);
-      if ((v >> 32) == fz.gen && (unsigned)v >= (unsigned)fz.nprod) break;
+    if (fz_load(sync + 1) < (unsigned long long)ncons) {
+      const unsigned long long v = fz_load(sync);
+      if ((v >> 32) == gen && (unsigned)v >= (unsigned)nprod) break;
     }
-    if (__builtin_amdgcn_s_memrealtime() - t0 > FZ_BUDGET) break;
+    if (__builtin_amdgcn_s_memrealtime() - t0 > FZ_BUDGET) {
+      fz_mark();
+      break;
+    }
     __builtin_amdgcn_s_sleep(4);
   }
 }
 // A producer that then runs side items, one thread, after counting itself:
-// wait until every producer of this launch has counted itself.  Its own count
-// followed this launch's arming, so the count it reads is this launch's and
-// no condition on the tiles' count is needed.
-__device__ __forceinline__ void fz_wait_producers(const FuseArgs &fz) {
+// wait until every producer of this launch has counted itself.  Its own
+// count followed this launch's arming, so the count it reads is this
+// launch's and no condition on the tiles' count is needed.
+__device__ __forceinline__ void fz_wait_producers(unsigned long long *sync, unsigned gen, int nprod) {
   const unsigned long long t0 = __builtin_amdgcn_s_memrealtime();
   for (;;) {
-    const unsigned long long v = fz_load(fz.sync);
-    if ((v >> 32) == fz.gen && (unsigned)v >= (unsigned)fz.nprod) break;
-    if (__builtin_amdgcn_s_memrealtime() - t0 > FZ_BUDGET) break;
+    const unsigned long long v = fz_load(sync);
+    if ((v >> 32) == gen && (unsigned)v >= (unsigned)nprod) break;
+    if (__builtin_amdgcn_s_memrealtime() - t0 > FZ_BUDGET) {
+      fz_mark();
+      break;
+    }
     __builtin_amdgcn_s_sleep(4);
   }
 }
+// A producer about to run side items, after its wait has seen every
+// producer's count: invalidate the caches that could hold lines older than
+// the other producers' device-scope stores of du (this CU's vector L1, and
+// the L2 lines not kept coherent across XCDs) -- the cache action of a
+// device-scope acquire, without its wait for every load in flight (the
+// count's own load has returned: its value decided the wait).  64 producers
+// pay it at no measurable cost; in the tiles it cost 10 us per launch at
+// T = 1024, so they rely on the argument in launch.hpp (FuseArgs) instead.
+__device__ __forceinline__ void fz_acquire() { asm volatile("buffer_inv sc1" ::: "memory"); }
 // A consumer, one thread, once it has passed.
-__device__ __forceinline__ void fz_done(const FuseArgs &fz) {
-  __hip_atomic_fetch_add(fz.sync + 1, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+__device__ __forceinline__ void fz_done(unsigned long long *sync) {
+  __hip_atomic_fetch_add(sync + 1, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 constexpr int cmax(int a, int b) { return a > b ? a : b; }
@@ -220,7 +265,7 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   if constexpr (FUSE) {
     if (bid < 0) {
       if ((int)blockIdx.x < fz.nprod) {
-        if (blockIdx.x == 0 && tid == 0) fz_arm(fz);
+        if (blockIdx.x == 0 && tid == 0) fz_arm(fz.sync, fz.gen);
         // Coherent stores, complete in every wave before the count: no L2
         // write-back (which would stall every tile of the XCD) is needed.
         auto prod = [&](auto JB, auto MB) {
@@ -236,18 +281,22 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
         }
         __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
         __syncthreads();
-        if (tid == 0) fz_produced(fz);
+        if (tid == 0) fz_produced(fz.sync, fz.gen);
         // Backward: the producers then run the dA / dB side items (dA needs
         // all of du), on CUs the tiles leave to them.
         const int nitems = BMODE == B_KMAJ_TR ? side_items_total<E>(side) : 0;
         if constexpr (BMODE == B_KMAJ_TR) if (nitems > 0) {
-          if (tid == 0) fz_wait_producers(fz);
+          if (tid == 0) {
+            fz_wait_producers(fz.sync, fz.gen, fz.nprod);
+            fz_acquire();
+          }
           __syncthreads();
           for (int it = blockIdx.x; it < nitems; it += fz.nprod) {
             side_item<E, WM * WN * WK>(side, it, smem);
             __syncthreads();
           }
         }
+        fz_report();
       }
       return;
     }
@@ -412,8 +461,8 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
         const int c = DBRB == 256 ? (lane & 15) ^ (4 * ((lane >> 4) & 3)) : (lane & 31) ^ (4 * (r & 3));
         const bool ok = c * 8 < BN && n0 + c * 8 < g.N;
         dkB[i] = 0;
+        // (k-major B2 has B's row length, so its offsets are B's.)
         dB[i] = ok ? (uint32_t)(r * g.ldb * ES + c * 16) : OOB;
-        dB2[i] = ok ? (uint32_t)(r * g.ldb2 * ES + c * 16) : OOB;
       }
     }
   }
@@ -654,7 +703,7 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
             (void *)base, (short)0, (int)(krem > 0 ? min(krem, BKE) * ld * ES : 0), 0x00020000);
 #pragma unroll
         for (int i = 0; i < DB_PW; ++i) {
-          dma16(rs, sB + (wv + i * NWV) * 1024, lora ? dB2[i] : dB[i], 0);
+          dma16(rs, sB + (wv + i * NWV) * 1024, dB[i], 0);
         }
       }
     }
@@ -758,7 +807,7 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
           const int64_t ld = lora ? g.ldb2 : g.ldb;
           const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
               (void *)base, (short)0, (int)(krem > 0 ? min(krem, BKE) * ld * ES : 0), 0x00020000);
-          dma16(rs, ring_b(BUF) + (wv + i * NWV) * 1024, lora ? dB2[i] : dB[i], 0);
+          dma16(rs, ring_b(BUF) + (wv + i * NWV) * 1024, dB[i], 0);
         }
       }
     }
@@ -843,7 +892,7 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
     // A fused launch's LoRA-step operands come from its producers: wait for
     // them before the first load of a LoRA stage (here when the prologue
     // already issues one, else in the step that does).
-    if (coh && nk_main < NBUF) fz_wait(fz);
+    if (coh && nk_main < NBUF) fz_wait(fz.sync, fz.gen, fz.nprod, fz.ncons);
     static_for<0, NBUF>([&](auto SI) { dma_stage(SI, decltype(SI)::value); });
     {
       constexpr int V = (NBUF - 1) * IPS;  // stage 0 landed
@@ -860,7 +909,7 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
       __builtin_amdgcn_sched_barrier(0);
       // A fused launch's LoRA stage holds its producers' output: wait for them
       // before the step that issues its loads.
-      if (FUSE && coh && kt + NBUF == nk_main) fz_wait(fz);
+      if (FUSE && coh && kt + NBUF == nk_main) fz_wait(fz.sync, fz.gen, fz.nprod, fz.ncons);
       __builtin_amdgcn_sched_barrier(0);
       // The loads of stage kt + NBUF are spread between the fragment reads of
       // stage kt + 1 (in source order: an LDS read cannot pass the load
@@ -907,7 +956,7 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
     __builtin_amdgcn_s_waitcnt(0 | W_ENC);
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    if (coh && tid == 0) fz_done(fz);
+    if (coh && tid == 0) fz_done(fz.sync);
   } else if constexpr (FS) {
     // Staged fragments: every MFMA fragment of a stage is read from LDS one
     // step ahead into the second of two register sets, so the MFMAs of a
@@ -1288,6 +1337,8 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
       }
     }
   }
+  // A fused tile wave whose wait gave up is counted once its stores are out.
+  if (coh) fz_report();
 }
 
 // Tile rows per XCD group: each XCD's ~ntiles/8 consecutive tiles form a block
@@ -1305,11 +1356,13 @@ template <class E, int BM, int BN, int WM, int WN, int WK, int BMODE, int BKB, i
           int QB = 0, int EPI = EPI_STORE, int DMA = 0>
 static hipError_t launch_cfg(const GemmArgs &g, const SideArgs *side, hipStream_t st, FuseArgs *fz = nullptr) {
   const int tm = g.M > 0 ? (g.M + BM - 1) / BM : 0, tn = (g.N + BN - 1) / BN;
+  // Direct-to-LDS tiles address a k-major B2 with B's per-lane offsets.
+  if (DMA && BMODE == B_KMAJ_TR && g.r > 0 && g.ldb2 != g.ldb) return hipErrorInvalidValue;
   SideArgs sa{};
   int nside = 0;
   if (side) {
     sa = *side;
-    nside = side_workgroups(sa, std::is_same<E, BF16>::value ? DT_BF16 : DT_F32);
+    nside = side_workgroups(&sa, std::is_same<E, BF16>::value ? DT_BF16 : DT_F32);
   }
   FuseArgs fa{};
   if (fz && fz->nprod > 0) {
@@ -1322,7 +1375,7 @@ static hipError_t launch_cfg(const GemmArgs &g, const SideArgs *side, hipStream_
     const int mb = ((T + 15) / 16 + 7) / 8 * 8 <= free ? 1 : 2;
     fz->row.mb = mb;
     fz->nprod = (int)((T + 16 * mb - 1) / (16 * mb));
-    fz->ncons = tm * tn;  // consumers: the tiles
+    fz->ncons = fz->hold ? 0 : tm * tn;  // consumers: the tiles (0: every wait gives up)
     fz->nwg = (fz->nprod + 7) / 8 * 8;
     fa = *fz;
   }
@@ -1334,10 +1387,14 @@ static hipError_t launch_cfg(const GemmArgs &g, const SideArgs *side, hipStream_
   return hipGetLastError();
 }
 
-int side_workgroups(const SideArgs &s, Dtype dt) {
+int side_workgroups(SideArgs *s, Dtype dt) {
   const int cols = dt == DT_BF16 ? SideShape<BF16>::COLS : SideShape<F32>::COLS;
   int n = 0;
-  for (int i = 0; i < s.njobs; ++i) n += (s.job[i].L + cols - 1) / cols * ((s.r + 31) / 32);
+  for (int i = 0; i < s->njobs; ++i) {
+    n += (s->job[i].L + cols - 1) / cols * ((s->r + 31) / 32);
+    if (i == 0) s->n0 = n;
+  }
+  s->ntot = n;
   return (n + 7) / 8 * 8;
 }
 
@@ -1367,6 +1424,13 @@ static int pick_shape(int M, int N, bool b_kmajor, bool with_side) {
   if (c3 < c0 && c3 < c1 && c3 < c2) return 3;
   if (c2 <= c1 && c2 <= c0) return 2;
   return c1 < c0 ? 1 : 0;
+}
+
+void gemm_tile_shape(int M, int N, bool b_kmajor, bool with_side, Dtype dt, int *bm, int *bn) {
+  static const int shp[5][2] = {{128, 128}, {256, 128}, {256, 256}, {128, 64}, {256, 192}};
+  const int c = dt == DT_BF16 ? pick_shape(M, N, b_kmajor, with_side) : 0;
+  *bm = shp[c][0];
+  *bn = shp[c][1];
 }
 
 hipError_t launch_gemm_epi(const GemmArgs &g, int epi, hipStream_t st) {
@@ -1455,6 +1519,14 @@ hipError_t launch_gemm(const GemmArgs &g, Dtype dt, bool b_kmajor, const SideArg
   }
   return b_kmajor ? launch_cfg<F32, 128, 128, 2, 4, 1, B_KMAJ_REG, 128, 2, 2, 0>(g, side, st)
                   : launch_cfg<F32, 128, 128, 2, 4, 1, B_ROW, 128, 2, 2, 0>(g, side, st);
+}
+
+hipError_t handover_giveups(unsigned *count, bool reset) {
+  hipError_t e = hipMemcpyFromSymbol(count, HIP_SYMBOL(g_fz_giveups), sizeof(unsigned), 0,
+                                     hipMemcpyDeviceToHost);
+  if (e != hipSuccess || !reset) return e;
+  const unsigned zero = 0;
+  return hipMemcpyToSymbol(HIP_SYMBOL(g_fz_giveups), &zero, sizeof(unsigned), 0, hipMemcpyHostToDevice);
 }
 
 }  // namespace lora

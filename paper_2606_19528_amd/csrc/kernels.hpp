@@ -113,15 +113,18 @@ typedef __attribute__((address_space(3))) void lds_void;
 // flight.  Every read of a stage is ordered after its loads by the explicit
 // wait + barrier protocol of the main loop instead.  (No compiler-generated
 // code of these kernels keeps a value in M0.)  The compiler does not look
-// into the assembly for hazards, so it carries its own wait states: five
-// before the load may read SGPRs that a vector instruction wrote, one
-// between the write of M0 and the load that reads it.
+// into the assembly for hazards, so it carries the one wait state the write
+// of M0 needs before the load reads it.  The other hazard such a load has --
+// five wait states after a vector instruction writes an SGPR the load reads
+// (its resource or soffset) -- does not arise in these kernels: those
+// operands come from scalar instructions, which the generated-code tests
+// check for every load (a blanket s_nop 4 here cost 1-7 % of GEMM time).
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
 __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, char *lds, uint32_t voffset,
                                       int soffset) {
   const uint32_t base = (uint32_t)(uintptr_t)(lds_void *)lds;
-  asm volatile("s_nop 4\n\ts_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds" ::"s"(base),
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds" ::"s"(base),
                "v"(voffset),
                "s"(rs), "s"(soffset)
                : "memory", "m0");

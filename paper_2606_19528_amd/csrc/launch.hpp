@@ -14,28 +14,27 @@ void set_last_error(const char *msg);
 
 // Side work run by extra workgroups of the backward GEMM launch (they
 // overlap with the dx tiles): token-reduced products
-//   dA = du^T x   out [r, L] (transposed store), scale 1
-//   dB = s dy^T u out [L, r],                    scale s
-// out[l][j] = scale * sum_t X[t*ldx + l] * V[t*r + j], t < T.
-// V may be given as `vparts` partial sums V_p = V + p * vstride (p < vparts),
-// added in ascending p when loaded.
+//   job 0: dA = du^T x   out [r, L] (transposed store), scale 1
+//   job 1: dB = s dy^T u out [L, r],                    scale s (scale1)
+// out[l][j] = scale * sum_t X[t*L + l] * V[t*r + j], t < T (X has rows of
+// L elements).  V may be given as `vparts` partial sums V_p = V + p * vstride
+// (p < vparts), added in ascending p when loaded.  (Kept small: these
+// arguments share the kernel's scalar registers with the tiles.)
 struct ColJob {
   const void *X;
-  int64_t ldx;
-  int L;
   const float *V;
   float *out;
-  int transpose_out;
-  float scale;
+  int L;
   int vparts;
-  int64_t vstride;
 };
 struct SideArgs {
   ColJob job[2];
   int njobs;
   int T, r;
+  float scale1;
+  int64_t vstride;
+  int n0, ntot;  // work items of job 0 and of both (set by the GEMM launcher)
 };
-
 
 // C[M, N] = sum_k Aop[m][k] Bop[n][k]  (+ LoRA step), rounded to the element type.
 //   Aop[m][k] = A[m*lda + k]                         m < M, k < K
@@ -163,8 +162,13 @@ hipError_t launch_gemm(const GemmArgs &g, Dtype dt, bool b_kmajor, const SideArg
 hipError_t launch_gemm_q(const GemmArgs &g, int bits, bool b_kmajor, const SideArgs *side,
                          hipStream_t st);
 
-// Number of side workgroups needed for `side` (a multiple of 8).
-int side_workgroups(const SideArgs &s, Dtype dt);
+// Output tile (BM x BN) that launch_gemm / launch_gemm_fused run for an
+// M x N product with this B layout, with or without side items.
+void gemm_tile_shape(int M, int N, bool b_kmajor, bool with_side, Dtype dt, int *bm, int *bn);
+
+// Counts the work items of `side` into s->n0 and s->ntot and returns the
+// number of side workgroups they need (a multiple of 8).
+int side_workgroups(SideArgs *s, Dtype dt);
 
 enum { V_ROW = 0, V_KMAJ_TR = 1, V_KMAJ_GATHER = 2 };
 enum { BCOPY_NONE = 0, BCOPY_COLS = 1, BCOPY_FLAT = 2 };
@@ -214,21 +218,37 @@ hipError_t launch_row_skinny(const RowArgs &a, Dtype dt, hipStream_t st);
 // nothing else may use them during the launch):
 //   sync[0] = (gen << 32) | producers counted, sync[1] = tiles that passed.
 // Workgroup 0 arms the launch before its work (sync[0] = gen << 32, then,
-// released after it, sync[1] = 0).  A producer stores its rows coherently at
-// device scope (write-through, no L2 write-back that would stall the tiles of
-// its XCD), waits until every wave's stores have completed, and counts itself
-// in sync[0] once it sees the launch armed: sync[1] == 0, then the tag in
-// sync[0].  A tile, in the step that issues its LoRA stage, waits until
-// sync[1] < ncons and then sync[0] holds the tag and all producers, reads the
-// producers' rows with ordinary loads, and counts itself in sync[1] after its
-// main loop.  The reads see the producers' data: no L2 holds an older copy of
-// those rows (the L2s are invalidated when a launch starts, and nothing in
-// the launch reads the rows before the wait), so every read fetches the rows
-// as the producers stored them.  A stale state left by an earlier launch with
-// the same tag (a replayed graph) has sync[1] == ncons, so it never passes
-// for armed; a workspace with arbitrary contents holds the tag only by a
-// 2^-32 chance.  Every wait gives up after about 0.2 s, so a broken hand-over
-// yields wrong results, never a hang.
+// released after it, sync[1] = 0).  A producer stores its rows with
+// device-scope atomic stores (relaxed; on gfx950 they carry the sc1 policy
+// and write through to the point of coherence, with no L2 write-back that
+// would stall the tiles of its XCD), waits until every wave's stores have
+// completed (vmcnt 0), and counts itself in sync[0] once it sees the launch
+// armed: sync[1] == 0, then the tag in sync[0].  A tile, in the step that
+// issues its LoRA stage, waits until sync[1] < ncons and sync[0] holds the
+// tag and all producers, reads the producers' rows with ordinary loads, and
+// counts itself in sync[1] after its main loop.
+// Why ordinary loads see the producers' stores without an acquire fence: a
+// fence would make the reads fetch past any cache line older than the
+// stores, and no such line can exist -- the caches hold no line of the
+// workspace from an earlier launch (a kernel boundary writes back and
+// invalidates the L1s and the per-XCD L2s), each producer owns whole
+// 128-byte lines of the rows (16 or 32 rows of r >= 8 fp32, or of 64 bf16),
+// and no wave of the launch reads any of those lines before its wait has
+// seen every producer's count, i.e. after every producer's stores completed
+// at the point of coherence.  The first read of such a line therefore
+// misses in the reader's L1 and L2 and fetches the stored bytes.  (Measured
+// at T = 1024: the tiles' device-scope acquire cost 10 us per fused launch,
+// sc1 loads of the LoRA stage made the 256 x 128 tiles spill registers.)
+// The side items on the producers read du after an invalidate of that
+// kind, which costs them nothing measurable.
+// A stale state left by an earlier launch with the same tag (a replayed
+// graph) has sync[1] == ncons, so it never passes for armed; a workspace
+// with arbitrary contents holds the tag only by a 2^-32 chance.
+// Every wait gives up after 0.2 s (the 100 MHz real-time counter), so no
+// launch can hang on a broken hand-over; each wave whose wait gave up adds
+// one to a per-device counter once its work is done (handover_giveups),
+// which callers and tests check, because that launch may have computed with
+// incomplete producer rows.
 struct FuseArgs {
   RowArgs row;
   int nprod;                 // producers (row blocks); 0: no fusion
@@ -236,7 +256,12 @@ struct FuseArgs {
   unsigned long long *sync;  // sync[0], sync[1]
   unsigned int gen;          // this launch's tag, never 0
   int ncons;                 // consumers: the tiles (set by launch_gemm_fused)
+  int hold;                  // 0; 1 only from a test: the tiles' waits then give up
 };
+
+// Reads (and, with reset, clears) this device's count of hand-over waits
+// that gave up.  Synchronous.
+hipError_t handover_giveups(unsigned *count, bool reset);
 
 // Whether the bf16 GEMM of this shape (forward: row-major B; backward:
 // k-major B, carrying the dA / dB side items) runs a tile configuration that

@@ -27,6 +27,12 @@ class _Node(ctypes.Structure):
                 ("d_out", ctypes.c_int64), ("r", ctypes.c_int64), ("scale", ctypes.c_float)]
 
 
+class _Plan(ctypes.Structure):
+    """lora_plan_t of the C ABI."""
+    _fields_ = [(n, ctypes.c_int) for n in ("fwd_tile_m", "fwd_tile_n", "fwd_fused", "fwd_u_parts",
+                                             "bwd_tile_m", "bwd_tile_n", "bwd_fused", "bwd_du_parts")]
+
+
 class LoraError(RuntimeError):
     def __init__(self, status: int, where: str, detail: str):
         super().__init__(f"{where}: status {status} ({detail})")
@@ -96,6 +102,12 @@ def lib() -> ctypes.CDLL:
     L.lora_kernel_name.restype = ctypes.c_char_p
     L.lora_kernel_count.argtypes = []
     L.lora_kernel_count.restype = i32
+    L.lora_linear_plan.argtypes = [i64, i64, i64, i64, i32, ctypes.POINTER(_Plan)]
+    L.lora_linear_plan.restype = i32
+    L.lora_handover_giveups.argtypes = [ctypes.POINTER(ctypes.c_uint64), i32]
+    L.lora_handover_giveups.restype = i32
+    L.lora_debug_set_handover.argtypes = [i32]
+    L.lora_debug_set_handover.restype = i32
     _lib = L
     return L
 
@@ -132,13 +144,20 @@ def _stream(stream):
     return ctypes.c_void_p(stream.cuda_stream)
 
 
-def _ws(ws, nbytes: int, like):
+def _ws(ws, nbytes: int, like, stream=None):
+    """The caller's workspace, or a temporary one.  A temporary is allocated on
+    the stream the call is enqueued on, so the caching allocator does not hand
+    its block to another tensor while that stream's kernels still use it."""
     import torch
 
     if nbytes == 0:
         return None, 0
     if ws is None:
-        ws = torch.empty(nbytes, dtype=torch.uint8, device=like.device)
+        if stream is None:
+            ws = torch.empty(nbytes, dtype=torch.uint8, device=like.device)
+        else:
+            with torch.cuda.stream(stream):
+                ws = torch.empty(nbytes, dtype=torch.uint8, device=like.device)
     return ws, ws.numel() * ws.element_size()
 
 
@@ -155,7 +174,7 @@ def lora_linear_fwd(x, W, A, B, y, u_save=None, scale: float = 1.0, ws=None, str
     d_out = W.shape[0]
     r = 0 if A is None else A.shape[0]
     dt = _dtype_code(x)
-    ws, ws_bytes = _ws(ws, lora_linear_workspace_bytes(LORA_OP_FWD, T, d_in, d_out, r, dt), x)
+    ws, ws_bytes = _ws(ws, lora_linear_workspace_bytes(LORA_OP_FWD, T, d_in, d_out, r, dt), x, stream)
     st = lib().lora_linear_fwd(_ptr(x), _ptr(W), _ptr(A), _ptr(B), _ptr(y), _ptr(u_save), T, d_in,
                                d_out, r, float(scale), dt, _ptr(ws), ws_bytes, _stream(stream))
     _check(st, "lora_linear_fwd")
@@ -168,7 +187,7 @@ def lora_linear_bwd(x, W, A, B, u_saved, dy, dx, dA, dB, scale: float = 1.0, ws=
     d_in = W.shape[1]
     r = 0 if A is None else A.shape[0]
     dt = _dtype_code(dy)
-    ws, ws_bytes = _ws(ws, lora_linear_workspace_bytes(LORA_OP_BWD, T, d_in, d_out, r, dt), dy)
+    ws, ws_bytes = _ws(ws, lora_linear_workspace_bytes(LORA_OP_BWD, T, d_in, d_out, r, dt), dy, stream)
     st = lib().lora_linear_bwd(_ptr(x), _ptr(W), _ptr(A), _ptr(B), _ptr(u_saved), _ptr(dy),
                                _ptr(dx), _ptr(dA), _ptr(dB), T, d_in, d_out, r, float(scale), dt,
                                _ptr(ws), ws_bytes, _stream(stream))
@@ -205,7 +224,7 @@ def lora_linear_fwd_q(x, Wq, A, B, y, u_save=None, scale: float = 1.0, ws=None, 
     codes, sc, off, bits, group, d_out, d_in = _qw(Wq)
     T = x.shape[0]
     r = 0 if A is None else A.shape[0]
-    ws, ws_bytes = _ws(ws, lora_linear_workspace_bytes(LORA_OP_FWD, T, d_in, d_out, r, LORA_BF16), x)
+    ws, ws_bytes = _ws(ws, lora_linear_workspace_bytes(LORA_OP_FWD, T, d_in, d_out, r, LORA_BF16), x, stream)
     st = lib().lora_linear_fwd_q(_ptr(x), _ptr(codes), _ptr(sc), _ptr(off), bits, group, _ptr(A),
                                  _ptr(B), _ptr(y), _ptr(u_save), T, d_in, d_out, r, float(scale),
                                  _ptr(ws), ws_bytes, _stream(stream))
@@ -219,7 +238,7 @@ def lora_linear_bwd_q(x, Wq, A, B, u_saved, dy, dx, dA, dB, scale: float = 1.0, 
     codes, sc, off, bits, group, d_out, d_in = _qw(Wq)
     T = dy.shape[0]
     r = 0 if A is None else A.shape[0]
-    ws, ws_bytes = _ws(ws, lora_linear_workspace_bytes(LORA_OP_BWD, T, d_in, d_out, r, LORA_BF16), dy)
+    ws, ws_bytes = _ws(ws, lora_linear_workspace_bytes(LORA_OP_BWD, T, d_in, d_out, r, LORA_BF16), dy, stream)
     st = lib().lora_linear_bwd_q(_ptr(x), _ptr(codes), _ptr(sc), _ptr(off), bits, group, _ptr(A),
                                  _ptr(B), _ptr(u_saved), _ptr(dy), _ptr(dx), _ptr(dA), _ptr(dB), T,
                                  d_in, d_out, r, float(scale), _ptr(ws), ws_bytes, _stream(stream))
@@ -259,7 +278,7 @@ def lm_head_build_vocab(table, k: int, targets, rows, ws=None, stream=None):
     nrows = rows.shape[0]
     J = torch.empty(V, dtype=torch.int32, device=table.device)
     tpos = torch.empty(nrows, dtype=torch.int32, device=table.device)
-    ws, ws_bytes = _ws(ws, lm_head_workspace_bytes(LM_HEAD_OP_VOCAB, T, V, 8, nrows), table)
+    ws, ws_bytes = _ws(ws, lm_head_workspace_bytes(LM_HEAD_OP_VOCAB, T, V, 8, nrows), table, stream)
     nJ = ctypes.c_int64(0)
     st = lib().lm_head_build_vocab(_ptr(table), V, ldtab, k, _ptr(targets), T, _ptr(rows), nrows,
                                    _ptr(J), _ptr(tpos), ctypes.byref(nJ), _ptr(ws), ws_bytes,
@@ -276,7 +295,7 @@ def lm_head_reduced_ce(h, W, rows, J, tpos, loss_rows, loss_total=None, dh=None,
     V = W.shape[0]
     nrows, nJ = rows.shape[0], J.shape[0]
     op = LM_HEAD_OP_LOSS if dh is None else LM_HEAD_OP_LOSS_DH
-    ws, ws_bytes = _ws(ws, lm_head_workspace_bytes(op, T, V, D, nrows, nJ), h)
+    ws, ws_bytes = _ws(ws, lm_head_workspace_bytes(op, T, V, D, nrows, nJ), h, stream)
     st = lib().lm_head_reduced_ce(_ptr(h), _ptr(W), T, V, D, _ptr(rows), nrows, _ptr(J), nJ,
                                   _ptr(tpos), _ptr(loss_rows), _ptr(loss_total), _ptr(dh),
                                   float(dscale), _ptr(ws), ws_bytes, _stream(stream))
@@ -296,7 +315,7 @@ def topk_table_build(W, k: int, table=None, values=None, ws=None, stream=None):
     n = lib().topk_table_workspace_bytes(V, D, k)
     if n == ctypes.c_size_t(-1).value:
         raise LoraError(LORA_EINVAL, "topk_table_workspace_bytes", "sizes rejected")
-    ws, ws_bytes = _ws(ws, int(n), W)
+    ws, ws_bytes = _ws(ws, int(n), W, stream)
     st = lib().topk_table_build(_ptr(W), V, D, k, _ptr(table), _ptr(values), _ptr(ws), ws_bytes,
                                 _stream(stream))
     _check(st, "topk_table_build")
@@ -373,3 +392,24 @@ def profiler_read(name: str):
     n = ctypes.c_int64(0)
     _check(lib().lora_profiler_read(idx, ctypes.byref(ms), ctypes.byref(n)), "lora_profiler_read")
     return ms.value, n.value
+
+
+# --- plan and hand-over diagnostics -------------------------------------------------
+def lora_linear_plan(T: int, d_in: int, d_out: int, r: int, dt: int = LORA_BF16) -> dict:
+    """Kernel configuration of lora_linear_fwd / lora_linear_bwd for these sizes:
+    GEMM output tiles, whether the rank-r pass is fused, number of partial sums."""
+    p = _Plan()
+    _check(lib().lora_linear_plan(T, d_in, d_out, r, dt, ctypes.byref(p)), "lora_linear_plan")
+    return {n: getattr(p, n) for n, _ in _Plan._fields_}
+
+
+def handover_giveups(reset: bool = False) -> int:
+    """Hand-over waits that gave up on the current device (synchronises it)."""
+    n = ctypes.c_uint64(0)
+    _check(lib().lora_handover_giveups(ctypes.byref(n), 1 if reset else 0), "lora_handover_giveups")
+    return n.value
+
+
+def debug_set_handover(hold: int = 0):
+    """Test hook: 1 makes every tile's hand-over wait give up (results invalid)."""
+    _check(lib().lora_debug_set_handover(hold), "lora_debug_set_handover")

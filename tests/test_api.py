@@ -328,3 +328,41 @@ def test_python_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(L, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError, match="not built"):
         L.lib()
+
+
+def test_plan_coverage():
+    """The W = 0 / B = 0 isolation cases of the GPU tests together select every
+    kernel configuration (GEMM tile, fused or not, one or several partial
+    sums) that any workload linear runs, in both directions."""
+    from test_gpu_isolation import CASES, signatures
+    from workloads import WORKLOADS
+
+    fwd = {c[1] for c in CASES}
+    bwd = {c[2] for c in CASES}
+    for w in WORKLOADS.values():
+        for lin in w.linears:
+            f, b = signatures(w.tokens, lin.d_in, lin.d_out, lin.rank)
+            assert f in fwd, (w.key, lin.name, f)
+            assert b in bwd, (w.key, lin.name, b)
+
+
+def test_plan_query():
+    p = lm.lora_linear_plan(1024, 3072, 3072, 16)
+    assert (p["fwd_tile_m"], p["fwd_tile_n"], p["fwd_fused"]) == (128, 128, 1)
+    p = lm.lora_linear_plan(300, 520, 392, 16, L.LORA_F32)
+    assert (p["fwd_tile_m"], p["fwd_tile_n"], p["fwd_fused"], p["bwd_fused"]) == (128, 128, 0, 0)
+    p = lm.lora_linear_plan(64, 128, 128, 0)
+    assert p["fwd_fused"] == 0 and p["fwd_u_parts"] == 0 and p["bwd_du_parts"] == 0
+    lib = lm.lib()
+    plan = L._Plan()
+    assert lib.lora_linear_plan(0, 128, 128, 8, 0, ctypes.byref(plan)) == EINVAL
+    assert lib.lora_linear_plan(64, 100, 128, 8, 0, ctypes.byref(plan)) == EUNSUP
+    assert lib.lora_linear_plan(64, 128, 128, 8, 0, None) == EINVAL
+
+
+def test_handover_hooks_reject_bad_arguments():
+    lib = lm.lib()
+    assert lib.lora_debug_set_handover(-1) == EINVAL
+    assert lib.lora_debug_set_handover(2) == EINVAL
+    assert lib.lora_handover_giveups(None, 0) == EINVAL
+    assert lib.lora_debug_set_handover(0) == L.LORA_OK

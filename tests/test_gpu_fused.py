@@ -139,3 +139,35 @@ def test_backward_side_items_on_producers(orc, shape, recompute):
     torch.cuda.synchronize()
     ref = oracle_lora(orc, inp, s)
     compare({k: v.cpu() for k, v in o.items()}, ref, torch.bfloat16, label="side items on producers")
+
+
+def test_handover_giveup_is_reported(orc):
+    """A hand-over that never completes for the tiles (the test hook makes
+    their wait condition unsatisfiable) must not hang: every tile wave gives
+    up after the 0.2 s budget, each kernel exits normally, and the give-ups
+    are counted.  The next launches with the default settings are correct
+    again and give up nowhere."""
+    T, K, N, r = 384, 512, 640, 16
+    p = lm.lora_linear_plan(T, K, N, r)
+    assert p["fwd_fused"] and p["bwd_fused"]
+    s = 2.0
+    inp = lora_inputs(T, K, N, r, seed=83)
+    d = {k: v.cuda() for k, v in inp.items()}
+    ws = _ws(T, K, N, r)
+    lm.handover_giveups(reset=True)
+    try:
+        lm.debug_set_handover(1)
+        _announce("fused hand-over forced to give up")
+        _step(d, _buffers(T, K, N, r), s, ws, ws)
+        torch.cuda.synchronize()
+        n = lm.handover_giveups(reset=True)
+    finally:
+        lm.debug_set_handover(0)
+        lm.handover_giveups(reset=True)
+    assert n > 0
+    o = _buffers(T, K, N, r)
+    _step(d, o, s, ws, ws)
+    torch.cuda.synchronize()
+    assert lm.handover_giveups() == 0
+    ref = oracle_lora(orc, inp, s)
+    compare({k: v.cpu() for k, v in o.items()}, ref, torch.bfloat16, label="after give-ups")
