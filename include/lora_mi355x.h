@@ -114,6 +114,23 @@ lora_status_t lora_linear_bwd(const void *x, const void *W, const void *A, const
                               float scale, lora_dtype_t dt, void *ws, size_t ws_bytes,
                               void *hip_stream);
 
+/* For callers that cannot allocate device memory -- code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc: the same
+ * operation as lora_linear_bwd, with the workspace taken from a static
+ * device array of the library (LORA_NOALLOC_SCRATCH_BYTES per GPU, held by
+ * every GPU the library runs on until the process ends) instead of a caller
+ * buffer.  Calls no allocating routine.  Arguments, outputs and errors as for
+ * lora_linear_bwd, plus LORA_EWORKSPACE when the sizes need more workspace
+ * than the static array holds, and LORA_EHIP if its address cannot be looked
+ * up.  The array belongs to the current device (hip_stream must be one of
+ * its streams) and keeps the last call's contents; calls that overlap on
+ * one GPU (other streams, other threads) race on it and must not be issued. */
+#define LORA_NOALLOC_SCRATCH_BYTES (16u << 20)
+lora_status_t lora_linear_bwd_noalloc(const void *x, const void *W, const void *A, const void *B,
+                                      const float *u_saved, const void *dy, void *dx, float *dA,
+                                      float *dB, int64_t T, int64_t d_in, int64_t d_out, int64_t r,
+                                      float scale, lora_dtype_t dt, void *hip_stream);
+
 /* Rank-0 frozen linear input gradient, dx = dy W (the frozen LM head of the
  * paper's checkpointing scheme, whose backward needs only dx):
  *   dy [T, d_out], W [d_out, d_in], dx [T, d_in]. */

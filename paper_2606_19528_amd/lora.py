@@ -57,6 +57,9 @@ def lib() -> ctypes.CDLL:
     L.lora_linear_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i64, i64, i64, i64, f32, i32,
                                   vp, sz, vp]
     L.lora_linear_bwd.restype = i32
+    L.lora_linear_bwd_noalloc.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i64, i64, i64, i64, f32, i32,
+                                          vp]
+    L.lora_linear_bwd_noalloc.restype = i32
     L.frozen_linear_bwd_dx.argtypes = [vp, vp, vp, i64, i64, i64, i32, vp, sz, vp]
     L.frozen_linear_bwd_dx.restype = i32
     L.lora_linear_fwd_q.argtypes = [vp, vp, vp, vp, i32, i64, vp, vp, vp, vp, i64, i64, i64, i64,
@@ -192,6 +195,20 @@ def lora_linear_bwd(x, W, A, B, u_saved, dy, dx, dA, dB, scale: float = 1.0, ws=
                                _ptr(dx), _ptr(dA), _ptr(dB), T, d_in, d_out, r, float(scale), dt,
                                _ptr(ws), ws_bytes, _stream(stream))
     _check(st, "lora_linear_bwd")
+    return dx, dA, dB
+
+
+def lora_linear_bwd_noalloc(x, W, A, B, u_saved, dy, dx, dA, dB, scale: float = 1.0, stream=None):
+    """lora_linear_bwd with the library's static device scratch as workspace
+    (no allocation by the library or by this wrapper)."""
+    T, d_out = dy.shape
+    d_in = W.shape[1]
+    r = 0 if A is None else A.shape[0]
+    dt = _dtype_code(dy)
+    st = lib().lora_linear_bwd_noalloc(_ptr(x), _ptr(W), _ptr(A), _ptr(B), _ptr(u_saved), _ptr(dy),
+                                       _ptr(dx), _ptr(dA), _ptr(dB), T, d_in, d_out, r, float(scale), dt,
+                                       _stream(stream))
+    _check(st, "lora_linear_bwd_noalloc")
     return dx, dA, dB
 
 
