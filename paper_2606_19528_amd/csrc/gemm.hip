@@ -1314,6 +1314,79 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
     return;
   }
   T *C = (T *)g.C;
+  if constexpr (DMA && WK == 1 && ES == 2) {
+    // Stores staged through LDS (free once the ring has drained), 32 rows of
+    // the wave's tile at a time: the lanes write their runs of 4 columns into
+    // the wave's own LDS rows, then read whole 16-byte pieces back so that
+    // each store instruction writes complete 128-byte lines of C.  (Storing
+    // the runs directly scatters 16-byte pieces over 32 rows per
+    // instruction; the staged form took 8-10 us off every wave of 256-wide
+    // tiles.)  Each wave uses its own rows, and a wave's LDS accesses are
+    // performed in order, so no barrier is needed.
+    constexpr int ROWB = WTN * 2 + 16;        // padded LDS row
+    constexpr int LPR = WTN / 8, RPI = 64 / LPR;  // lanes per row, rows per store
+    static_assert(NWV * 32 * ROWB <= LDS, "staged epilogue fits the LDS");
+    char *rows = smem + wave * 32 * ROWB;
+    const int ncol = n0 + wn * WTN + (lane % LPR) * 8;
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const uint32_t lo = (uint32_t)E::from_float(acc[i][j][4 * q + 0]) |
+                              ((uint32_t)E::from_float(acc[i][j][4 * q + 1]) << 16);
+          const uint32_t hi = (uint32_t)E::from_float(acc[i][j][4 * q + 2]) |
+                              ((uint32_t)E::from_float(acc[i][j][4 * q + 3]) << 16);
+          *(uint2 *)(rows + lrow * ROWB + (j * 32 + 8 * q + 4 * (lane >> 5)) * 2) = make_uint2(lo, hi);
+        }
+#pragma unroll
+      for (int r0 = 0; r0 < 32; r0 += RPI) {
+        const int row = r0 + lane / LPR;
+        if (lane < RPI * LPR && row < 32) {
+          const u32x4 v = ld16(rows + row * ROWB + (lane % LPR) * 16);
+          const int m = m0 + wm * WTM + i * 32 + row;
+          if (m < g.M && ncol < g.N) st16(C + (int64_t)m * g.ldc + ncol, v);
+        }
+      }
+    }
+    if (coh) fz_report();
+    return;
+  }
+  if constexpr (DMA && WK > 1 && ES == 2) {
+    // The same for tiles whose waves split k: after the reduction each wave
+    // owns some 32 x 32 blocks of its wave tile, so the whole tile is staged
+    // in LDS (the reduction's last barrier has freed it), and after one
+    // barrier every thread stores 16-byte pieces of whole rows.
+    constexpr int ROWB = BN * 2 + 16;
+    constexpr int LPR = BN / 8, RPR = NT / LPR;  // lanes per row, rows per round
+    static_assert(BM * ROWB <= LDS, "staged epilogue fits the LDS");
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      if (b % WK != wk) continue;
+      const int i = b / FN, j = b % FN;
+      const int row = wm * WTM + i * 32 + lrow;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t lo = (uint32_t)E::from_float(acc[i][j][4 * q + 0]) |
+                            ((uint32_t)E::from_float(acc[i][j][4 * q + 1]) << 16);
+        const uint32_t hi = (uint32_t)E::from_float(acc[i][j][4 * q + 2]) |
+                            ((uint32_t)E::from_float(acc[i][j][4 * q + 3]) << 16);
+        *(uint2 *)(smem + row * ROWB + (wn * WTN + j * 32 + 8 * q + 4 * (lane >> 5)) * 2) = make_uint2(lo, hi);
+      }
+    }
+    __syncthreads();
+    const int ncol = n0 + (tid % LPR) * 8;
+#pragma unroll
+    for (int r0 = 0; r0 < BM; r0 += RPR) {
+      const int row = r0 + tid / LPR;
+      const u32x4 v = ld16(smem + row * ROWB + (tid % LPR) * 16);
+      const int m = m0 + row;
+      if (m < g.M && ncol < g.N) st16(C + (int64_t)m * g.ldc + ncol, v);
+    }
+    if (coh) fz_report();
+    return;
+  }
 #pragma unroll
   for (int b = 0; b < NB; ++b) {
     if (WK > 1 && b % WK != wk) continue;
