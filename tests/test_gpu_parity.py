@@ -93,11 +93,15 @@ def test_wide_tiles(orc, shape):
 
 
 # 256 x 192 tiles fill the 256 CUs in one wave where the output is about
-# 4096 x 3072: T = 4000 and d_in = d_out = 3000 select them for the forward and
-# for dx, with ragged row and column tiles and both reduction axes not a
-# multiple of the stage depth.  Sampled rows of y and dx; dA and dB in full.
+# 4096 x 3072: T = 4000 and d_in = d_out = 3000 select them for the forward
+# (dx, which carries the dA / dB side items, runs 256 x 256 tiles; the k-major
+# 256 x 192 path is covered by test_frozen_dx_one_wave_tiles), with ragged row
+# and column tiles and both reduction axes not a multiple of the stage depth.
+# Sampled rows of y and dx; dA and dB in full.
 def test_one_wave_tiles(orc):
     T, K, N, r = 4000, 3000, 3000, 16
+    p = lm.lora_linear_plan(T, K, N, r)
+    assert (p["fwd_tile_m"], p["fwd_tile_n"], p["bwd_tile_m"], p["bwd_tile_n"]) == (256, 192, 256, 256)
     rows = list(range(0, T, 53)) + [T - 1]
     _case(orc, T, K, N, r, 2.0 * r, seed=61, rows=rows)
 
