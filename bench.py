@@ -391,7 +391,7 @@ def cpu_info():
     return model, os.cpu_count(), aff
 
 
-def cpu_baseline(workload, layers, head, target_s=10.0):
+def cpu_baseline(workload, layers, head, target_s=15.0):
     """The fp64 oracle (as it stands) timed on the host on a bounded sample of
     the same workload: the full fwd + bwd of the first decoder layer's linears
     over their first Ts tokens (Ts chosen so the sample takes about

@@ -7,6 +7,9 @@ ratio would blow up where the reference is near zero.
 """
 from __future__ import annotations
 
+import json
+import os
+
 import numpy as np
 import torch
 
@@ -87,6 +90,17 @@ def oracle_lora(orc, inp: dict, s: float, rows=None) -> dict:
             "dA": orc.da(dU, x), "dB": orc.db(dy, U, s)}
 
 
+def log_errors(label: str, errs: dict) -> None:
+    """Append the errors of one case to the JSON-lines file named by
+    LORA_PARITY_LOG, if set (a record of the achieved errors per test)."""
+    path = os.environ.get("LORA_PARITY_LOG")
+    if not path:
+        return
+    test = os.environ.get("PYTEST_CURRENT_TEST", "").split(" ")[0]
+    with open(path, "a") as f:
+        f.write(json.dumps({"test": test, "case": label, "errors": errs}) + "\n")
+
+
 def compare(gpu: dict, ref: dict, dtype, rows=None, label: str = "") -> dict:
     """Per-tensor errors; asserts each is within the dtype's tolerance."""
     tol = TOL[dtype]
@@ -98,6 +112,7 @@ def compare(gpu: dict, ref: dict, dtype, rows=None, label: str = "") -> dict:
         if rows is not None and k in ("y", "dx"):
             g = g[rows]
         errs[k] = relerr(g, ref[k])
+    log_errors(label, errs)
     bad = {k: e for k, e in errs.items() if not e <= tol}
     assert not bad, f"{label} errors above {tol}: {bad} (all: {errs})"
     return errs

@@ -12,7 +12,7 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_helpers import TOL, compare, gpu_lora, oracle_lora, relerr
+from gpu_helpers import TOL, compare, gpu_lora, log_errors, oracle_lora, relerr
 from workloads import WORKLOADS, frozen_inputs, linear_seed, lora_inputs, sample_rows
 
 pytestmark = pytest.mark.gpu
@@ -249,7 +249,9 @@ def test_full_llama_lm_head_dx(orc):
     torch.cuda.synchronize()
     rows = sample_rows(T, 16)
     ref = orc.frozen_dx(inp["dy"][rows], inp["W"])
-    assert relerr(dx.cpu()[rows].to(torch.float64).numpy(), ref) <= TOL[torch.bfloat16]
+    err = relerr(dx.cpu()[rows].to(torch.float64).numpy(), ref)
+    log_errors(f"T={T} K={head.d_in} N={head.d_out} r=0", {"dx": err})
+    assert err <= TOL[torch.bfloat16]
 
 
 def test_no_dw_sized_allocation():
