@@ -57,8 +57,10 @@ __device__ __forceinline__ int side_items_total(const SideArgs &s) {
   return s.ntot;
 }
 
+// Always inlined: called as a function, it takes the launch's arguments by
+// address, so every wave of the launch first copies them to scratch memory.
 template <class E, int NW>
-__device__ void side_item(const SideArgs &s, int item, char *smem) {
+__device__ __forceinline__ void side_item(const SideArgs &s, int item, char *smem) {
   typedef typename E::T T;
   constexpr int VEC = E::VEC;
   constexpr int COLS = SideShape<E>::COLS;
@@ -71,9 +73,8 @@ __device__ void side_item(const SideArgs &s, int item, char *smem) {
     ji = 1;
     item -= s.n0;
   }
-  // The job's fields, each chosen by a select between the two constant
-  // indices (indexing the argument array with the run-time ji made the
-  // compiler copy the arguments to scratch memory).
+  // The job's fields, each a select between the two jobs' (indexing the job
+  // array with the run-time ji would copy the arguments to scratch memory).
   const void *jX = ji ? s.job[1].X : s.job[0].X;
   const float *jV = ji ? s.job[1].V : s.job[0].V;
   float *jout = ji ? s.job[1].out : s.job[0].out;

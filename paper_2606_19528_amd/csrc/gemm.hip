@@ -301,9 +301,12 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
       return;
     }
   }
-  if (bid < nside) {
-    if (bid < side_items_total<E>(side)) side_item<E, WM * WN * WK>(side, bid, smem);
-    return;
+  // (A fused launch runs its side items on the producers: nside = 0.)
+  if constexpr (!FUSE) {
+    if (bid < nside) {
+      if (bid < side_items_total<E>(side)) side_item<E, WM * WN * WK>(side, bid, smem);
+      return;
+    }
   }
   int t;
   {

@@ -127,3 +127,26 @@ def test_hazard_scan_catches_a_planted_hazard():
                       "s_add_u32 s3, s3, 4", "s_mov_b32 m0, s4", "s_nop 0",
                       "buffer_load_dwordx4 v1, s[8:11], s12 offen lds"])
     assert not _sgpr_hazards(far)[1]
+
+
+def _resources(asm, name):
+    tail = asm[asm.index(name + ": ;"):]
+    tail = tail[tail.index(".Lfunc_end"):][:6000]
+    return {k: int(re.search(r"; %s: (\d+)" % k, tail).group(1)) for k in ("ScratchSize", "NumVgprs")}
+
+
+def test_gemm_kernels_make_no_calls_and_fused_backward_does_not_spill(gemm_asm):
+    # A device function the compiler leaves out of line takes the kernel's
+    # arguments by address, so every wave copies them to scratch memory at
+    # entry.  The fused backward instances (k-major B, DMA = 2: tiles,
+    # producers and side items in one kernel) must not spill at all.  (The
+    # 256 x 128 row-major tiles hold 256 VGPRs per lane and spill a few
+    # dwords, as measured.)
+    for name, body in _kernels(gemm_asm):
+        assert "s_swappc" not in body, name
+        # template integers: BM BN WM WN WK BMODE BKB NBUF RD FS QB EPI DMA
+        p = [int(v) for v in re.findall(r"Li(\d+)E", name)]
+        assert len(p) == 13, name
+        bmode, dma = p[5], p[12]
+        if dma == 2 and bmode == 2:
+            assert _resources(gemm_asm, name)["ScratchSize"] == 0, name
