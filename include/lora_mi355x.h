@@ -149,8 +149,11 @@ lora_status_t frozen_linear_bwd_dx(const void *dy, const void *W, void *dx, int6
  *   W_codes   [d_out][d_in * bits / 8] bytes of unsigned codes; bits = 8:
  *             one code per byte; bits = 4: two per byte, the code of the even
  *             input k in the low nibble, of k + 1 in the high nibble.
- *   W_scale,  [d_out][d_in / group] fp32: the weight of code q in row n,
- *   W_offset  input k is  W_scale[n][k / group] * q + W_offset[n][k / group].
+ *   W_scale,  [d_in / group][d_out] fp32, group-major: the weight of code q
+ *   W_offset  in row n, input k is
+ *               W_scale[k / group][n] * q + W_offset[k / group][n]
+ *             (a GEMM stage reads one group's scales for many consecutive
+ *             rows, which this layout keeps contiguous).
  *   group     a power of two >= 16 that divides d_in.
  * Everything else is as for the bf16 entry points, with dt = LORA_BF16
  * (x, A, B, y, dy, dx bf16) and rank r <= 64.  Errors as above, plus

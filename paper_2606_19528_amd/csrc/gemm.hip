@@ -202,7 +202,36 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   constexpr int DSTAGE = DA_BYTES + DB_BYTES;
   constexpr int DA_PW = DA_BYTES / 1024 / NWV, DB_PW = DB_BYTES / 1024 / NWV;  // loads per wave per stage
   constexpr int IPS = DA_PW + DB_PW;
-  constexpr int RING = DMA ? NBUF * DSTAGE : NBUF * STAGE;
+  // Quantized B on the direct-to-LDS path (DMA = 1, QB = 4 or 8; groups of at
+  // least 64 weights, so a stage of a row-major B holds one group per row):
+  // the stage's codes and the scales and offsets it needs are loaded straight
+  // into LDS too, into a ring of three slots of their own, two stages ahead
+  // of the stage's A loads; each step then dequantizes one stage from its
+  // slot into the bf16 B area of the ring (same layout as the bf16 path).
+  // A code slot holds the stage's runs of 16 weights (one W row, one group)
+  // in order: row-major B run = tile row * (BKE / 16) + k / 16, k-major B run
+  // = k row * (BN / 16) + n / 16, at 2 * QB bytes each.  Scales and offsets
+  // (group-major in memory, so those of one group and consecutive W rows are
+  // contiguous): k-major B, one slot per stage holding, per group touched by
+  // the tile's columns, its BKE k rows (group - first group) * BKE + k row;
+  // row-major B, whose tile rows keep a group for G / BKE stages, one slot
+  // per group (group % 4) holding the group's BN tile rows, loaded with the
+  // codes of the group's first stage.  Wave 0 issues them (two 16-byte
+  // loads), first in their step, and only in the steps that have some; the
+  // wait at the top of the next step counts them only where that step
+  // issued them.
+  constexpr bool QD = DMA == 1 && QB != 0;
+  constexpr int QCW = QD ? 128 / QB : 16;                               // weights per 16-byte code chunk
+  constexpr int QCHUNKS = QD ? BKE * BN / QCW : 0;                      // code chunks per stage
+  constexpr int QC_PW = (QCHUNKS + 64 * NWV - 1) / (64 * NWV);          // code loads per wave per stage
+  constexpr int QSLOT = QC_PW * NWV * 1024;                             // bytes of a code slot
+  constexpr int QSO = 1024;                                             // bytes of a slot's scales (or offsets)
+  constexpr int QRUNS = QD ? BKE * BN / 16 : 0;                         // runs of 16 weights per stage
+  constexpr int QRPT = QD ? (QRUNS + NT - 1) / NT : 1;                  // runs per thread
+  constexpr int QIPS = QC_PW + DA_PW;                                   // counted loads per wave per step
+  constexpr int QSOSLOTS = BMODE == B_ROW ? 4 : 3;                        // scale / offset slots
+  constexpr int QAREA = QD ? 3 * QSLOT + QSOSLOTS * 2 * QSO : 0;
+  constexpr int RING = DMA ? NBUF * DSTAGE + QAREA : NBUF * STAGE;
   constexpr int LDS0 = RING > RED_BYTES ? RING : RED_BYTES;
   constexpr int SIDE = side_lds_bytes<E, WM * WN * WK>();
   // Producer workgroups of a fused rank-r pass ahead of the bf16
@@ -225,7 +254,11 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile");
   static_assert(BMODE != B_KMAJ_TR || ES == 2, "transposed LDS reads are bf16");
   static_assert(DMA ? (NBUF == 3 || NBUF == 4) : (NBUF == 2 || NBUF == 3), "LDS ring depth");
-  static_assert(!DMA || (QB == 0 && ES == 2 && FS == 2 && (BKB == 128 || BKB == 64) && BMODE != B_KMAJ_REG &&
+  static_assert(!QD || (NBUF == 3 && BN <= 256 && (BN / 64 + 1) * BKE <= 256 && QCW * QC_PW * 64 * NWV >= BKE * BN &&
+                        QRUNS * 2 * QB <= QSLOT && QRPT * NT * 2 * QB <= QSLOT && EPI == EPI_STORE &&
+                        BKE % 16 == 0 && BN % 16 == 0 && QIPS < 64),
+                "quantized direct-to-LDS stages: a ring of three, whole runs of 16 weights");
+  static_assert(!DMA || ((QB == 0 || DMA == 1) && ES == 2 && FS == 2 && (BKB == 128 || BKB == 64) && BMODE != B_KMAJ_REG &&
                          DA_BYTES % (1024 * NWV) == 0 && DB_BYTES % (1024 * NWV) == 0 &&
                          (BMODE != B_KMAJ_TR || DBRB == 256 || DBRB == 512)),
                 "direct-to-LDS stages: bf16, 64- or 32-deep stages, whole 1 KB loads per wave");
@@ -238,7 +271,7 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   static_assert(EPI == EPI_STORE || (ES == 2 && FS), "cross-entropy / fp32 epilogues: bf16 kernels");
   static_assert((EPI != EPI_CE_STATS && EPI != EPI_TOPK) || (NT == 4 * BM && BM * (BN + 1) * 4 + BN * 4 <= LDS),
                 "row statistics / candidates: four threads per tile row, the fp32 tile in LDS");
-  static_assert(QB == 0 || (ES == 2 && FS && BMODE != B_KMAJ_REG && QPIECES == NT),
+  static_assert(QB == 0 || QD || (ES == 2 && FS && BMODE != B_KMAJ_REG && QPIECES == NT),
                 "quantized B: bf16, staged fragments, one 16-weight piece per thread");
 
   __shared__ __align__(16) char smem[LDS];
@@ -472,21 +505,66 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
 
   // Quantized B: the thread's piece of 16 weights (W row `qrow`, first weight
   // of the piece `qcol` within the stage or tile), codes through one buffer
-  // resource, per-group scale and offset through two more.
+  // resource, per-group scale and offset through two more.  Scales and
+  // offsets are group-major: [groups per W row][W rows] (q_wrows W rows: N
+  // for row-major B, K for k-major B).
   const int qrow = BMODE == B_ROW ? tid / (BKE / 16) : tid / (BN / 16);
   const int qcol = BMODE == B_ROW ? (tid % (BKE / 16)) * 16 : (tid % (BN / 16)) * 16;
   const int64_t q_rowbytes = (int64_t)g.ldb * (QB ? QB : 8) / 8;
   const int64_t q_ldg = g.ldb >> g.qlog2g;  // groups per W row
+  const int q_wrows = BMODE == B_ROW ? g.N : g.K;
   __amdgpu_buffer_rsrc_t rsQ, rsQs, rsQo;
-  if constexpr (QB && BMODE == B_ROW) {
-    const int nrows = min(g.N - n0, BN);
-    rsQ = __builtin_amdgcn_make_buffer_rsrc((void *)((const char *)g.B + n0 * q_rowbytes), (short)0,
-                                            (int)(nrows * q_rowbytes), 0x00020000);
-    rsQs = __builtin_amdgcn_make_buffer_rsrc((void *)(g.qscale + n0 * q_ldg), (short)0,
-                                             (int)(nrows * q_ldg * 4), 0x00020000);
-    rsQo = __builtin_amdgcn_make_buffer_rsrc((void *)(g.qoffset + n0 * q_ldg), (short)0,
-                                             (int)(nrows * q_ldg * 4), 0x00020000);
+  if constexpr (QB) {
+    if constexpr (BMODE == B_ROW) {
+      const int nrows = min(g.N - n0, BN);
+      rsQ = __builtin_amdgcn_make_buffer_rsrc((void *)((const char *)g.B + n0 * q_rowbytes), (short)0,
+                                              (int)(nrows * q_rowbytes), 0x00020000);
+    }
+    rsQs = __builtin_amdgcn_make_buffer_rsrc((void *)g.qscale, (short)0, (int)(q_ldg * q_wrows * 4), 0x00020000);
+    rsQo = __builtin_amdgcn_make_buffer_rsrc((void *)g.qoffset, (short)0, (int)(q_ldg * q_wrows * 4), 0x00020000);
   }
+  // Quantized direct-to-LDS loads (QD): per lane, the offset of its code
+  // chunk relative to the stage's first weight and the k position (row-major
+  // B) or k row (k-major B) that masks it against K; row-major codes go
+  // through rsQ (the tile's W rows, stage k in soffset), k-major codes
+  // through a resource over all K rows (stage row in soffset).  Scales and
+  // offsets: one 16-byte load per lane covering four W rows of one group --
+  // row-major B, tile rows 4 lane .. 4 lane + 3 (group in soffset); k-major
+  // B, k rows 4 kq .. 4 kq + 3 of group q_g0 + gg, lane = gg (BKE / 4) + kq
+  // (stage row in soffset).  Out of range: rows past N (row-major), groups
+  // past the row's last, k rows past K (per stage).
+  const int q_ngk = BMODE == B_KMAJ_TR ? (BN >> g.qlog2g) + 1 : 1;  // groups of a k row the tile touches
+  const int q_g0 = n0 >> g.qlog2g;                                  // the first of them
+  uint32_t dQ[QD ? QC_PW : 1], dS = OOB;
+  int dkQ[QD ? QC_PW : 1], dkS = 0;
+  __amdgpu_buffer_rsrc_t rsQk;
+  if constexpr (QD) {
+#pragma unroll
+    for (int i = 0; i < QC_PW; ++i) {
+      const int c = (wv + i * NWV) * 64 + lane;
+      if constexpr (BMODE == B_ROW) {
+        constexpr int CPRQ = BKE / QCW;  // chunks per W row per stage
+        const int n = c / CPRQ, kc = (c % CPRQ) * QCW;
+        dQ[i] = c < QCHUNKS ? (uint32_t)(n * q_rowbytes + kc * QB / 8) : OOB;
+        dkQ[i] = kc;
+      } else {
+        constexpr int CPRQ = BN / QCW;  // chunks per k row of the tile
+        const int kk = c / CPRQ, nc = (c % CPRQ) * QCW;
+        dQ[i] = c < QCHUNKS && n0 + nc < g.N ? (uint32_t)(kk * q_rowbytes + (int64_t)(n0 + nc) * QB / 8) : OOB;
+        dkQ[i] = kk;
+      }
+    }
+    if constexpr (BMODE == B_ROW) {
+      dS = 4 * lane < BN && n0 + 4 * lane < g.N ? (uint32_t)((n0 + 4 * lane) * 4) : OOB;
+    } else {
+      constexpr int LPG = BKE / 4;  // lanes per group
+      const int gg = lane / LPG, kq = lane % LPG;
+      dS = gg < q_ngk && q_g0 + gg < q_ldg ? (uint32_t)(((q_g0 + gg) * q_wrows + 4 * kq) * 4) : OOB;
+      dkS = 4 * kq;
+      rsQk = __builtin_amdgcn_make_buffer_rsrc((void *)g.B, (short)0, (int)(g.K * q_rowbytes), 0x00020000);
+    }
+  }
+
   constexpr int QW = QB == 4 ? 2 : 4;  // dwords of codes per piece
   uint32_t rqc[QB ? RD : 1][QW];
   float rqs[QB ? RD : 1], rqo[QB ? RD : 1];
@@ -528,19 +606,17 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
         const bool ok = k0 + qcol < g.K;
         rq = rsQ; rs = rsQs; ro = rsQo;
         vq = ok ? (uint32_t)(qrow * q_rowbytes + (int64_t)(k0 + qcol) * QB / 8) : OOB;
-        vs = ok ? (uint32_t)((qrow * q_ldg + ((k0 + qcol) >> g.qlog2g)) * 4) : OOB;
+        vs = ok && n0 + qrow < g.N ? (uint32_t)((((k0 + qcol) >> g.qlog2g) * q_wrows + n0 + qrow) * 4) : OOB;
       } else {
         // W rows k0 .. k0 + BKE - 1 (rows past K out of range), columns of the tile
         const int rows = krem > 0 ? min(krem, BKE) : 0;
         rq = __builtin_amdgcn_make_buffer_rsrc((void *)((const char *)g.B + k0 * q_rowbytes), (short)0,
                                                (int)(rows * q_rowbytes), 0x00020000);
-        rs = __builtin_amdgcn_make_buffer_rsrc((void *)(g.qscale + k0 * q_ldg), (short)0,
-                                               (int)(rows * q_ldg * 4), 0x00020000);
-        ro = __builtin_amdgcn_make_buffer_rsrc((void *)(g.qoffset + k0 * q_ldg), (short)0,
-                                               (int)(rows * q_ldg * 4), 0x00020000);
+        rs = rsQs;
+        ro = rsQo;
         const bool ok = n0 + qcol < g.N;
         vq = ok ? (uint32_t)(qrow * q_rowbytes + (int64_t)(n0 + qcol) * QB / 8) : OOB;
-        vs = ok ? (uint32_t)((qrow * q_ldg + ((n0 + qcol) >> g.qlog2g)) * 4) : OOB;
+        vs = ok && qrow < rows ? (uint32_t)((((n0 + qcol) >> g.qlog2g) * q_wrows + k0 + qrow) * 4) : OOB;
       }
       if constexpr (QB == 4) {
         const auto c = __builtin_amdgcn_raw_buffer_load_b64(rq, vq, 0, 0);
@@ -691,6 +767,8 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
         const uint32_t vo = dkA[i] < krem ? (lora ? dA2[i] : dA[i]) : (uint32_t)OOB;
         dma16(ra_rs, sA + (wv + i * NWV) * 1024, vo, soff);
       }
+      // (Quantized B: only the LoRA stages' B is loaded here, as bf16.)
+      if (QD && !lora) return;
       if constexpr (BMODE == B_ROW) {
         const __amdgpu_buffer_rsrc_t rb_rs = lora ? rsB2 : rsB;
 #pragma unroll
@@ -840,6 +918,156 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
       }
     }
   };
+  // ---- quantized direct-to-LDS stages (QD) --------------------------------------
+  auto qcode_slot = [&](auto S) -> char * { return smem + NBUF * DSTAGE + decltype(S)::value * QSLOT; };
+  // Scale / offset slot of quantized stage kt (k-major: the stage's ring
+  // slot S; row-major: its group's slot).
+  auto qso_slot = [&](auto S, int kt) -> char * {
+    const int slot = BMODE == B_ROW ? (stage_k0(kt) >> g.qlog2g) & 3 : decltype(S)::value;
+    return smem + NBUF * DSTAGE + 3 * QSLOT + slot * 2 * QSO;
+  };
+  // Whether this wave loads scales and offsets (two loads) for quantized
+  // stage kt: wave 0, for k-major B every stage, for row-major B the first
+  // stage of every group.
+  auto so_loads = [&](int kt) -> bool {
+    if constexpr (BMODE == B_ROW) {
+      const int k0 = stage_k0(kt);
+      return wv == 0 && !is_lora(kt) && k0 < g.K && (k0 & ((1 << g.qlog2g) - 1)) == 0;
+    } else {
+      return wv == 0;
+    }
+  };
+  // Those loads, into slot S; issued first in their step.
+  auto dma_so = [&](auto S, int kt) __attribute__((always_inline)) {
+    if constexpr (QD) {
+      if (so_loads(kt)) {
+        const int k0 = stage_k0(kt);
+        char *dst = qso_slot(S, kt);
+        int so;
+        uint32_t vo = dS;
+        if constexpr (BMODE == B_ROW) {
+          so = (k0 >> g.qlog2g) * q_wrows * 4;
+        } else {
+          const int krem = is_lora(kt) ? 0 : g.K - k0;
+          so = k0 * 4;
+          vo = dkS < krem ? dS : (uint32_t)OOB;
+        }
+        dma16(rsQs, dst, vo, so);
+        dma16(rsQo, dst + QSO, vo, so);
+      }
+    }
+  };
+  // Code load q (< QC_PW) of quantized stage kt into code slot S.  With MASK
+  // = 0 the stage is a full main stage; else lanes past K read zeros, and so
+  // does a LoRA stage (no codes).
+  auto dma_code = [&](auto S, int kt, auto QI, auto MASK) __attribute__((always_inline)) {
+    if constexpr (QD) {
+      constexpr int i = decltype(QI)::value;
+      const int k0 = stage_k0(kt);
+      const int krem = is_lora(kt) ? 0 : g.K - k0;
+      char *dst = qcode_slot(S) + (wv + i * NWV) * 1024;
+      const uint32_t vo = !decltype(MASK)::value || dkQ[i] < krem ? dQ[i] : (uint32_t)OOB;
+      if constexpr (BMODE == B_ROW)
+        dma16(rsQ, dst, vo, k0 * QB / 8);
+      else
+        dma16(rsQk, dst, vo, (int)((int64_t)k0 * q_rowbytes));
+    }
+  };
+  // Load q (< DA_PW) of main stage kt's A into ring buffer BUF.
+  auto dma_a_one = [&](auto BUF, int kt, auto QI, auto MASK) __attribute__((always_inline)) {
+    constexpr int q = decltype(QI)::value;
+    const int k0 = stage_k0(kt);
+    const uint32_t vo = !decltype(MASK)::value || dkA[q] < g.K - k0 ? dA[q] : (uint32_t)OOB;
+    dma16(rsA, ring_a(BUF) + (wv + q * NWV) * 1024, vo, k0 * ES);
+  };
+  // Dequantization of the stage in slot S into the B area of ring buffer BUF:
+  // w = scale * code + offset (one fp32 fma), rounded to bf16, in the layout
+  // the bf16 direct-to-LDS loads produce.  Thread t takes runs t, t + NT, ...
+  struct QRun {
+    uint32_t c[QB == 8 ? 4 : 2];
+    float s, o;
+  };
+  auto dq_read = [&](auto S, int kt, QRun(&q)[QRPT]) __attribute__((always_inline)) {
+    if constexpr (QD) {
+      const char *cs = qcode_slot(S);
+      const float *ss = (const float *)qso_slot(S, kt);
+#pragma unroll
+      for (int j = 0; j < QRPT; ++j) {
+        int rho = tid + j * NT;
+        if (QRUNS % NT) rho = rho < QRUNS ? rho : 0;
+        if constexpr (QB == 8) {
+          const u32x4 v = ld16(cs + rho * 16);
+#pragma unroll
+          for (int d = 0; d < 4; ++d) q[j].c[d] = v[d];
+        } else {
+          const uint2 v = *(const uint2 *)(cs + rho * 8);
+          q[j].c[0] = v.x;
+          q[j].c[1] = v.y;
+        }
+        int pr;
+        if constexpr (BMODE == B_ROW) {
+          pr = rho / (BKE / 16);  // tile row
+        } else {
+          const int kk = rho / (BN / 16), nr = rho % (BN / 16);
+          pr = (((n0 + nr * 16) >> g.qlog2g) - q_g0) * BKE + kk;
+        }
+        q[j].s = ss[pr];
+        q[j].o = ss[QSO / 4 + pr];
+      }
+    }
+  };
+  auto dq_write = [&](auto BUF, const QRun(&q)[QRPT]) __attribute__((always_inline)) {
+    if constexpr (QD) {
+      char *sB = ring_b(BUF);
+#pragma unroll
+      for (int j = 0; j < QRPT; ++j) {
+        const int rho = tid + j * NT;
+        if (QRUNS % NT == 0 || rho < QRUNS) {
+          // w = fma(scale, code, offset) per weight, rounded to bf16 in pairs.
+          // Each code byte converts with one v_cvt_f32_ubyteN: for 4-bit codes
+          // the low and the high nibbles are first spread to bytes of their
+          // own (an empty asm hides their known-zero bits, which would
+          // otherwise turn each conversion into a bit-field extract plus a
+          // conversion).
+          const float qs = q[j].s, qo = q[j].o;
+          uint32_t w[8];
+          if constexpr (QB == 4) {
+            // dword d: weights 8d .. 8d + 7, weight 8d + 2i in the low nibble of byte i
+#pragma unroll
+            for (int d = 0; d < 2; ++d) {
+              uint32_t lo = q[j].c[d] & 0x0F0F0F0Fu, hi = (q[j].c[d] >> 4) & 0x0F0F0F0Fu;
+              asm("" : "+v"(lo), "+v"(hi));
+#pragma unroll
+              for (int i = 0; i < 4; ++i)
+                w[4 * d + i] = pack_bf16x2(fmaf(qs, (float)((lo >> (8 * i)) & 0xFFu), qo),
+                                           fmaf(qs, (float)((hi >> (8 * i)) & 0xFFu), qo));
+            }
+          } else {
+#pragma unroll
+            for (int d = 0; d < 4; ++d)
+#pragma unroll
+              for (int i = 0; i < 2; ++i)
+                w[2 * d + i] = pack_bf16x2(fmaf(qs, (float)((q[j].c[d] >> (16 * i)) & 0xFFu), qo),
+                                           fmaf(qs, (float)((q[j].c[d] >> (16 * i + 8)) & 0xFFu), qo));
+          }
+          const u32x4 lo = u32x4{w[0], w[1], w[2], w[3]}, hi = u32x4{w[4], w[5], w[6], w[7]};
+          if constexpr (BMODE == B_ROW) {
+            // row n, 16-byte chunks 2 kr and 2 kr + 1, chunk c kept at c ^ swz(n)
+            const int n = rho / (BKE / 16), kr = rho % (BKE / 16);
+            const int swz = CPR == 8 ? (n & 7) ^ ((n >> 3) & 1) : (n >> 2) & 3;
+            st16(sB + n * BKB + ((2 * kr) ^ swz) * 16, lo);
+            st16(sB + n * BKB + ((2 * kr + 1) ^ swz) * 16, hi);
+          } else {
+            // k row kk, chunks 2 nr and 2 nr + 1, chunk c kept at c ^ 4 (kk & 3)
+            const int kk = rho / (BN / 16), nr = rho % (BN / 16);
+            const int swz = 4 * (kk & 3);
+            st16(sB + kk * DBRB + ((2 * nr) ^ swz) * 16, lo);
+            st16(sB + kk * DBRB + ((2 * nr + 1) ^ swz) * 16, hi);
+          }
+        }
+      }
+    }
+  };
   // D = Bop * Aop^T: D rows are output columns n, D columns are rows m, so each
   // lane ends up holding runs of 4 consecutive n of one output row.
   auto mma_frags = [&](const Frag &f) {
@@ -892,68 +1120,164 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
 #pragma unroll
       for (int s2 = 0; s2 < SPW; ++s2) mma_frags(f[s2]);
     };
-    // A fused launch's LoRA-step operands come from its producers: wait for
-    // them before the first load of a LoRA stage (here when the prologue
-    // already issues one, else in the step that does).
-    if (coh && nk_main < NBUF) fz_wait(fz.sync, fz.gen, fz.nprod, fz.ncons);
-    static_for<0, NBUF>([&](auto SI) { dma_stage(SI, decltype(SI)::value); });
-    {
-      constexpr int V = (NBUF - 1) * IPS;  // stage 0 landed
-      __builtin_amdgcn_s_waitcnt((V & 15) | ((V >> 4) << 14) | W_ENC);
-    }
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_sched_barrier(0);
-    read_stage_d(IC<0>(), F[0]);
-    auto step = [&](auto PH, int kt, auto MASK) __attribute__((always_inline)) {
-      constexpr int P = decltype(PH)::value;  // kt % UN
-      constexpr int V = (NBUF - 2) * IPS;     // stage kt + 1 landed
-      __builtin_amdgcn_s_waitcnt((V & 15) | ((V >> 4) << 14) | (7 << 4));  // and lgkmcnt(0)
+    if constexpr (QD) {
+      // Quantized B.  Step kt: wait for its loads of stage kt + 1 and of the
+      // codes of stage kt + NBUF (both issued two steps earlier), barrier,
+      // dequantize stage kt + NBUF into the B area of the buffer that stage
+      // kt vacated, issue the codes, scales and offsets of stage kt + NBUF + 2
+      // and the A loads of stage kt + NBUF, read the fragments of stage kt + 1
+      // and run the MFMAs of stage kt.  The LoRA stages come first (all
+      // within the prologue, as bf16).
+      constexpr int QL = QC_PW;  // counted loads of a stage's codes
+      constexpr int W_LGKM = 15 | (7 << 4) | (3 << 14);  // lgkmcnt(0) only
+      static_for<0, NBUF>([&](auto SI) {
+        dma_so(SI, decltype(SI)::value);
+        dma_stage(SI, decltype(SI)::value);
+        static_for<0, QL>([&](auto QI) { dma_code(SI, decltype(SI)::value, QI, IC<1>()); });
+      });
+      __builtin_amdgcn_s_waitcnt(0 | W_ENC);
       __builtin_amdgcn_s_barrier();
       __builtin_amdgcn_sched_barrier(0);
-      // A fused launch's LoRA stage holds its producers' output: wait for them
-      // before the step that issues its loads.
-      if (FUSE && coh && kt + NBUF == nk_main) fz_wait(fz.sync, fz.gen, fz.nprod, fz.ncons);
-      __builtin_amdgcn_sched_barrier(0);
-      // The loads of stage kt + NBUF are spread between the fragment reads of
-      // stage kt + 1 (in source order: an LDS read cannot pass the load
-      // assembly), so the load path, the LDS and the matrix cores work side by
-      // side instead of all loads queueing at the top of the step.
-      constexpr int NRO = SPW * (FM + FN);
-      static_for<0, NRO>([&](auto RI) {
-        constexpr int ri = decltype(RI)::value;
-        read_one_d(IC<(P + 1) % NBUF>(), RI, F[(P + 1) % 2]);
-        static_for<ri * IPS / NRO, (ri + 1) * IPS / NRO>(
-            [&](auto QI) { dma_one(IC<P % NBUF>(), kt + NBUF, QI, MASK); });
+      static_for<0, NBUF>([&](auto SI) {
+        if (decltype(SI)::value >= nk_lora) {
+          QRun q[QRPT];
+          dq_read(SI, decltype(SI)::value, q);
+          dq_write(SI, q);
+        }
       });
-      mma_stage(F[P % 2]);
-      constexpr int NM = SPW * FM * FN;
-      constexpr int NR = SPW * (FM + FN * (BMODE == B_KMAJ_TR ? 2 : 1));
-      static_for<0, NM>([&](auto MI) {
-        constexpr int m = decltype(MI)::value;
-        constexpr int r = (m + 1) * NR / NM - m * NR / NM;
-        if constexpr (r > 0) __builtin_amdgcn_sched_group_barrier(0x100, r, 0);  // DS read
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                       // MFMA
-      });
+      __builtin_amdgcn_s_waitcnt(W_LGKM);
+      __builtin_amdgcn_s_barrier();
       __builtin_amdgcn_sched_barrier(0);
-    };
-    // Steps whose loads fill a full main stage (stage kt + NBUF below the K
-    // tail) run unmasked; the K tail, the LoRA stages and the stages past the
-    // end (zeros) run masked.
-    // (Launches with producers, and the 256 x 128 tile with k-major B, keep
-    // one loop: the second copy of the steps costs them registers and spills.)
-    constexpr bool SPLIT = !FUSE && !(BM == 256 && BN == 128 && BMODE == B_KMAJ_TR);
-    const bool whole_ok = BMODE != B_KMAJ_TR || (int64_t)g.K * g.ldb * ES < (int64_t)1 << 31;
-    const int nb = QB || !whole_ok ? 0 : g.K / BKE - NBUF;
-    int kt = 0;
-    if constexpr (SPLIT)
+      static_for<0, 2>([&](auto SI) {
+        dma_so(SI, NBUF + decltype(SI)::value);
+        static_for<0, QL>([&](auto QI) { dma_code(SI, NBUF + decltype(SI)::value, QI, IC<1>()); });
+      });
+      __builtin_amdgcn_s_waitcnt((QL & 15) | ((QL >> 4) << 14) | W_ENC);  // stage NBUF's codes landed
+      __builtin_amdgcn_s_barrier();
+      __builtin_amdgcn_sched_barrier(0);
+      read_stage_d(IC<0>(), F[0]);
+      auto qstep = [&](auto PH, int kt, auto MASK) __attribute__((always_inline)) {
+        constexpr int P = decltype(PH)::value;  // kt % UN
+        // the loads of the last step (with its scale loads, if any) may be in flight
+        constexpr int V = QIPS, V2 = QIPS + 2;
+        if (so_loads(kt + NBUF + 1))
+          __builtin_amdgcn_s_waitcnt((V2 & 15) | ((V2 >> 4) << 14) | (7 << 4));  // and lgkmcnt(0)
+        else
+          __builtin_amdgcn_s_waitcnt((V & 15) | ((V >> 4) << 14) | (7 << 4));
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        QRun q[QRPT];
+        dq_read(IC<P % NBUF>(), kt + NBUF, q);
+        dma_so(IC<(P + 2) % NBUF>(), kt + NBUF + 2);
+        constexpr int NRO = SPW * (FM + FN);
+        static_for<0, NRO>([&](auto RI) {
+          constexpr int ri = decltype(RI)::value;
+          read_one_d(IC<(P + 1) % NBUF>(), RI, F[(P + 1) % 2]);
+          static_for<ri * QIPS / NRO, (ri + 1) * QIPS / NRO>([&](auto QI) {
+            constexpr int qi = decltype(QI)::value;
+            if constexpr (qi < QL)
+              dma_code(IC<(P + 2) % NBUF>(), kt + NBUF + 2, QI, MASK);
+            else
+              dma_a_one(IC<P % NBUF>(), kt + NBUF, IC<qi - QL>(), MASK);
+          });
+        });
+        dq_write(IC<P % NBUF>(), q);
+        mma_stage(F[P % 2]);
+        constexpr int NM = SPW * FM * FN;
+        constexpr int NR = SPW * (FM + FN * (BMODE == B_KMAJ_TR ? 2 : 1));
+        constexpr int NQR = QRPT * 3;                     // dequant LDS reads
+        constexpr int NQV = QRPT * (QB == 4 ? 46 : 40);   // dequant vector instructions (about)
+        constexpr int NQW = QRPT * 2;                     // dequant LDS writes
+        // The dequantization's LDS reads go first and its arithmetic starts
+        // two MFMAs later, so the first MFMAs do not wait for those reads.
+        constexpr int M0 = NM > 4 ? 2 : 1;
+        static_for<0, NM>([&](auto MI) {
+          constexpr int m = decltype(MI)::value;
+          constexpr int r = (m + 1) * NR / NM - m * NR / NM;
+          constexpr int v = m < M0 ? 0 : (m - M0 + 1) * NQV / (NM - M0) - (m - M0) * NQV / (NM - M0);
+          if constexpr (m == 0) __builtin_amdgcn_sched_group_barrier(0x100, NQR, 0);  // DS read
+          if constexpr (r > 0) __builtin_amdgcn_sched_group_barrier(0x100, r, 0);   // DS read
+          if constexpr (v > 0) __builtin_amdgcn_sched_group_barrier(0x002, v, 0);   // VALU
+          if constexpr (m >= NM - NQW) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // DS write
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                        // MFMA
+        });
+        __builtin_amdgcn_sched_barrier(0);
+      };
+      // Steps whose loads are all of full main stages run unmasked.
+      const int nb = nk_lora + g.K / BKE - NBUF - 2;
+      int kt = 0;
       for (; kt + UN <= nb; kt += UN)
-        static_for<0, UN>([&](auto PH) { step(PH, kt + decltype(PH)::value, IC<0>()); });
-    for (; kt + UN <= nk; kt += UN)
-      static_for<0, UN>([&](auto PH) { step(PH, kt + decltype(PH)::value, IC<1>()); });
-    static_for<0, UN - 1>([&](auto PH) {
-      constexpr int P = decltype(PH)::value;
-      if (kt + P < nk) step(PH, kt + P, IC<1>());
-    });
+        static_for<0, UN>([&](auto PH) { qstep(PH, kt + decltype(PH)::value, IC<0>()); });
+      for (; kt + UN <= nk; kt += UN)
+        static_for<0, UN>([&](auto PH) { qstep(PH, kt + decltype(PH)::value, IC<1>()); });
+      static_for<0, UN - 1>([&](auto PH) {
+        constexpr int P = decltype(PH)::value;
+        if (kt + P < nk) qstep(PH, kt + P, IC<1>());
+      });
+    } else {
+      // A fused launch's LoRA-step operands come from its producers: wait for
+      // them before the first load of a LoRA stage (here when the prologue
+      // already issues one, else in the step that does).
+      if (coh && nk_main < NBUF) fz_wait(fz.sync, fz.gen, fz.nprod, fz.ncons);
+      static_for<0, NBUF>([&](auto SI) { dma_stage(SI, decltype(SI)::value); });
+      {
+        constexpr int V = (NBUF - 1) * IPS;  // stage 0 landed
+        __builtin_amdgcn_s_waitcnt((V & 15) | ((V >> 4) << 14) | W_ENC);
+      }
+      __builtin_amdgcn_s_barrier();
+      __builtin_amdgcn_sched_barrier(0);
+      read_stage_d(IC<0>(), F[0]);
+      auto step = [&](auto PH, int kt, auto MASK) __attribute__((always_inline)) {
+        constexpr int P = decltype(PH)::value;  // kt % UN
+        constexpr int V = (NBUF - 2) * IPS;     // stage kt + 1 landed
+        __builtin_amdgcn_s_waitcnt((V & 15) | ((V >> 4) << 14) | (7 << 4));  // and lgkmcnt(0)
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        // A fused launch's LoRA stage holds its producers' output: wait for them
+        // before the step that issues its loads.
+        if (FUSE && coh && kt + NBUF == nk_main) fz_wait(fz.sync, fz.gen, fz.nprod, fz.ncons);
+        __builtin_amdgcn_sched_barrier(0);
+        // The loads of stage kt + NBUF are spread between the fragment reads of
+        // stage kt + 1 (in source order: an LDS read cannot pass the load
+        // assembly), so the load path, the LDS and the matrix cores work side by
+        // side instead of all loads queueing at the top of the step.
+        constexpr int NRO = SPW * (FM + FN);
+        static_for<0, NRO>([&](auto RI) {
+          constexpr int ri = decltype(RI)::value;
+          read_one_d(IC<(P + 1) % NBUF>(), RI, F[(P + 1) % 2]);
+          static_for<ri * IPS / NRO, (ri + 1) * IPS / NRO>(
+              [&](auto QI) { dma_one(IC<P % NBUF>(), kt + NBUF, QI, MASK); });
+        });
+        mma_stage(F[P % 2]);
+        constexpr int NM = SPW * FM * FN;
+        constexpr int NR = SPW * (FM + FN * (BMODE == B_KMAJ_TR ? 2 : 1));
+        static_for<0, NM>([&](auto MI) {
+          constexpr int m = decltype(MI)::value;
+          constexpr int r = (m + 1) * NR / NM - m * NR / NM;
+          if constexpr (r > 0) __builtin_amdgcn_sched_group_barrier(0x100, r, 0);  // DS read
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                       // MFMA
+        });
+        __builtin_amdgcn_sched_barrier(0);
+      };
+      // Steps whose loads fill a full main stage (stage kt + NBUF below the K
+      // tail) run unmasked; the K tail, the LoRA stages and the stages past the
+      // end (zeros) run masked.
+      // (Launches with producers, and the 256 x 128 tile with k-major B, keep
+      // one loop: the second copy of the steps costs them registers and spills.)
+      constexpr bool SPLIT = !FUSE && !(BM == 256 && BN == 128 && BMODE == B_KMAJ_TR);
+      const bool whole_ok = BMODE != B_KMAJ_TR || (int64_t)g.K * g.ldb * ES < (int64_t)1 << 31;
+      const int nb = QB || !whole_ok ? 0 : g.K / BKE - NBUF;
+      int kt = 0;
+      if constexpr (SPLIT)
+        for (; kt + UN <= nb; kt += UN)
+          static_for<0, UN>([&](auto PH) { step(PH, kt + decltype(PH)::value, IC<0>()); });
+      for (; kt + UN <= nk; kt += UN)
+        static_for<0, UN>([&](auto PH) { step(PH, kt + decltype(PH)::value, IC<1>()); });
+      static_for<0, UN - 1>([&](auto PH) {
+        constexpr int P = decltype(PH)::value;
+        if (kt + P < nk) step(PH, kt + P, IC<1>());
+      });
+    }
     // The loads of the stages past the end still write LDS: drain them before
     // the buffers are reused.
     __builtin_amdgcn_s_waitcnt(0 | W_ENC);
@@ -1523,8 +1847,48 @@ hipError_t launch_gemm_epi(const GemmArgs &g, int epi, hipStream_t st) {
   return hipErrorInvalidValue;
 }
 
+// Dequantizing direct-to-LDS tiles (the shapes of the bf16 path; 256 x 128
+// and 128 x 64 choices run 128 x 128 tiles).
+template <int QB>
+static hipError_t launch_q_dma(const GemmArgs &g, int shape, bool kmaj, const SideArgs *side, hipStream_t st) {
+  if (kmaj) {
+    switch (shape) {
+      case 2:
+        return launch_cfg<BF16, 256, 256, 2, 2, 1, B_KMAJ_TR, 64, 3, 3, 2, QB, EPI_STORE, 1>(g, side, st);
+      case 4:
+        return launch_cfg<BF16, 256, 192, 2, 2, 1, B_KMAJ_TR, 64, 3, 3, 2, QB, EPI_STORE, 1>(g, side, st);
+      default:
+        return launch_cfg<BF16, 128, 128, 2, 2, 2, B_KMAJ_TR, 128, 3, 3, 2, QB, EPI_STORE, 1>(g, side, st);
+    }
+  }
+  switch (shape) {
+    case 2:
+      return launch_cfg<BF16, 256, 256, 2, 2, 1, B_ROW, 64, 3, 3, 2, QB, EPI_STORE, 1>(g, side, st);
+    case 4:
+      return launch_cfg<BF16, 256, 192, 2, 2, 1, B_ROW, 64, 3, 3, 2, QB, EPI_STORE, 1>(g, side, st);
+    default:
+      return launch_cfg<BF16, 128, 128, 2, 2, 2, B_ROW, 128, 3, 3, 2, QB, EPI_STORE, 1>(g, side, st);
+  }
+}
+
+bool gemm_q_direct(const GemmArgs &g, int bits, bool b_kmajor, bool with_side) {
+  // Groups of at least 64 weights (a row-major stage then holds one group per
+  // row), the LoRA stages within the first three, and the scales (and, for
+  // k-major B, the codes of all K rows) within 32-bit offsets.
+  const int shape = pick_shape(g.M, g.N, b_kmajor, with_side);
+  const int bke = shape == 2 || shape == 4 ? 32 : 64;
+  const int64_t rowbytes = g.ldb * bits / 8, ldg = g.ldb >> g.qlog2g;
+  const int64_t wrows = b_kmajor ? g.K : g.N;
+  return (bits == 4 || bits == 8) && g.qlog2g >= 6 && g.r <= 3 * bke && wrows * ldg * 4 < (int64_t(1) << 31) &&
+         (!b_kmajor || (int64_t)g.K * rowbytes < (int64_t(1) << 31));
+}
+
 hipError_t launch_gemm_q(const GemmArgs &g, int bits, bool b_kmajor, const SideArgs *side,
                          hipStream_t st) {
+  if (gemm_q_direct(g, bits, b_kmajor, side != nullptr)) {
+    const int shape = pick_shape(g.M, g.N, b_kmajor, side != nullptr);
+    return bits == 4 ? launch_q_dma<4>(g, shape, b_kmajor, side, st) : launch_q_dma<8>(g, shape, b_kmajor, side, st);
+  }
   if (bits == 4)
     return b_kmajor ? launch_cfg<BF16, 128, 128, 2, 2, 2, B_KMAJ_TR, 128, 2, 3, 2, 4>(g, side, st)
                     : launch_cfg<BF16, 128, 128, 2, 2, 2, B_ROW, 128, 2, 3, 2, 4>(g, side, st);

@@ -77,6 +77,12 @@ __device__ __forceinline__ u32x4 pack_vec(BF16, const float *f) {
     r[d] = (uint32_t)BF16::from_float(f[2 * d]) | ((uint32_t)BF16::from_float(f[2 * d + 1]) << 16);
   return r;
 }
+// Two floats to a bf16 pair (round to nearest even) in one v_cvt_pk_bf16_f32.
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  typedef float f32x2_t __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
+}
 __device__ __forceinline__ u32x4 pack_vec(F32, const float *f) {
   u32x4 r;
 #pragma unroll
@@ -125,6 +131,15 @@ __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, char *lds, uint
                                       int soffset) {
   const uint32_t base = (uint32_t)(uintptr_t)(lds_void *)lds;
   asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds" ::"s"(base),
+               "v"(voffset),
+               "s"(rs), "s"(soffset)
+               : "memory", "m0");
+}
+// The 4-byte form: 4 bytes per lane into lds + 4 * lane.
+__device__ __forceinline__ void dma4(__amdgpu_buffer_rsrc_t rs, char *lds, uint32_t voffset,
+                                     int soffset) {
+  const uint32_t base = (uint32_t)(uintptr_t)(lds_void *)lds;
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, %3 offen lds" ::"s"(base),
                "v"(voffset),
                "s"(rs), "s"(soffset)
                : "memory", "m0");

@@ -67,7 +67,9 @@ struct GemmArgs {
   // Quantized B (launch_gemm_q): B holds unsigned codes of W ([rows][ldb]
   // weights, bits/8 bytes each, two 4-bit codes per byte with the even weight
   // in the low nibble), w = qscale * code + qoffset with one scale and offset
-  // per group of 2^qlog2g consecutive weights of a W row ([rows][ldb >> qlog2g]).
+  // per group of 2^qlog2g consecutive weights of a W row, group-major:
+  // [ldb >> qlog2g][rows] (the scales of one group for consecutive rows are
+  // contiguous).
   const float *qscale;
   const float *qoffset;
   int qlog2g;
@@ -159,6 +161,8 @@ hipError_t launch_gemm(const GemmArgs &g, Dtype dt, bool b_kmajor, const SideArg
                        hipStream_t st);
 // bf16 GEMM whose B is the quantized frozen weight (bits = 4 or 8), dequantized
 // into LDS; the LoRA step (r <= 64) runs first.
+// Whether launch_gemm_q runs the dequantizing direct-to-LDS tiles for g.
+bool gemm_q_direct(const GemmArgs &g, int bits, bool b_kmajor, bool with_side);
 hipError_t launch_gemm_q(const GemmArgs &g, int bits, bool b_kmajor, const SideArgs *side,
                          hipStream_t st);
 

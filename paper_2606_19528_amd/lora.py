@@ -228,11 +228,11 @@ def frozen_linear_bwd_dx(dy, W, dx, ws=None, stream=None):
 def _qw(Wq):
     """(codes, scale, offset, bits, group, d_out, d_in) of a quantized weight given
     as a dict with keys codes (uint8 [d_out, d_in*bits/8]), scale and offset
-    (fp32 [d_out, d_in/group]) and bits."""
+    (fp32 [d_in/group, d_out], group-major) and bits."""
     codes, sc, off, bits = Wq["codes"], Wq["scale"], Wq["offset"], int(Wq["bits"])
     d_out = codes.shape[0]
     d_in = codes.shape[1] * 8 // bits
-    group = d_in // sc.shape[1]
+    group = d_in // sc.shape[0]
     return codes, sc, off, bits, group, d_out, d_in
 
 

@@ -21,7 +21,8 @@ def _announce(msg):
 
 
 def _dequant(orc, Wq, group):
-    return torch.from_numpy(orc.dequant(Wq["codes"], Wq["scale"], Wq["offset"], Wq["bits"], group))
+    # the library takes scales and offsets group-major, the oracle per row
+    return torch.from_numpy(orc.dequant(Wq["codes"], Wq["scale"].t(), Wq["offset"].t(), Wq["bits"], group))
 
 
 def _qcase(orc, T, K, N, r, bits, group, seed, recompute=False, rows=None, s=2.0):
@@ -65,8 +66,25 @@ def test_quant_zero_weight_isolates_lora(orc):
     compare(gpu, ref, torch.bfloat16, label="quant W=0")
 
 
+# Groups of 64 weights or more run the dequantizing direct-to-LDS tiles (codes,
+# scales and offsets loaded into LDS, dequantized there); the tile shape is the
+# bf16 path's choice for the same product.  Cases: the 256 x 192 forward with
+# ragged rows and columns and the 256 x 256 dx (side items, a reduction tail);
+# the 256 x 256 forward and 128 x 128 dx in INT8 with groups of 64; 128 x 128
+# both ways with groups of 256; the 28-layer stack's gate shape in INT4.
+@pytest.mark.parametrize("shape", [
+    (4000, 3072, 3000, 16, 4, 128), (2304, 2048, 6144, 16, 8, 64), (1000, 1536, 1032, 8, 4, 256),
+    (4096, 3072, 8192, 32, 4, 128),
+])
+def test_quant_direct_tiles(orc, shape):
+    T, K, N, r, bits, group = shape
+    rows = list(range(0, T, 97)) + [T - 1]
+    _qcase(orc, T, K, N, r, bits, group, seed=T + N + bits, rows=rows)
+
+
 @pytest.mark.parametrize("shape", [(129, 256, 392, 8, 128), (64, 3072, 1000, 8, 128),
-                                   (33, 1024, 136, 4, 16)])
+                                   (33, 1024, 136, 4, 16), (4000, 3072, 3000, 8, 128),
+                                   (2048, 8192, 3000, 8, 64), (1024, 3072, 8192, 4, 128)])
 def test_quant_frozen_dx(orc, shape):
     T, K, N, bits, group = shape
     _announce(f"quant frozen dx T={T} K={K} N={N} bits={bits} group={group}")
@@ -77,8 +95,9 @@ def test_quant_frozen_dx(orc, shape):
     lm.frozen_linear_bwd_dx_q(dy.cuda(), {k: (v.cuda() if hasattr(v, "cuda") else v)
                                           for k, v in Wq.items()}, dx)
     torch.cuda.synchronize()
-    ref = orc.frozen_dx(dy, _dequant(orc, Wq, group))
-    assert relerr(dx.cpu().double().numpy(), ref) <= TOL[torch.bfloat16]
+    rows = list(range(0, T, 61)) + [T - 1] if T > 256 else list(range(T))
+    ref = orc.frozen_dx(dy[rows], _dequant(orc, Wq, group))
+    assert relerr(dx.cpu()[rows].double().numpy(), ref) <= TOL[torch.bfloat16]
 
 
 def test_quant_deterministic(orc):

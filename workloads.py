@@ -153,7 +153,9 @@ def quant_weight(d_out: int, d_in: int, bits: int = 4, group: int = 128, seed: i
     ~ 0.02 * sqrt(12) / 2^bits * U(0.5, 1.5) and an fp32 offset centring the
     codes' range near zero, so that the weights spread like the N(0, 0.02)
     bf16 weights of lora_inputs.  Drawn in that order (codes, scale factor,
-    offset jitter) from one seeded generator."""
+    offset jitter; scales and offsets row by row) from one seeded generator.
+    scale and offset are stored group-major, [d_in / group][d_out] (their
+    transposes are the [row][group] arrays the oracle's dequant takes)."""
     g = _gen(seed, device)
     levels = 1 << bits
     q = torch.randint(0, levels, (d_out, d_in), generator=g, device=device, dtype=torch.int32)
@@ -166,8 +168,8 @@ def quant_weight(d_out: int, d_in: int, bits: int = 4, group: int = 128, seed: i
     scale = step * (0.5 + torch.rand(d_out, ng, generator=g, device=device))
     jitter = 0.25 * (torch.rand(d_out, ng, generator=g, device=device) - 0.5)
     offset = -scale * ((levels - 1) / 2.0 + jitter)
-    return {"codes": codes.contiguous(), "scale": scale.float().contiguous(),
-            "offset": offset.float().contiguous(), "bits": bits}
+    return {"codes": codes.contiguous(), "scale": scale.float().t().contiguous(),
+            "offset": offset.float().t().contiguous(), "bits": bits}
 
 
 def head_inputs(T: int, V: int, D: int, ktab: int, trainable: float = 0.3, clusters: int = 64,
