@@ -137,8 +137,9 @@ lora_status_t check_shapes(int64_t T, int64_t d_in, int64_t d_out, int64_t r, lo
 // needs no partial sums and no padded copy of B (A), and the workspace starts
 // with the hand-over words of the launch.  In the backward the producers then
 // run the dA / dB side items, so those take no CUs of their own.
-bool fuse_ok(int64_t T, int64_t N, int64_t r, lora_dtype_t dt, bool b_kmajor = false) {
-  return dt == LORA_BF16 && r >= 8 && r <= 32 && r % 8 == 0 && gemm_fusable((int)T, (int)N, b_kmajor);
+// (N, K: the GEMM's output columns and reduction length.)
+bool fuse_ok(int64_t T, int64_t N, int64_t K, int64_t r, lora_dtype_t dt, bool b_kmajor = false) {
+  return dt == LORA_BF16 && r >= 8 && r <= 32 && r % 8 == 0 && gemm_fusable((int)T, (int)N, (int)K, b_kmajor);
 }
 // Tag of a fused launch: distinct for every call of this process, never 0.
 unsigned int next_gen() {
@@ -169,7 +170,7 @@ FwdLayout fwd_layout(int64_t T, int64_t K, int64_t N, int64_t r, lora_dtype_t dt
   FwdLayout L{};
   if (r == 0) return L;
   const Dtype d = dt == LORA_BF16 ? DT_BF16 : DT_F32;
-  L.fused = fuse_ok(T, N, r, dt);
+  L.fused = fuse_ok(T, N, K, r, dt);
   if (L.fused) {
     L.sp = whole_rows(K, d);
     L.ldt = tail_ld((int)r, d);
@@ -208,8 +209,8 @@ BwdLayout bwd_layout(int64_t T, int64_t K, int64_t N, int64_t r, lora_dtype_t dt
   const Dtype d = dt == LORA_BF16 ? DT_BF16 : DT_F32;
   // A recomputed u is summed exactly as the forward pass summed it (whole
   // rows when the forward runs fused), so it is bitwise the saved one.
-  L.sp_u = fuse_ok(T, N, r, dt) ? whole_rows(K, d) : row_split(T, K, (int)r, d);
-  L.fused = fuse_ok(T, K, r, dt, true);
+  L.sp_u = fuse_ok(T, N, K, r, dt) ? whole_rows(K, d) : row_split(T, K, (int)r, d);
+  L.fused = fuse_ok(T, K, N, r, dt, true);
   L.sp_du = L.fused ? whole_rows(N, d) : row_split(T, N, (int)r, d);
   L.ldt = tail_ld(L.sp_du.nsplit * (int)r, d);
   size_t off = 0;

@@ -243,9 +243,15 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
   static_assert(!FUSE || (QB == 0 && EPI == EPI_STORE && ES == 2 && (BMODE == B_ROW || BMODE == B_KMAJ_TR)),
                 "producers: bf16 direct-to-LDS tiles that store C");
   constexpr int PV = BMODE == B_ROW ? V_ROW : V_KMAJ_TR;
-  constexpr int PROD = FUSE ? cmax(cmax(row_lds_bytes<E, 1, PV, 4, 1>(), row_lds_bytes<E, 2, PV, 4, 1>()),
-                                   cmax(row_lds_bytes<E, 1, PV, 4, 2>(), row_lds_bytes<E, 2, PV, 4, 2>()))
-                            : 0;
+  // (Only the 256 x 256 tiles, which leave 64 CUs to the producers at 4096
+  // rows, need producers of 64 rows.)
+  constexpr bool PROD4 = FUSE && BM == 256 && BN == 256;
+  constexpr int PNW = NT / 64;  // the producers' waves: the tile's
+  constexpr int PROD =
+      FUSE ? cmax(cmax(cmax(row_lds_bytes<E, 1, PV, 4, 1, PNW>(), row_lds_bytes<E, 2, PV, 4, 1, PNW>()),
+                       cmax(row_lds_bytes<E, 1, PV, 4, 2, PNW>(), row_lds_bytes<E, 2, PV, 4, 2, PNW>())),
+                  PROD4 ? cmax(row_lds_bytes<E, 1, PV, 4, 4, PNW>(), row_lds_bytes<E, 2, PV, 4, 4, PNW>()) : 0)
+           : 0;
   constexpr int LDS1 = LDS0 > SIDE ? LDS0 : SIDE;
   constexpr int LDS = LDS1 > PROD ? LDS1 : PROD;
   constexpr uint32_t OOB = 0x80000000u;      // offset past every buffer: loads return 0
@@ -302,14 +308,16 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
         // Coherent stores, complete in every wave before the count: no L2
         // write-back (which would stall every tile of the XCD) is needed.
         auto prod = [&](auto JB, auto MB) {
-          row_item<E, decltype(JB)::value, PV, 4, decltype(MB)::value, true>(fz.row, blockIdx.x, 0, fz.nprod, 1,
+          row_item<E, decltype(JB)::value, PV, 4, decltype(MB)::value, true, NT / 64>(fz.row, blockIdx.x, 0, fz.nprod, 1,
                                                                              smem);
         };
         if (fz.row.r <= 16) {
-          if (fz.row.mb == 2) prod(IC<1>(), IC<2>());
+          if (PROD4 && fz.row.mb == 4) prod(IC<1>(), IC<PROD4 ? 4 : 1>());
+          else if (fz.row.mb == 2) prod(IC<1>(), IC<2>());
           else prod(IC<1>(), IC<1>());
         } else {
-          if (fz.row.mb == 2) prod(IC<2>(), IC<2>());
+          if (PROD4 && fz.row.mb == 4) prod(IC<2>(), IC<PROD4 ? 4 : 1>());
+          else if (fz.row.mb == 2) prod(IC<2>(), IC<2>());
           else prod(IC<2>(), IC<1>());
         }
         __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
@@ -1769,10 +1777,11 @@ static hipError_t launch_cfg(const GemmArgs &g, const SideArgs *side, hipStream_
     // Side items of a fused launch run on the producer workgroups.
     nside = 0;
     // 16 rows per producer while they fit beside the tiles on the 256 CUs (a
-    // tile needs the producers' rows only in its last steps), else 32.
+    // tile needs the producers' rows only in its last steps), else 32, else
+    // (256 x 256 tiles) 64.
     const int free = 256 - tm * tn;
     const int64_t T = fz->row.M;
-    const int mb = ((T + 15) / 16 + 7) / 8 * 8 <= free ? 1 : 2;
+    const int mb = ((T + 15) / 16 + 7) / 8 * 8 <= free ? 1 : ((T + 31) / 32 + 7) / 8 * 8 <= free || BM * BN != 65536 ? 2 : 4;
     fz->row.mb = mb;
     fz->nprod = (int)((T + 16 * mb - 1) / (16 * mb));
     fz->ncons = fz->hold ? 0 : tm * tn;  // consumers: the tiles (0: every wait gives up)
@@ -1899,10 +1908,19 @@ hipError_t launch_gemm_q(const GemmArgs &g, int bits, bool b_kmajor, const SideA
 }
 
 // Producers only pay off on CUs the tiles leave idle: fused when the tile
-// shape is direct-to-LDS and 32-row producers fit beside the tiles.
-bool gemm_fusable(int M, int N, bool b_kmajor) {
+// shape is direct-to-LDS and 32-row producers fit beside the tiles; beside
+// the backward's 256 x 256 tiles (e.g. 64 producers of 64 rows beside 192
+// tiles at 4096 rows) only over reductions of 2048 or more, where the tiles
+// outlast the producers and the side items that follow them on the same
+// CUs (over 1024 the fused launch measured 59 us against 47 + 6 us for the
+// two launches, over 3072 78 against 74 + 10, over 8192 188 against 183 + 19).
+bool gemm_fusable(int M, int N, int K, bool b_kmajor) {
   const int cfg = pick_shape(M, N, b_kmajor, b_kmajor);
-  if (cfg == 2 || cfg == 4) return false;
+  if (cfg == 4 || (cfg == 2 && !b_kmajor)) return false;
+  if (cfg == 2) {  // the backward's 256 x 256 tiles, with producers of up to 64 rows
+    const long tiles = (long)((M + 255) / 256) * ((N + 255) / 256);
+    return K >= 2048 && tiles + ((M + 63) / 64 + 7) / 8 * 8 <= 256;
+  }
   const long bm = cfg == 1 ? 256 : 128, bn = cfg == 3 ? 64 : 128;
   const long tiles = ((M + bm - 1) / bm) * ((N + bn - 1) / bn);
   return tiles + ((M + 31) / 32 + 7) / 8 * 8 <= 256;
@@ -1916,6 +1934,8 @@ hipError_t launch_gemm_fused(const GemmArgs &g, FuseArgs *fz, const SideArgs *si
     return hipErrorInvalidValue;
   if (kmaj) {
     switch (pick_shape(g.M, g.N, true, true)) {
+      case 2:
+        return launch_cfg<BF16, 256, 256, 2, 2, 1, B_KMAJ_TR, 64, 3, 3, 2, 0, EPI_STORE, 2>(g, side, st, fz);
       case 1:
         return launch_cfg<BF16, 256, 128, 4, 2, 1, B_KMAJ_TR, 128, 3, 3, 2, 0, EPI_STORE, 2>(g, side, st, fz);
       case 0:

@@ -267,10 +267,11 @@ struct FuseArgs {
 // that gave up.  Synchronous.
 hipError_t handover_giveups(unsigned *count, bool reset);
 
-// Whether the bf16 GEMM of this shape (forward: row-major B; backward:
-// k-major B, carrying the dA / dB side items) runs a tile configuration that
-// takes producer workgroups, and leaves the CUs for them.
-bool gemm_fusable(int M, int N, bool b_kmajor);
+// Whether the bf16 GEMM of this shape (M x N, reduction K; forward:
+// row-major B; backward: k-major B, carrying the dA / dB side items) runs a
+// tile configuration that takes producer workgroups, and leaves the CUs for
+// them.
+bool gemm_fusable(int M, int N, int K, bool b_kmajor);
 // The bf16 GEMM with producers at the front (fz->nprod > 0; chooses
 // fz->row.mb and sets fz->nprod, fz->nwg and fz->ncons).  fz->row.vmode
 // selects the forward (V_ROW, side must be null) or the backward (V_KMAJ_TR,

@@ -53,24 +53,27 @@ constexpr int row_stage_bytes() { return (16 * MB + 16 * JB) * ROW_KS * 2; }
 template <int JB, int MB>
 constexpr int row_nbuf() { return row_stage_bytes<JB, MB>() <= 32768 ? 4 : 3; }
 
-// LDS bytes of one item.
-template <class E, int JB, int VMODE, int U, int MB>
+// LDS bytes of one item (NW waves).
+template <class E, int JB, int VMODE, int U, int MB, int NW = ROW_NW>
 constexpr int row_lds_bytes() {
   constexpr int CE = 128 / (int)sizeof(typename E::T);
   constexpr int REGION = U * CE * JB * 16 * 2;
-  constexpr int RED = ROW_NW * 16 * MB * (JB * 16 + 1) * 4;
+  constexpr int RED = NW * 16 * MB * (JB * 16 + 1) * 4;
   if constexpr (row_streamed<E, JB, VMODE>()) {
     constexpr int RING = row_nbuf<JB, MB>() * row_stage_bytes<JB, MB>();
     return RING > RED ? RING : RED;
   }
-  return (VMODE == V_KMAJ_TR && ROW_NW * REGION > RED) ? ROW_NW * REGION : RED;
+  return (VMODE == V_KMAJ_TR && NW * REGION > RED) ? NW * REGION : RED;
 }
 
 // COH: the outputs (out, tail) are stored coherently at device scope (sc1):
 // a consumer in another XCD reads them while the launch still runs.
-template <class E, int JB, int VMODE, int U, int MB, bool COH = false>
+// NW: waves of the workgroup, 8 or (streamed form only) 4; four waves take
+// two k-slices of every stage each.
+template <class E, int JB, int VMODE, int U, int MB, bool COH = false, int NW = ROW_NW>
 __device__ __forceinline__ void row_item(const RowArgs &a, int bx, int by, int gx, int gy, char *smem) {
-  constexpr int NW = ROW_NW, NT = 64 * NW;
+  constexpr int NT = 64 * NW;
+  static_assert(NW == 8 || (NW == 4 && row_streamed<E, JB, VMODE>()), "eight waves, or four streaming");
   typedef typename E::T T;
   constexpr int VEC = E::VEC;
   constexpr int CE = 128 / (int)sizeof(T);  // elements per 128-byte chunk
@@ -143,7 +146,8 @@ __device__ __forceinline__ void row_item(const RowArgs &a, int bx, int by, int g
     constexpr int KS = ROW_KS, PB = KS * 2;
     constexpr int XB = 16 * MB * PB;
     constexpr int STAGE = row_stage_bytes<JB, MB>(), NBUF = row_nbuf<JB, MB>();
-    constexpr int LPW = MB + JB;  // loads per wave per stage
+    constexpr int F = ROW_NW / NW;     // k-slices per wave per stage
+    constexpr int LPW = F * (MB + JB);  // loads per wave per stage
     constexpr uint32_t OOB = 0x80000000u;
     const int wv = __builtin_amdgcn_readfirstlane(wave);
     const int klen = k_hi - k_lo, nst = (klen + KS - 1) / KS;
@@ -160,19 +164,19 @@ __device__ __forceinline__ void row_item(const RowArgs &a, int bx, int by, int g
     const __amdgpu_buffer_rsrc_t rsX = rsrc(Xp + (int64_t)m0 * a.ldx + k_lo, (int64_t)nrows * a.ldx * 2);
     const __amdgpu_buffer_rsrc_t rsV = VMODE == V_ROW ? rsrc(Vp + k_lo, (int64_t)r * a.ldv * 2)
                                                       : rsrc(Vp + (int64_t)k_lo * r, (int64_t)klen * r * 2);
-    // Load q of this wave covers stage bytes [1024 (wv + 8 q), + 1024): the
-    // item's rows for q < MB, V after.  kq: k (within a stage) of the lane's
-    // first element, or its k-row for k-major V.
+    // Load q of this wave covers 1 KB piece ii = wv + NW q' of the stage's
+    // rows (q < F MB, q' = q) or of V (after them, q' = q - F MB).  kq: k
+    // (within a stage) of the lane's first element, or its k-row for k-major V.
     uint32_t offq[LPW];
     int kq[LPW];
 #pragma unroll
     for (int q = 0; q < LPW; ++q) {
-      const int ii = wv + 8 * (q < MB ? q : q - MB);
-      if (q < MB || VMODE == V_ROW) {
+      const int ii = wv + NW * (q < F * MB ? q : q - F * MB);
+      if (q < F * MB || VMODE == V_ROW) {
         const int rr = 2 * ii + (lane >> 5);
         const int c = (lane & 31) ^ (rr & 15);
         kq[q] = c * 8;
-        offq[q] = (uint32_t)(rr * (q < MB ? a.ldx : a.ldv) * 2 + c * 16);
+        offq[q] = (uint32_t)(rr * (q < F * MB ? a.ldx : a.ldv) * 2 + c * 16);
       } else {
         const int byte = ii * 1024 + lane * 16;
         kq[q] = byte / (2 * r) < KS ? byte / (2 * r) : KS + klen;  // past the block: never loaded
@@ -185,13 +189,12 @@ __device__ __forceinline__ void row_item(const RowArgs &a, int bx, int by, int g
 #pragma unroll
       for (int q = 0; q < LPW; ++q) {
         const uint32_t vo = k0 + kq[q] < klen ? offq[q] : OOB;
-        if (q < MB) dma16(rsX, buf + (wv + 8 * q) * 1024, vo, k0 * 2);
-        else dma16(rsV, buf + XB + (wv + 8 * (q - MB)) * 1024, vo, VMODE == V_ROW ? k0 * 2 : k0 * r * 2);
+        if (q < F * MB) dma16(rsX, buf + (wv + NW * q) * 1024, vo, k0 * 2);
+        else dma16(rsV, buf + XB + (wv + NW * (q - F * MB)) * 1024, vo, VMODE == V_ROW ? k0 * 2 : k0 * r * 2);
       }
     };
 #pragma unroll
     for (int st = 0; st < NBUF - 1; ++st) issue(st);
-    const int pos = (4 * wv + (lane >> 4)) ^ (lane & 15);  // k-slice wv of a stage
     for (int s = 0; s < nst; ++s) {
       constexpr int V = (NBUF - 2) * LPW;  // this wave's loads of stage s landed, LDS reads done
       __builtin_amdgcn_s_waitcnt((V & 15) | ((V >> 4) << 14) | (7 << 4));
@@ -199,27 +202,32 @@ __device__ __forceinline__ void row_item(const RowArgs &a, int bx, int by, int g
       __builtin_amdgcn_sched_barrier(0);
       issue(s + NBUF - 1);  // into the buffer of stage s - 1, which nobody reads any more
       const char *buf = smem + (s % NBUF) * STAGE;
-      u32x4 xa[MB], vb[JB];
 #pragma unroll
-      for (int mt = 0; mt < MB; ++mt) xa[mt] = ld16(buf + (mt * 16 + (lane & 15)) * PB + pos * 16);
+      for (int h = 0; h < F; ++h) {
+        const int w = wv + NW * h;                                // k-slice of the stage
+        const int pos = (4 * w + (lane >> 4)) ^ (lane & 15);
+        u32x4 xa[MB], vb[JB];
 #pragma unroll
-      for (int jb = 0; jb < JB; ++jb) {
-        if constexpr (VMODE == V_ROW) {
-          vb[jb] = ld16(buf + XB + (jb * 16 + (lane & 15)) * PB + pos * 16);
-        } else {
-          // four consecutive k of one column per lane (as in the other form)
-          const int iq = lane & 15;
-          const char *pp = buf + XB + (32 * wv + 8 * g + (iq >> 2)) * (2 * r) + (jb * 16 + 4 * (iq & 3)) * 2;
-          rp_i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((rp_lds_i16x4 *)pp);
-          rp_i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((rp_lds_i16x4 *)(pp + 4 * (2 * r)));
-          vb[jb] = u32x4{__builtin_bit_cast(uint2, lo).x, __builtin_bit_cast(uint2, lo).y,
-                         __builtin_bit_cast(uint2, hi).x, __builtin_bit_cast(uint2, hi).y};
+        for (int mt = 0; mt < MB; ++mt) xa[mt] = ld16(buf + (mt * 16 + (lane & 15)) * PB + pos * 16);
+#pragma unroll
+        for (int jb = 0; jb < JB; ++jb) {
+          if constexpr (VMODE == V_ROW) {
+            vb[jb] = ld16(buf + XB + (jb * 16 + (lane & 15)) * PB + pos * 16);
+          } else {
+            // four consecutive k of one column per lane (as in the other form)
+            const int iq = lane & 15;
+            const char *pp = buf + XB + (32 * w + 8 * g + (iq >> 2)) * (2 * r) + (jb * 16 + 4 * (iq & 3)) * 2;
+            rp_i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((rp_lds_i16x4 *)pp);
+            rp_i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((rp_lds_i16x4 *)(pp + 4 * (2 * r)));
+            vb[jb] = u32x4{__builtin_bit_cast(uint2, lo).x, __builtin_bit_cast(uint2, lo).y,
+                           __builtin_bit_cast(uint2, hi).x, __builtin_bit_cast(uint2, hi).y};
+          }
         }
+#pragma unroll
+        for (int jb = 0; jb < JB; ++jb)
+#pragma unroll
+          for (int mt = 0; mt < MB; ++mt) mma16(E(), acc[mt][jb], xa[mt], vb[jb]);
       }
-#pragma unroll
-      for (int jb = 0; jb < JB; ++jb)
-#pragma unroll
-        for (int mt = 0; mt < MB; ++mt) mma16(E(), acc[mt][jb], xa[mt], vb[jb]);
     }
     __builtin_amdgcn_s_waitcnt((7 << 4));  // the loads past the end (zeros) too
   } else {

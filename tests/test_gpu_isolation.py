@@ -39,9 +39,9 @@ CASES = [
     ((2048, 2048, 11008, 8), (256, 128, 0, 1), (128, 128, 0, 1)),
     ((2048, 11008, 2048, 8), (128, 128, 0, 1), (256, 128, 0, 1)),
     ((2048, 2048, 256, 8), (128, 64, 1, 0), (128, 128, 0, 0)),
-    ((4096, 3072, 3072, 32), (256, 192, 0, 0), (256, 256, 0, 0)),
+    ((4096, 3072, 3072, 32), (256, 192, 0, 0), (256, 256, 1, 0)),
     ((4096, 3072, 1024, 32), (128, 128, 0, 0), (256, 256, 0, 0)),
-    ((4096, 3072, 8192, 32), (256, 256, 0, 0), (256, 256, 0, 1)),
+    ((4096, 3072, 8192, 32), (256, 256, 0, 0), (256, 256, 1, 0)),
     ((4096, 8192, 3072, 32), (256, 192, 0, 1), (256, 256, 0, 0)),
 ]
 
