@@ -18,7 +18,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "liblora_mi355x.so")
-SOURCES = ["gemm.hip", "skinny.hip", "head.hip", "topk.hip", "api.cpp", "ckpt.cpp", "static_ws.hip"]
+SOURCES = ["gemm.hip", "gemm_q.hip", "skinny.hip", "head.hip", "topk.hip", "api.cpp", "ckpt.cpp",
+           "static_ws.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

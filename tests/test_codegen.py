@@ -11,6 +11,7 @@ checked here on the generated code instead of being paid with a blanket
 s_nop before every load.  Compiling the sources to assembly takes a couple
 of minutes on the CPU.
 """
+import concurrent.futures as cf
 import os
 import re
 import shutil
@@ -37,7 +38,9 @@ def _asm(tmp_path_factory, src):
 
 @pytest.fixture(scope="module")
 def gemm_asm(tmp_path_factory):
-    return _asm(tmp_path_factory, "gemm.hip")
+    # the GEMM instances of both translation units (bf16 / fp32 and quantized)
+    with cf.ThreadPoolExecutor(2) as ex:
+        return "\n".join(ex.map(lambda src: _asm(tmp_path_factory, src), ["gemm.hip", "gemm_q.hip"]))
 
 
 @pytest.fixture(scope="module")
