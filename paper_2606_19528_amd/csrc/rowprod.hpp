@@ -1,6 +1,6 @@
 // rowprod.hpp -- one work item of the rank-r "row" product, shared by the
 // standalone row-skinny kernel (skinny.hip) and the producer workgroups of a
-// fused GEMM launch (gemm.hip):
+// fused GEMM launch (gemm_kernel.hpp):
 //   P_p[m][j] = sum_{k in segment p} X[m][k] V(j, k)
 // for the 16 * MB rows of row block `bx` and reduction segment `by` (see
 // RowArgs in launch.hpp).  The eight waves accumulate 16 x r tiles on 16x16
