@@ -438,7 +438,8 @@ def cpu_baseline(workload, layers, head, target_s=15.0):
         orc.frozen_dx(dyh, Wh)
         head_s = time.perf_counter() - t0
         head_flops = 2.0 * len(rows) * Wh.shape[0] * Wh.shape[1]
-    Ts = min(T, 16)
+    run_layer(min(T, 16))  # warm-up: the thread pool and the caches
+    Ts = min(T, 96)
     t = run_layer(Ts)
     budget = max(1.0, target_s - head_s)
     Ts = int(max(16, min(T, Ts * budget / max(t, 1e-3))))
