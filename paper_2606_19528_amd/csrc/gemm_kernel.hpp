@@ -9,17 +9,21 @@
 // Structure of one workgroup (4 or 8 waves, one BM x BN output tile):
 //  * k advances in stages of BKB bytes per row.  Global loads go through
 //    buffer resources (hardware bounds checks instead of per-load branches).
-//  * DMA = 1 or 2 (the bf16 128 x 128 and 256 x 128 tiles; 2 with producer
-//    workgroups of a fused rank-r pass in front): the loads write LDS directly
+//  * DMA = 1 or 2 (every bf16 tile shape; 2 with producer workgroups of a
+//    fused rank-r pass in front): the loads write LDS directly
 //    (buffer_load ... lds), into a ring of NBUF stages with NBUF - 1 stages
 //    in flight behind the one being read; no registers or LDS-write
 //    instructions are spent on staging.  One load moves 1 KB in lane order, so
 //    the lanes pick their source chunks to produce an XOR-swizzled layout whose
-//    fragment reads are bank-conflict free.
+//    fragment reads are bank-conflict free.  With a quantized B (QB = 4 or 8,
+//    DMA = 1) the codes, scales and offsets are loaded into LDS the same way,
+//    into slots of their own, and each step dequantizes one stage from them
+//    into the bf16 B area of the ring.
 //  * DMA = 0: loads go into a ring of RD register sets, then into an LDS ring
 //    of NBUF buffers; a stage's loads are issued RD - 1 steps before its LDS
-//    write, which covers the latency of reads that miss L2.  (The quantized-B
-//    path dequantizes in registers on the way into LDS, so it needs this.)
+//    write, which covers the latency of reads that miss L2 (the fp32 check
+//    mode, and a quantized B with groups of fewer than 64 weights, which is
+//    dequantized in registers on the way into LDS).
 //  * NBUF = 3: a stage is written to LDS two steps before it is consumed, so
 //    the first k-slice's MFMA fragments of the next stage can be read before
 //    the end-of-step barrier and the MFMAs of a step start without waiting on
