@@ -70,6 +70,30 @@ def test_split_reduction(orc, shape, recompute, dtype):
     _case(orc, T, K, N, r, 2.0 * r, seed=41, dtype=dtype, recompute=recompute)
 
 
+# Seeded random shapes over the ranges where the tile configuration, the
+# fused or unfused rank-r passes, their split partial sums and the ragged
+# tails change: small ones (T < 2600, d <= 3200; mostly 128 x 64 and 128 x 128
+# tiles) and large ones (T >= 1024, d >= 1024; 256 x 128 to 256 x 256 tiles),
+# ranks from 1 to 128.  dA and dB in full, 64 sampled rows of y and dx.
+def _random_shapes(n, seed, t_range, d_range, max_macs):
+    g = np.random.default_rng(seed)
+    out = []
+    while len(out) < n:
+        T = int(g.integers(*t_range))
+        K, N = (8 * int(g.integers(d_range[0] // 8, d_range[1] // 8)) for _ in range(2))
+        r = int(g.choice([1, 3, 8, 12, 16, 24, 32, 40, 64, 100, 128]))
+        if T * K * N <= max_macs:
+            out.append((T, K, N, r))
+    return out
+
+
+@pytest.mark.parametrize("shape", _random_shapes(16, 2026, (1, 2600), (8, 3200), 2.5e9) +
+                         _random_shapes(10, 7, (1024, 4300), (1024, 8200), 8e10))
+def test_random_shapes(orc, shape):
+    T, K, N, r = shape
+    _case(orc, T, K, N, r, 2.0 * r, seed=sum(shape), rows=sample_rows(T, 64))
+
+
 # Long T: the rank-r row products take several 16-row tiles per workgroup, or
 # whole rows, or two segments of 16-row blocks (ragged last block, rank not a
 # multiple of 16, u rematerialised, reduction axes on both sides of 4096).
