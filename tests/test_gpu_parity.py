@@ -190,6 +190,12 @@ def test_zero_B_gives_plain_linear(orc):
 
 
 # --- fp32 check mode -------------------------------------------------------------
+@pytest.mark.parametrize("shape", _random_shapes(8, 99, (1, 700), (8, 1100), 1e8))
+def test_fp32_check_mode_random_shapes(orc, shape):
+    T, K, N, r = shape
+    _case(orc, T, K, N, r, 2.0 * r, seed=sum(shape), dtype=torch.float32)
+
+
 @pytest.mark.parametrize("shape", [(128, 256, 256, 8), (3, 8, 24, 1), (129, 136, 144, 32),
                                    (300, 520, 392, 16), (65, 264, 128, 0)])
 def test_fp32_check_mode(orc, shape):

@@ -82,6 +82,30 @@ def test_quant_direct_tiles(orc, shape):
     _qcase(orc, T, K, N, r, bits, group, seed=T + N + bits, rows=rows)
 
 
+# Seeded random shapes: INT4 and INT8, groups of 16 to 256 (register-staged
+# below 64, direct-to-LDS from 64), ranks 0 to 64, 1 to 4300 tokens.  dA and
+# dB in full, 64 sampled rows of y and dx.
+def _random_qshapes(n, seed):
+    g = np.random.default_rng(seed)
+    out = []
+    while len(out) < n:
+        T = int(g.integers(1, 4300))
+        group = int(g.choice([16, 32, 64, 128, 256]))
+        K = group * int(g.integers(1, max(2, 6144 // group)))
+        N = 8 * int(g.integers(1, 800))
+        r = int(g.choice([0, 1, 3, 8, 16, 32, 64]))
+        bits = int(g.choice([4, 8]))
+        if T * K * N <= 3e10:
+            out.append((T, K, N, r, bits, group))
+    return out
+
+
+@pytest.mark.parametrize("shape", _random_qshapes(12, 404))
+def test_quant_random_shapes(orc, shape):
+    T, K, N, r, bits, group = shape
+    _qcase(orc, T, K, N, r, bits, group, seed=sum(shape), rows=sample_rows(T, 64))
+
+
 @pytest.mark.parametrize("shape", [(129, 256, 392, 8, 128), (64, 3072, 1000, 8, 128),
                                    (33, 1024, 136, 4, 16), (4000, 3072, 3000, 8, 128),
                                    (2048, 8192, 3000, 8, 64), (1024, 3072, 8192, 4, 128)])
