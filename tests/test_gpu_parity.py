@@ -218,6 +218,23 @@ def test_frozen_dx_small(orc, shape, dtype):
     assert relerr(dx.cpu().to(torch.float64).numpy(), ref) <= TOL[dtype]
 
 
+# Seeded random shapes of the frozen dx (every k-major tile shape, no side
+# items): bf16 on 64 sampled rows, fp32 in full on small shapes.
+@pytest.mark.parametrize("shape,dtype",
+                         [(sh[:3], torch.bfloat16) for sh in _random_shapes(8, 5, (1, 4300), (8, 8200), 6e10)] +
+                         [(sh[:3], torch.float32) for sh in _random_shapes(4, 6, (1, 600), (8, 1100), 1e8)])
+def test_frozen_dx_random_shapes(orc, shape, dtype):
+    T, K, N = shape
+    _announce(f"frozen T={T} K={K} N={N} {dtype}")
+    inp = frozen_inputs(T, K, N, seed=T + K + N, dtype=dtype)
+    dx = torch.empty(T, K, dtype=dtype, device="cuda")
+    lm.frozen_linear_bwd_dx(inp["dy"].cuda(), inp["W"].cuda(), dx)
+    torch.cuda.synchronize()
+    rows = sample_rows(T, 64) if dtype == torch.bfloat16 else list(range(T))
+    ref = orc.frozen_dx(inp["dy"], inp["W"], rows=rows)
+    assert relerr(dx.cpu().to(torch.float64).numpy()[rows], ref) <= TOL[dtype]
+
+
 # 256 x 192 tiles with k-major B (frozen dx carries no side items): ragged row
 # and column tiles, reduction axis not a multiple of the stage depth.
 def test_frozen_dx_one_wave_tiles(orc):
