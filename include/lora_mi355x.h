@@ -55,9 +55,11 @@
  * the rank-r products, across waves) adds its parts in a fixed order, so
  * identical inputs give bitwise identical outputs.  Atomics appear only where
  * they cannot change a result: the counters of the fused hand-over (they
- * order work; see lora_handover_giveups), and, in the top-k table build, the
- * reservation of candidate-list slots, whose order is normalised by the
- * selection (ties go to the smaller index).
+ * order work; see lora_handover_giveups); the part counts of the dA / dB
+ * token reductions that run as token parts (they pick the part that adds
+ * the parts' tiles, which it adds in ascending part order); and, in the
+ * top-k table build, the reservation of candidate-list slots, whose order is
+ * normalised by the selection (ties go to the smaller index).
  *
  * Device memory held by the library itself: one 4-byte counter per device
  * (lora_handover_giveups); everything else is the caller's.
@@ -288,10 +290,14 @@ lora_status_t lora_ckpt_backward(const lora_node_t *nodes, int n, int64_t T, con
  * (y, T x d_out) and of the dx GEMM (T x d_in); whether the rank-r pass runs
  * as producer workgroups inside that GEMM launch ("fused"); and otherwise
  * over how many partial sums of its reduction axis u = x A^T and
- * du = s dy B are computed.  Errors as for the entry points' size checks. */
+ * du = s dy B are computed; and over how many consecutive token ranges each
+ * output block of the token reductions dA = du^T x and dB = s dy^T u runs
+ * in the unfused dx launch (bwd_side_parts; 1 = all T in one workgroup).
+ * Errors as for the entry points' size checks. */
 typedef struct {
   int fwd_tile_m, fwd_tile_n, fwd_fused, fwd_u_parts;
   int bwd_tile_m, bwd_tile_n, bwd_fused, bwd_du_parts;
+  int bwd_side_parts;
 } lora_plan_t;
 lora_status_t lora_linear_plan(int64_t T, int64_t d_in, int64_t d_out, int64_t r, lora_dtype_t dt,
                                lora_plan_t *plan);

@@ -198,10 +198,11 @@ FwdLayout fwd_layout(int64_t T, int64_t K, int64_t N, int64_t r, lora_dtype_t dt
 }
 
 struct BwdLayout {
-  size_t sync, u, du, dutail, acat, total;
+  size_t sync, u, du, dutail, acat, scnt, spart, total;
   int ldt;
   bool fused;
   RowSplit sp_u, sp_du;
+  int tparts, tchunk;  // token parts of the dA / dB side items (unfused dx launch)
 };
 BwdLayout bwd_layout(int64_t T, int64_t K, int64_t N, int64_t r, lora_dtype_t dt) {
   BwdLayout L{};
@@ -224,6 +225,14 @@ BwdLayout bwd_layout(int64_t T, int64_t K, int64_t N, int64_t r, lora_dtype_t dt
   off += round256((size_t)T * L.ldt * esize(dt));
   L.acat = off;  // [nsplit * r][K]: A repeated once per partial
   off += L.sp_du.nsplit > 1 ? round256((size_t)L.sp_du.nsplit * r * K * esize(dt)) : 0;
+  L.tparts = 1;
+  L.tchunk = (int)T;
+  if (!L.fused) side_split(T, K, N, r, d, &L.tparts, &L.tchunk);
+  const size_t items = L.tparts > 1 ? (size_t)side_item_count(K, N, r, d) : 0;
+  L.scnt = off;  // [items] part counts of the side items
+  off += round256(items * 4);
+  L.spart = off;  // [items][tparts] part tiles
+  off += items * L.tparts * SIDE_SLOT_FLOATS * 4;
   L.total = off;
   return L;
 }
@@ -584,6 +593,10 @@ lora_status_t bwd_impl(const void *x, const void *W, const void *qc, const float
       ra.bcopy_mode = BCOPY_FLAT; ra.bcopy_src = A; ra.bcopy_dst = wsb + L.acat;
       ra.bcopy_period = r * d_in; ra.bcopy_elems = ns * r * d_in;
     }
+    if (L.tparts > 1) {  // the dx launch's side parts count from zero
+      ra.zero = (unsigned *)(wsb + L.scnt);
+      ra.nzero = side_item_count(d_in, d_out, r, d);
+    }
     Timed t(K_LORA_DY_B, st);
     e = launch_row_skinny(ra, d, st);
     t.done();
@@ -593,6 +606,9 @@ lora_status_t bwd_impl(const void *x, const void *W, const void *qc, const float
   sd.T = (int)T; sd.r = (int)r; sd.njobs = 2; sd.scale1 = scale; sd.vstride = T * r;
   sd.job[0] = ColJob{x, du, dA, (int)d_in, ns};
   sd.job[1] = ColJob{dy, u, dB, (int)d_out, u_parts};
+  sd.tparts = L.tparts; sd.tchunk = L.tchunk;
+  sd.cnt = (unsigned *)(wsb + L.scnt);
+  sd.part = (float *)(wsb + L.spart);
   g.A2 = wsb + L.dutail; g.lda2 = L.ldt;
   g.B2 = ns > 1 ? (const void *)(wsb + L.acat) : A; g.ldb2 = d_in;
   g.r = (int)(ns * r);
@@ -935,6 +951,7 @@ lora_status_t lora_linear_plan(int64_t T, int64_t d_in, int64_t d_out, int64_t r
     p.fwd_u_parts = F.sp.nsplit;
     p.bwd_fused = B.fused;
     p.bwd_du_parts = B.sp_du.nsplit;
+    p.bwd_side_parts = B.tparts;
   }
   *plan = p;
   return LORA_OK;

@@ -6,9 +6,10 @@
 // partial sums over a split reduction (added in ascending order on load).
 //
 // One work item = (column block of 16*VEC columns, group of 32 rank indices)
-// over all T tokens, so no partial sums leave the workgroup (cross-workgroup
-// reductions would need device-scope fences, which write back and invalidate
-// the per-XCD L2s).  Each wave reads VEC rows x 16 bytes of X (row-major,
+// over all T tokens -- or, in an unfused launch whose tiles leave CUs idle,
+// over one of `tparts` consecutive token ranges, the last part to finish
+// adding the parts' tiles in ascending part order (SideArgs), so the result
+// does not depend on the order the parts finish in.  Each wave reads VEC rows x 16 bytes of X (row-major,
 // coalesced), transposes the VEC x VEC block in registers so a lane holds VEC
 // consecutive tokens of one column -- the matrix-core operand whose reduction
 // axis is the token axis -- and accumulates a (16*VEC) x 32 tile, two token
@@ -59,7 +60,9 @@ __device__ __forceinline__ int side_items_total(const SideArgs &s) {
 
 // Always inlined: called as a function, it takes the launch's arguments by
 // address, so every wave of the launch first copies them to scratch memory.
-template <class E, int NW>
+// PARTS: the launch may run its items as token parts (s.tparts > 1); the
+// fused launches (no registers to spare) run every item over all T.
+template <class E, int NW, bool PARTS>
 __device__ __forceinline__ void side_item(const SideArgs &s, int item, char *smem) {
   typedef typename E::T T;
   constexpr int VEC = E::VEC;
@@ -68,6 +71,15 @@ __device__ __forceinline__ void side_item(const SideArgs &s, int item, char *sme
   constexpr int JB = SIDE_JB;
   constexpr int RS = JB * 16 + 1;  // padded LDS row (floats)
 
+  // Work unit -> (item, token part).
+  const int unit = item;
+  const int tparts = PARTS ? s.tparts : 1;
+  int part = 0;
+  if (tparts > 1) {
+    item = unit / tparts;
+    part = unit - item * tparts;
+  }
+  const int gitem = item;
   int ji = 0;
   if (item >= s.n0) {
     ji = 1;
@@ -87,7 +99,8 @@ __device__ __forceinline__ void side_item(const SideArgs &s, int item, char *sme
   const int cb = item / ngz;
   const int jg = z * 32;
   const int c0 = cb * COLS;
-  const int t_end = s.T;
+  const int t_begin = part * s.tchunk;
+  const int t_end = tparts > 1 ? min(s.T, t_begin + s.tchunk) : s.T;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 4, cl = lane & 15;
@@ -155,7 +168,7 @@ __device__ __forceinline__ void side_item(const SideArgs &s, int item, char *sme
     // token step.  Each virtual wave runs its own steps in ascending order,
     // exactly as a wave of an eight-wave workgroup would.
     const int w0 = __builtin_amdgcn_readfirstlane(wave);
-    auto tb_of = [&](int n) { return (w0 + NW * (n % PER) + VW * (n / PER)) * ROWS; };
+    auto tb_of = [&](int n) { return t_begin + (w0 + NW * (n % PER) + VW * (n / PER)) * ROWS; };
     Step cur, nxt;
     load(tb_of(0), cur);
     for (int n = 0; tb_of(n) < t_end; n += PER) {
@@ -201,9 +214,49 @@ __device__ __forceinline__ void side_item(const SideArgs &s, int item, char *sme
           for (int i = 0; i < 4; ++i) acc[0][q][jb][i] += slot[((4 * g + i) * VEC + q) * RS + jb * 16 + cl];
     }
   }
-  // Wave 0 holds the item's tile: scale and store it.
+  // Wave 0 holds the tile (of the item, or of this part).
   const int jn = min(32, r - jg);
   if (wave == 0) {
+    if (tparts > 1) {
+      // A part: its tile to its slot, one 16-byte quad per accumulator
+      // (quad (q, jb) of lane l at ((q * JB + jb) * 64 + l) * 4), by
+      // device-scope stores (relaxed atomic stores carry the sc1 policy on
+      // gfx950: written through to the point of coherence, no L2 write-back),
+      // complete before the count.
+      static_assert(VEC * JB * 4 * 64 <= SIDE_SLOT_FLOATS, "slot size");
+      float *slot = s.part + (int64_t)unit * SIDE_SLOT_FLOATS;
+#pragma unroll
+      for (int q = 0; q < VEC; ++q)
+#pragma unroll
+        for (int jb = 0; jb < JB; ++jb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            __hip_atomic_store(slot + ((q * JB + jb) * 64 + lane) * 4 + i, acc[0][q][jb][i], __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+      __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));  // vmcnt(0)
+      unsigned before = 0;
+      if (lane == 0) before = __hip_atomic_fetch_add(s.cnt + gitem, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      before = __builtin_amdgcn_readfirstlane(before);
+      if (before != (unsigned)(tparts - 1)) return;
+      // The last part: every slot of the item is complete.  Its lines are in
+      // no cache (see SideArgs), so ordinary loads, issued after the count
+      // (the compiler barrier keeps them there), fetch the stored values.
+      // A slot's sixteen 16-byte loads are all issued before its sums.
+      asm volatile("" ::: "memory");
+      const float *first = s.part + (int64_t)(unit - part) * SIDE_SLOT_FLOATS;
+      for (int pp = 0; pp < tparts; ++pp) {
+        const f32x4 *sl = (const f32x4 *)(first + (int64_t)pp * SIDE_SLOT_FLOATS);
+        f32x4 v[VEC][JB];
+#pragma unroll
+        for (int q = 0; q < VEC; ++q)
+#pragma unroll
+          for (int jb = 0; jb < JB; ++jb) v[q][jb] = sl[(q * JB + jb) * 64 + lane];
+#pragma unroll
+        for (int q = 0; q < VEC; ++q)
+#pragma unroll
+          for (int jb = 0; jb < JB; ++jb) acc[0][q][jb] = pp == 0 ? v[q][jb] : acc[0][q][jb] + v[q][jb];
+      }
+    }
 #pragma unroll
     for (int q = 0; q < VEC; ++q)
 #pragma unroll

@@ -1,6 +1,8 @@
 // gemm.hip -- launches of the bf16 / fp32 GEMM instances (the kernel template
 // and its launcher are in gemm_kernel.hpp; the quantized-B instances in
 // gemm_q.hip): plain, fused with rank-r producers, and with epilogues.
+#include <algorithm>
+
 #include "gemm_kernel.hpp"
 
 namespace lora {
@@ -12,8 +14,35 @@ int side_workgroups(SideArgs *s, Dtype dt) {
     n += (s->job[i].L + cols - 1) / cols * ((s->r + 31) / 32);
     if (i == 0) s->n0 = n;
   }
-  s->ntot = n;
-  return (n + 7) / 8 * 8;
+  if (s->tparts < 1) s->tparts = 1;
+  if (s->tparts == 1) s->tchunk = s->T;
+  s->ntot = n * s->tparts;
+  return (s->ntot + 7) / 8 * 8;
+}
+
+int side_item_count(int64_t d_in, int64_t d_out, int64_t r, Dtype dt) {
+  const int64_t cols = dt == DT_BF16 ? SideShape<BF16>::COLS : SideShape<F32>::COLS;
+  return (int)(((d_in + cols - 1) / cols + (d_out + cols - 1) / cols) * ((r + 31) / 32));
+}
+
+// SPLIT_RULE
+void side_split(int64_t T, int64_t d_in, int64_t d_out, int64_t r, Dtype dt, int *tparts, int *tchunk) {
+  constexpr int64_t STEP = 8 * SideShape<BF16>::ROWS;  // one step of each virtual wave
+  *tparts = 1;
+  *tchunk = (int)T;
+  if (dt != DT_BF16) return;
+  int bm = 0, bn = 0;
+  gemm_tile_shape((int)T, (int)d_in, true, true, dt, &bm, &bn);
+  const int64_t tiles = ((T + bm - 1) / bm) * ((d_in + bn - 1) / bn);
+  const int64_t items = side_item_count(d_in, d_out, r, dt);
+  if (tiles >= 256 || items < 1) return;
+  int64_t p = std::min<int64_t>({4, T / STEP, (256 - tiles) / items});
+  // The part tiles stay within an eighth of the fp32 dW the method never forms.
+  while (p > 1 && items * p * SIDE_SLOT_FLOATS * 4 > d_in * d_out / 2) --p;
+  if (p <= 1) return;
+  const int64_t chunk = ((T + p - 1) / p + STEP - 1) / STEP * STEP;
+  *tparts = (int)((T + chunk - 1) / chunk);
+  *tchunk = (int)chunk;
 }
 
 void gemm_tile_shape(int M, int N, bool b_kmajor, bool with_side, Dtype dt, int *bm, int *bn) {

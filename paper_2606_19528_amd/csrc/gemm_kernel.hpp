@@ -339,7 +339,7 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
           }
           __syncthreads();
           for (int it = blockIdx.x; it < nitems; it += fz.nprod) {
-            side_item<E, WM * WN * WK>(side, it, smem);
+            side_item<E, WM * WN * WK, false>(side, it, smem);
             __syncthreads();
           }
         }
@@ -348,10 +348,11 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void gemm_kernel(GemmArgs g, int
       return;
     }
   }
-  // (A fused launch runs its side items on the producers: nside = 0.)
-  if constexpr (!FUSE) {
+  // (A fused launch runs its side items on the producers: nside = 0.  Only
+  // the dx launches, k-major B, carry side items.)
+  if constexpr (!FUSE && BMODE != B_ROW) {
     if (bid < nside) {
-      if (bid < side_items_total<E>(side)) side_item<E, WM * WN * WK>(side, bid, smem);
+      if (bid < side_items_total<E>(side)) side_item<E, WM * WN * WK, true>(side, bid, smem);
       return;
     }
   }
@@ -1794,6 +1795,7 @@ static hipError_t launch_cfg(const GemmArgs &g, const SideArgs *side, hipStream_
     fz->nwg = (fz->nprod + 7) / 8 * 8;
     fa = *fz;
   }
+  if (BMODE == B_ROW && nside > 0) return hipErrorInvalidValue;  // side items run in k-major launches only
   const int grid = tm * tn + nside + fa.nwg;
   if (grid == 0) return hipSuccess;
   hipLaunchKernelGGL((gemm_kernel<E, BM, BN, WM, WN, WK, BMODE, BKB, NBUF, RD, FS, QB, EPI, DMA>), dim3(grid),

@@ -20,6 +20,17 @@ void set_last_error(const char *msg);
 // L elements).  V may be given as `vparts` partial sums V_p = V + p * vstride
 // (p < vparts), added in ascending p when loaded.  (Kept small: these
 // arguments share the kernel's scalar registers with the tiles.)
+// An item (column block, rank group) may run as `tparts` parts over
+// consecutive ranges of `tchunk` tokens (unfused launches only).  A part
+// stores its tile in its slot of `part` (SIDE_SLOT_FLOATS floats) with
+// device-scope stores, waits until they have completed, and counts itself in
+// cnt[item] (zero before the launch); the part that counts last reads the
+// item's slots with ordinary loads, adds them in ascending part order and
+// stores the result.  Why ordinary loads see the other parts' stores: as for
+// the hand-over of FuseArgs below -- no cache holds a slot line from an
+// earlier launch, each part owns whole lines, and no wave reads a slot
+// before the count shows that every part's stores have completed.
+// tparts = 1: each item over all T, no slots.
 struct ColJob {
   const void *X;
   const float *V;
@@ -33,8 +44,18 @@ struct SideArgs {
   int T, r;
   float scale1;
   int64_t vstride;
-  int n0, ntot;  // work items of job 0 and of both (set by the GEMM launcher)
+  int n0, ntot;  // work items of job 0, and parts of both jobs' items (set by the GEMM launcher)
+  int tparts, tchunk;
+  float *part;
+  unsigned *cnt;
 };
+constexpr int SIDE_SLOT_FLOATS = 4096;  // a part's tile: 64 values per lane of one wave
+// Side items of a backward with reduction lengths d_in (dA) and d_out (dB).
+int side_item_count(int64_t d_in, int64_t d_out, int64_t r, Dtype dt);
+// Token parts per side item of the unfused dx launch, and tokens per part:
+// more than one only where the launch's tiles leave CUs idle (fewer than 256
+// tiles) and the parts fit on them (bf16; fp32: one part).
+void side_split(int64_t T, int64_t d_in, int64_t d_out, int64_t r, Dtype dt, int *tparts, int *tchunk);
 
 // C[M, N] = sum_k Aop[m][k] Bop[n][k]  (+ LoRA step), rounded to the element type.
 //   Aop[m][k] = A[m*lda + k]                         m < M, k < K
@@ -170,8 +191,8 @@ hipError_t launch_gemm_q(const GemmArgs &g, int bits, bool b_kmajor, const SideA
 // M x N product with this B layout, with or without side items.
 void gemm_tile_shape(int M, int N, bool b_kmajor, bool with_side, Dtype dt, int *bm, int *bn);
 
-// Counts the work items of `side` into s->n0 and s->ntot and returns the
-// number of side workgroups they need (a multiple of 8).
+// Counts the work items of `side` into s->n0 and their parts into s->ntot,
+// and returns the number of side workgroups they need (a multiple of 8).
 int side_workgroups(SideArgs *s, Dtype dt);
 
 enum { V_ROW = 0, V_KMAJ_TR = 1, V_KMAJ_GATHER = 2 };
@@ -207,6 +228,8 @@ struct RowArgs {
   int bcopy_rows;
   int64_t bcopy_period, bcopy_elems;
   int mb;  // row tiles of 16 per workgroup: 1 (0), 2 or 4 (bf16, r <= 32)
+  unsigned *zero;  // row_skinny only: workgroup (0, 0) also sets zero[0 .. nzero) to 0
+  int nzero;
 };
 hipError_t launch_row_skinny(const RowArgs &a, Dtype dt, hipStream_t st);
 

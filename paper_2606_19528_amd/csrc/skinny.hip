@@ -19,6 +19,9 @@ template <class E, int JB, int VMODE, int U, int MB>
 __global__ __launch_bounds__(64 * ROW_NW) void row_skinny_kernel(RowArgs a) {
   __shared__ __align__(16) char smem[row_lds_bytes<E, JB, VMODE, U, MB>()];
   row_item<E, JB, VMODE, U, MB>(a, blockIdx.x, blockIdx.y, gridDim.x, gridDim.y, smem);
+  // After the row work, so that nothing delays its first loads.
+  if (blockIdx.x == 0 && blockIdx.y == 0)
+    for (int i = threadIdx.x; i < a.nzero; i += blockDim.x) a.zero[i] = 0;
 }
 
 template <class E, int VMODE, int MB>
@@ -65,6 +68,7 @@ hipError_t launch_row_skinny(const RowArgs &a, Dtype dt, hipStream_t st) {
   if ((int64_t)(a.nsplit - 1) * a.seg >= a.L || (int64_t)a.nsplit * a.seg < a.L) return hipErrorInvalidValue;
   if (a.tail && a.nsplit * a.r > a.ldt) return hipErrorInvalidValue;
   if (a.mb > 1 && (a.r > 32 || dt != DT_BF16)) return hipErrorInvalidValue;
+  if (a.nzero < 0 || (a.nzero > 0 && !a.zero)) return hipErrorInvalidValue;
   if (dt == DT_BF16) {
     if (a.vmode == V_ROW) return row_dispatch_mb<BF16, V_ROW>(a, st);
     if (a.r % 8 == 0) return row_dispatch_mb<BF16, V_KMAJ_TR>(a, st);

@@ -30,7 +30,8 @@ class _Node(ctypes.Structure):
 class _Plan(ctypes.Structure):
     """lora_plan_t of the C ABI."""
     _fields_ = [(n, ctypes.c_int) for n in ("fwd_tile_m", "fwd_tile_n", "fwd_fused", "fwd_u_parts",
-                                             "bwd_tile_m", "bwd_tile_n", "bwd_fused", "bwd_du_parts")]
+                                             "bwd_tile_m", "bwd_tile_n", "bwd_fused", "bwd_du_parts",
+                                             "bwd_side_parts")]
 
 
 class LoraError(RuntimeError):

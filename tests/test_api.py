@@ -56,17 +56,20 @@ def test_workspace_query():
     # forward: partial sums of u (at most ldt / r of them over the split
     # reduction axis), the bf16 LoRA-step operand (ldt = 64 columns) and B
     # repeated once per partial; backward: partial sums of u and du, the
-    # LoRA-step operand and A repeated once per partial -- all far below the
-    # fp32 dW the method never forms.
+    # LoRA-step operand, A repeated once per partial, and where the dA / dB
+    # items run as token parts their counts and part tiles (at most an eighth
+    # of the fp32 dW) -- all far below the fp32 dW the method never forms.
     assert ws(L.LORA_OP_BWD, 128, 256, 256, 0) == 0
     for T, K, N, r in [(128, 256, 256, 8), (1024, 3072, 3072, 16), (2048, 3072, 8192, 16),
-                       (4096, 8192, 3072, 32), (2048, 2048, 256, 8), (16, 4096, 4096, 128)]:
+                       (4096, 8192, 3072, 32), (2048, 2048, 256, 8), (16, 4096, 4096, 128),
+                       (4096, 3072, 1024, 32), (1500, 1544, 2056, 12)]:
         ldt = (r + 63) // 64 * 64
         S = ldt // r
         f = ws(L.LORA_OP_FWD, T, K, N, r)
         assert T * r * 4 <= f <= S * T * r * 4 + (T + N) * ldt * 2 + 3 * 256, (T, K, N, r, f)
         b = ws(L.LORA_OP_BWD, T, K, N, r)
-        assert 8 * T * r <= b <= 2 * S * T * r * 4 + T * ldt * 2 + S * r * K * 2 + 4 * 256, (T, K, N, r, b)
+        side = (-(-K // 128) - (-N // 128)) * -(-r // 32) * 4 + 256 + K * N // 2
+        assert 8 * T * r <= b <= 2 * S * T * r * 4 + T * ldt * 2 + S * r * K * 2 + side + 4 * 256, (T, K, N, r, b)
         assert b < N * K * 4, (T, K, N, r, b)
     # fp32 check mode pads the LoRA step to 32 columns
     assert 64 * 16 * 4 <= ws(L.LORA_OP_FWD, 64, 256, 256, 16, dt=L.LORA_F32) <= 2 * 64 * 16 * 4 + (64 + 256) * 32 * 4 + 768

@@ -340,6 +340,35 @@ def test_bwd_without_dx_matches(orc):
     assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1])
 
 
+# Where the dx tiles leave CUs idle, the dA / dB token reductions run as parts
+# over consecutive token ranges and the last part of each output block adds
+# the parts' tiles: two parts with a ragged second one (T = 1000: 512 + 488
+# tokens), three parts (T = 1500), r = 32 (the Llama k / v case, also at full
+# size in test_full_llama_stack_layer).  dA and dB in full, sampled dx; then a
+# second call (the counts start from zero again) and one without dx, both
+# bitwise equal to the first.
+@pytest.mark.parametrize("shape,parts", [((1000, 1544, 1032, 12), 2), ((1500, 1544, 2056, 12), 3),
+                                         ((2000, 1544, 1032, 32), 2)])
+def test_side_items_in_token_parts(orc, shape, parts):
+    T, K, N, r = shape
+    assert lm.lora_linear_plan(T, K, N, r)["bwd_side_parts"] == parts
+    _case(orc, T, K, N, r, 2.0 * r, seed=61, rows=sample_rows(T, 64))
+    inp = {k: v.cuda() for k, v in lora_inputs(T, K, N, r, seed=62).items()}
+    u = torch.empty(T, r, device="cuda")
+    y = torch.empty(T, N, dtype=torch.bfloat16, device="cuda")
+    lm.lora_linear_fwd(inp["x"], inp["W"], inp["A"], inp["B"], y, u, 2.0)
+    outs = []
+    for with_dx in (True, True, False):
+        dx = torch.empty(T, K, dtype=torch.bfloat16, device="cuda") if with_dx else None
+        dA = torch.full((r, K), float("nan"), device="cuda")
+        dB = torch.full((N, r), float("nan"), device="cuda")
+        lm.lora_linear_bwd(inp["x"], inp["W"], inp["A"], inp["B"], u, inp["dy"], dx, dA, dB, 2.0)
+        torch.cuda.synchronize()
+        outs.append((dA.cpu(), dB.cpu()))
+    for o in outs[1:]:
+        assert torch.equal(outs[0][0], o[0]) and torch.equal(outs[0][1], o[1])
+
+
 def test_repeated_calls_reuse_workspace(orc):
     """The side reductions' counters are left zeroed: back-to-back calls sharing one
     workspace (and calls with a smaller shape in between) give identical results."""
