@@ -2,7 +2,7 @@
 scratch as workspace, for callers that cannot allocate.  Checked against
 lora_linear_bwd (the same kernels with a caller workspace) through the C ABI:
 every output bitwise equal and within the fp64 oracle's tolerance, on calls
-in a row whose second and third use smaller inputs (the scratch keeps the
+in a row whose later ones use smaller inputs (the scratch keeps the
 previous call's contents), with no device allocation during the calls; and,
 on the CPU, the rejection of sizes beyond the scratch.
 """
@@ -46,9 +46,12 @@ def _bufs(T, K, N, r, dev="cuda"):
 
 @pytest.mark.gpu
 def test_noalloc_matches_workspace_entry_point(orc):
-    # fused backward (q_proj), an unfused one with split partial sums, then a
-    # smaller fused one: each after the previous left its state in the scratch
-    shapes = [(1024, 3072, 3072, 16), (2048, 2048, 2048, 8), (300, 520, 392, 16)]
+    # fused backward (q_proj), an unfused one with split partial sums, one
+    # whose dA / dB items run as token parts (their counts must start from
+    # zero in a scratch that holds the previous call's), then a smaller fused
+    # one: each after the previous left its state in the scratch
+    shapes = [(1024, 3072, 3072, 16), (2048, 2048, 2048, 8), (1000, 1544, 1032, 12), (300, 520, 392, 16)]
+    assert lm.lora_linear_plan(1000, 1544, 1032, 12)["bwd_side_parts"] == 2
     for i, (T, K, N, r) in enumerate(shapes):
         print(f"[case] noalloc bwd T={T} K={K} N={N} r={r}", file=sys.stderr, flush=True)
         s = 2.0
