@@ -15,7 +15,7 @@ import pytest
 import torch
 
 from gpu_helpers import compare, oracle_lora
-from workloads import lora_inputs
+from workloads import lora_inputs, sample_rows
 
 pytestmark = pytest.mark.gpu
 
@@ -93,13 +93,17 @@ def test_arbitrary_workspace_contents(orc, fill):
         compare({k: v.cpu() for k, v in o.items()}, ref, torch.bfloat16, label=f"fill={fill}")
 
 
-def test_graph_replay(orc):
-    """A captured forward + backward replayed with new input values each time:
-    every replay carries the same tag, and each must still wait for its own
-    producers (the tiles' count left by the previous replay keeps a stale
-    state from passing for armed)."""
-    T, K, N, r = 256, 512, 768, 16
+@pytest.mark.parametrize("shape", [(256, 512, 768, 16), (1000, 1544, 1032, 12)])
+def test_graph_replay(orc, shape):
+    """A captured forward + backward replayed with new input values each time.
+    Fused (256 x 512 -> 768): every replay carries the same tag, and each must
+    still wait for its own producers (the tiles' count left by the previous
+    replay keeps a stale state from passing for armed).  Unfused with the
+    dA / dB items in token parts (1000 x 1544 -> 1032): the part counts the
+    previous replay left must be zeroed again inside the graph."""
+    T, K, N, r = shape
     s = 2.0
+    rows = sample_rows(T, 64)
     d = {k: v.cuda() for k, v in lora_inputs(T, K, N, r, seed=60).items()}
     o = _buffers(T, K, N, r)
     ws_f, ws_b = _ws(T, K, N, r), _ws(T, K, N, r)
@@ -118,8 +122,8 @@ def test_graph_replay(orc):
         torch.cuda.synchronize()
         graph.replay()
         torch.cuda.synchronize()
-        ref = oracle_lora(orc, inp, s)
-        compare({k: v.cpu() for k, v in o.items()}, ref, torch.bfloat16, label=f"replay {it}")
+        ref = oracle_lora(orc, inp, s, rows=rows)
+        compare({k: v.cpu() for k, v in o.items()}, ref, torch.bfloat16, rows=rows, label=f"replay {it}")
 
 
 @pytest.mark.parametrize("shape,recompute", [((48, 2056, 1032, 8), False), ((48, 2056, 1032, 8), True),
