@@ -100,6 +100,17 @@ def _random_qshapes(n, seed):
     return out
 
 
+# The dx launch's dA / dB items as token parts (the plan's bwd_side_parts)
+# beside the dequantizing tiles: two parts of 512 + 488 tokens with
+# register-staged INT8 groups of 32, and the Llama k / v shape in INT4 with
+# direct-to-LDS groups of 128 (sampled rows).
+@pytest.mark.parametrize("shape", [(1000, 1536, 1032, 12, 8, 32), (4096, 3072, 1024, 32, 4, 128)])
+def test_quant_side_items_in_token_parts(orc, shape):
+    T, K, N, r, bits, group = shape
+    assert lm.lora_linear_plan(T, K, N, r)["bwd_side_parts"] == 2
+    _qcase(orc, T, K, N, r, bits, group, seed=T + K, rows=sample_rows(T, 64))
+
+
 @pytest.mark.parametrize("shape", _random_qshapes(12, 404))
 def test_quant_random_shapes(orc, shape):
     T, K, N, r, bits, group = shape
