@@ -25,7 +25,16 @@ int side_item_count(int64_t d_in, int64_t d_out, int64_t r, Dtype dt) {
   return (int)(((d_in + cols - 1) / cols + (d_out + cols - 1) / cols) * ((r + 31) / 32));
 }
 
-// SPLIT_RULE
+// An item over all T draws 40 - 55 GB/s (one workgroup per CU): at T = 4096
+// (1.5 MB of x or dy and of du or u) it outlasts the tiles it runs beside in
+// the dx launches of a 3072 -> 1024 linear (192 tiles of 256 x 256 over a
+// reduction of 1024).  Where the tiles leave CUs idle, the items' parts take
+// them.  Where the tiles fill the CUs, the items delay as many tiles by
+// their own duration; parts of at least 2048 tokens (T >= 4096), one round
+// of them, shorten that delay (8192 -> 3072 at T = 4096: 88 items as 176
+// parts, 0.34 ms less per 28-layer step), while shorter parts do not shrink
+// with their token count (fixed cost of about 5 us, and many parts at
+// different token offsets lose the DRAM row locality whole items share).
 void side_split(int64_t T, int64_t d_in, int64_t d_out, int64_t r, Dtype dt, int *tparts, int *tchunk) {
   constexpr int64_t STEP = 8 * SideShape<BF16>::ROWS;  // one step of each virtual wave
   *tparts = 1;
@@ -35,8 +44,9 @@ void side_split(int64_t T, int64_t d_in, int64_t d_out, int64_t r, Dtype dt, int
   gemm_tile_shape((int)T, (int)d_in, true, true, dt, &bm, &bn);
   const int64_t tiles = ((T + bm - 1) / bm) * ((d_in + bn - 1) / bn);
   const int64_t items = side_item_count(d_in, d_out, r, dt);
-  if (tiles >= 256 || items < 1) return;
-  int64_t p = std::min<int64_t>({4, T / STEP, (256 - tiles) / items});
+  if (items < 1 || (tiles >= 256 && T < 4096)) return;
+  int64_t p = tiles >= 256 ? std::min<int64_t>({8, T / STEP, 256 / items})
+                           : std::min<int64_t>({4, T / STEP, (256 - tiles) / items});
   // The part tiles stay within an eighth of the fp32 dW the method never forms.
   while (p > 1 && items * p * SIDE_SLOT_FLOATS * 4 > d_in * d_out / 2) --p;
   if (p <= 1) return;

@@ -53,8 +53,9 @@ constexpr int SIDE_SLOT_FLOATS = 4096;  // a part's tile: 64 values per lane of 
 // Side items of a backward with reduction lengths d_in (dA) and d_out (dB).
 int side_item_count(int64_t d_in, int64_t d_out, int64_t r, Dtype dt);
 // Token parts per side item of the unfused dx launch, and tokens per part:
-// more than one only where the launch's tiles leave CUs idle (fewer than 256
-// tiles) and the parts fit on them (bf16; fp32: one part).
+// more than one where the launch's tiles leave CUs idle (fewer than 256
+// tiles) and the parts fit on them, or, from 4096 tokens, one round of parts
+// ahead of tiles that fill the CUs (bf16; fp32: one part).
 void side_split(int64_t T, int64_t d_in, int64_t d_out, int64_t r, Dtype dt, int *tparts, int *tchunk);
 
 // C[M, N] = sum_k Aop[m][k] Bop[n][k]  (+ LoRA step), rounded to the element type.
