@@ -32,9 +32,10 @@ int side_item_count(int64_t d_in, int64_t d_out, int64_t r, Dtype dt) {
 // them.  Where the tiles fill the CUs, the items delay as many tiles by
 // their own duration; parts of at least 2048 tokens (T >= 4096), one round
 // of them, shorten that delay (8192 -> 3072 at T = 4096: 88 items as 176
-// parts, 0.34 ms less per 28-layer step), while shorter parts do not shrink
-// with their token count (fixed cost of about 5 us, and many parts at
-// different token offsets lose the DRAM row locality whole items share).
+// parts, 0.34 ms less per 28-layer step), while shorter parts were measured
+// not to shrink with their token count (512-token parts of a 2048-token item
+// took 10 - 17 us against 19.5 us for the whole item; about 5 us of it is a
+// part's fixed cost: load ramp, LDS tree).
 void side_split(int64_t T, int64_t d_in, int64_t d_out, int64_t r, Dtype dt, int *tparts, int *tchunk) {
   constexpr int64_t STEP = 8 * SideShape<BF16>::ROWS;  // one step of each virtual wave
   *tparts = 1;
