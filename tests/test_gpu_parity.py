@@ -346,11 +346,13 @@ def test_bwd_without_dx_matches(orc):
 # tokens), three parts (T = 1500), r = 32 (the Llama k / v case, also at full
 # size in test_full_llama_stack_layer), and three parts of 1536 + 1536 + 1028
 # tokens ahead of tiles that fill the CUs (T = 4100; the Llama down_proj case
-# at full size in test_full_llama_stack_layer).  dA and dB in full, sampled dx; then a
+# at full size in test_full_llama_stack_layer), and two rank groups (r = 40:
+# 32 + 8 rank indices) in two parts.  dA and dB in full, sampled dx; then a
 # second call (the counts start from zero again) and one without dx, both
 # bitwise equal to the first.
 @pytest.mark.parametrize("shape,parts", [((1000, 1544, 1032, 12), 2), ((1500, 1544, 2056, 12), 3),
-                                         ((2000, 1544, 1032, 32), 2), ((4100, 4104, 1032, 16), 3)])
+                                         ((2000, 1544, 1032, 32), 2), ((4100, 4104, 1032, 16), 3),
+                                         ((4096, 4096, 4096, 40), 2)])
 def test_side_items_in_token_parts(orc, shape, parts):
     T, K, N, r = shape
     assert lm.lora_linear_plan(T, K, N, r)["bwd_side_parts"] == parts
