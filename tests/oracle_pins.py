@@ -21,9 +21,20 @@ The frozen LM head's reduced-vocabulary cross entropy with logits masking
 """
 from __future__ import annotations
 
+import json
+import os
+
 import numpy as np
 
 TIGHT = 1e-12
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def _golden(name):
+    """A hand-worked example from tests/golden (inputs, expected values, the
+    passage that defines the operation and the derivation)."""
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
 
 
 def _rng(seed):
@@ -52,40 +63,17 @@ def _full(o, c, s):
     return U, Y, bw
 
 
-def pin_scalar_closed_form(o):
-    """1x1x1 rank-1 case worked by hand: x=2, W=3, A=5, B=7, s=0.5, dy=11."""
-    X, W, A, B, dY, s = [[2.0]], [[3.0]], [[5.0]], [[7.0]], [[11.0]], 0.5
-    U, Y = o.forward(np.array(X), np.array(W), np.array(A), np.array(B), s)
-    bw = o.backward(np.array(X), np.array(W), np.array(A), np.array(B), np.array(dY), s, U=U)
-    assert U[0, 0] == 2.0 * 5.0
-    assert Y[0, 0] == 2.0 * 3.0 + 0.5 * (2.0 * 5.0) * 7.0          # 41
-    assert bw["G"][0, 0] == 11.0 * 7.0                              # 77
-    assert bw["dU"][0, 0] == 0.5 * 11.0 * 7.0                       # 38.5
-    assert bw["dX"][0, 0] == 11.0 * 3.0 + (0.5 * 11.0 * 7.0) * 5.0  # 225.5
-    assert bw["dA"][0, 0] == (0.5 * 11.0 * 7.0) * 2.0               # 77
-    assert bw["dB"][0, 0] == 0.5 * 11.0 * (2.0 * 5.0)               # 55
-
-
-def pin_small_closed_form(o):
-    """Hand-worked 1x2 -> 3 example with distinct entries, so a transposed or
-    mis-indexed operand changes the answer (T=1, K=2, N=3, r=1, s=2)."""
-    X = np.array([[1.0, 2.0]])
-    W = np.array([[1.0, 2.0], [3.0, 4.0], [5.0, 6.0]])   # rows are output features
-    A = np.array([[1.0, -1.0]])                          # U = 1 - 2 = -1
-    B = np.array([[1.0], [0.0], [2.0]])
-    dY = np.array([[1.0, 10.0, 100.0]])
-    s = 2.0
-    U, Y = o.forward(X, W, A, B, s)
-    assert U.tolist() == [[-1.0]]
-    # base: [1+4, 3+8, 5+12] = [5, 11, 17]; lora: s*U*B^T = -2*[1, 0, 2]
-    assert Y.tolist() == [[3.0, 11.0, 13.0]]
-    bw = o.backward(X, W, A, B, dY, s, U=U)
-    assert bw["G"].tolist() == [[1.0 + 0.0 + 200.0]]       # dY B = 201
-    assert bw["dU"].tolist() == [[402.0]]
-    # dY W = [1+30+500, 2+40+600] = [531, 642]; dU A = 402*[1, -1]
-    assert bw["dX"].tolist() == [[933.0, 240.0]]
-    assert bw["dA"].tolist() == [[402.0, 804.0]]            # dU^T X
-    assert bw["dB"].tolist() == [[-2.0], [-20.0], [-200.0]]  # s dY^T U
+def pin_lora_worked_examples(o):
+    """Hand-worked LoRA forward and backward (golden/lora_closed_form.json): a
+    1x1x1 rank-1 case and a 1x2 -> 3 case with distinct entries, so that a
+    transposed or mis-indexed operand changes the answer.  Exact in fp64."""
+    for c in _golden("lora_closed_form.json")["cases"]:
+        X, W, A, B, dY = (np.array(c[k], np.float64) for k in ("X", "W", "A", "B", "dY"))
+        U, Y = o.forward(X, W, A, B, c["s"])
+        bw = o.backward(X, W, A, B, dY, c["s"], U=U)
+        got = {"U": U, "Y": Y, "G": bw["G"], "dU": bw["dU"], "dX": bw["dX"], "dA": bw["dA"], "dB": bw["dB"]}
+        for k, v in c["expect"].items():
+            assert got[k].tolist() == v, (c["name"], k, got[k].tolist(), v)
 
 
 def pin_rank0_textbook_gemm(o):
@@ -253,21 +241,19 @@ def pin_torch_autograd(o):
 
 # --- dequantization of a quantized frozen base (W = s W_q + b per group) --------
 def pin_dequant_worked_example(o):
-    """Codes and parameters worked by hand.  4-bit, one row, K = 32, G = 16:
-    byte 0 = 0x5A holds k=0 -> 0xA = 10 (low nibble) and k=1 -> 5; byte 1 = 0x01
-    holds k=2 -> 1 and k=3 -> 0; byte 8 = 0xF3 (first byte of group 1) holds
-    k=16 -> 3 and k=17 -> 15.  Group 0 has s=0.5, b=-1; group 1 s=2, b=3."""
-    Wq = np.zeros((1, 16), np.uint8)
-    Wq[0, 0], Wq[0, 1], Wq[0, 8] = 0x5A, 0x01, 0xF3
-    W = o.dequant(Wq, np.array([[0.5, 2.0]]), np.array([[-1.0, 3.0]]), 4, 16)
-    assert W.shape == (1, 32)
-    assert list(W[0, :4]) == [4.0, 1.5, -0.5, -1.0]
-    assert W[0, 15] == -1.0                      # code 0 in group 0: the offset
-    assert list(W[0, 16:19]) == [9.0, 33.0, 3.0]
-    # 8-bit: one code per byte, K = 4, G = 2
-    W8 = o.dequant(np.array([[200, 7, 255, 0]], np.uint8), np.array([[0.25, -1.0]]),
-                   np.array([[1.0, 0.5]]), 8, 2)
-    assert list(W8[0]) == [51.0, 2.75, -254.5, 0.5]
+    """Codes and parameters worked by hand (golden/dequant_worked_example.json):
+    4-bit codes two per byte across two groups, and 8-bit codes."""
+    c4, c8 = _golden("dequant_worked_example.json")["cases"]
+    Wq = np.zeros((1, c4["nbytes"]), np.uint8)
+    for b, v in c4["bytes"].items():
+        Wq[0, int(b)] = v
+    W = o.dequant(Wq, np.array(c4["scale"]), np.array(c4["offset"]), c4["bits"], c4["group"])
+    assert W.shape == (1, c4["K"])
+    for k, v in c4["expect"].items():
+        assert W[0, int(k)] == v, (k, W[0, int(k)], v)
+    W8 = o.dequant(np.array([c8["codes"]], np.uint8), np.array(c8["scale"]), np.array(c8["offset"]),
+                   c8["bits"], c8["group"])
+    assert list(W8[0]) == c8["expect_row"]
 
 
 def pin_dequant_unit_scale_is_the_codes(o):
@@ -299,21 +285,14 @@ def pin_dequant_groups(o):
 
 # --- reduced-vocabulary LM head cross entropy with logits masking --------------
 def pin_ce_worked_example(o):
-    """Hand-worked: D = 1, vocabulary embeddings w = (1, 0, -1), hidden states
-    h = 1 (target token 0) and h = 2 (target token 2).  Position 1 has
-    logits (2, 0, -2): loss = log(e^2 + 1 + e^-2) + 2 and
-    dh = (e^2 - e^-2) / (e^2 + 1 + e^-2) + 1 (its target embedding is -1);
-    position 0 likewise with logits (1, 0, -1)."""
-    import math
-    H = np.array([[1.0], [2.0]])
-    W = np.array([[1.0], [0.0], [-1.0]])
-    loss, dH = o.ce_reduced(H, W, [0, 1], [0, 1, 2], [0, 2])
-    z0 = math.e + 1.0 + 1.0 / math.e
-    z1 = math.e ** 2 + 1.0 + math.e ** -2
-    assert abs(loss[0] - (math.log(z0) - 1.0)) < 1e-14
-    assert abs(loss[1] - (math.log(z1) + 2.0)) < 1e-14
-    assert abs(dH[0, 0] - ((math.e - 1.0 / math.e) / z0 - 1.0)) < 1e-14
-    assert abs(dH[1, 0] - ((math.e ** 2 - math.e ** -2) / z1 + 1.0)) < 1e-14
+    """Hand-worked reduced-vocabulary cross entropy and dh
+    (golden/ce_worked_example.json): D = 1, embeddings (1, 0, -1), hidden
+    states 1 and 2 with targets 0 and 2."""
+    c = _golden("ce_worked_example.json")
+    loss, dH = o.ce_reduced(np.array(c["H"]), np.array(c["W"]), c["rows"], c["cols"], c["targets"])
+    tol = c["tolerance"]
+    assert np.abs(np.asarray(loss) - np.array(c["expect"]["loss"])).max() < tol
+    assert np.abs(np.asarray(dH) - np.array(c["expect"]["dH"])).max() < tol
 
 
 def _torch_ce(H, W, cols, rows, targets_local):
@@ -405,14 +384,14 @@ def pin_reduced_vocab_union(o):
 
 # --- top-k similarity table ------------------------------------------------------
 def pin_topk_table_worked_example(o):
-    """Four 2-d embeddings at angles 0, 30, 90 and 180 degrees (scaled
-    differently: the table depends on directions only)."""
-    import math
-    W = np.array([[2.0, 0.0], [math.sqrt(3), 1.0], [0.0, 5.0], [-1.0, 0.0]])
-    A, C = o.topk_table(W, 4)
-    assert [list(r) for r in A] == [[0, 1, 2, 3], [1, 0, 2, 3], [2, 1, 0, 3], [3, 2, 1, 0]]
-    assert abs(C[0, 1] - math.cos(math.pi / 6)) < 1e-14 and abs(C[1, 2] - 0.5) < 1e-14
-    assert C[3, 3] == -1.0 and C[0, 2] == 0.0 and C[2, 2] == 0.0
+    """Four 2-d embeddings at angles 0, 30, 90 and 180 degrees, scaled
+    differently (the table depends on directions only):
+    golden/topk_worked_example.json."""
+    c = _golden("topk_worked_example.json")
+    A, C = o.topk_table(np.array(c["W"]), c["k"])
+    assert [list(r) for r in A] == c["expect_table"]
+    for i, m, v in c["expect_cos"]:
+        assert abs(C[i, m] - v) < c["tolerance"], (i, m, C[i, m], v)
 
 
 def pin_topk_table_is_argsort(o):
@@ -492,7 +471,7 @@ def pin_chain_of_one_is_one_layer(o):
 
 
 ALL_PINS = [
-    pin_scalar_closed_form, pin_small_closed_form, pin_rank0_textbook_gemm,
+    pin_lora_worked_examples, pin_rank0_textbook_gemm,
     pin_down_projection_gemm, pin_finite_differences, pin_dense_identities,
     pin_zero_B, pin_zero_A, pin_zero_W, pin_linear_in_scale,
     pin_token_split_additivity, pin_row_permutation, pin_row_sampling,
